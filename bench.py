@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Throughput of the joint-evaluation forward pass on one MI355X.
+
+A step is one pass of all five C-ABI calls (context encoding, distinct-item encoding, assembly,
+sequence + cross-sequence encoding, scoring + argmax) over one batch of synthetic requests whose
+inputs are already resident in HBM.  The default workload is the RecSys base batch (B=64
+requests, T=256 context rows, d=128, 4 heads, 2 layers per module, pool M=200, K=50 lists of
+L=10); `--workload 2 --K k` runs the K sweep on the same shapes.
+
+Prints one JSON line:  lists/s over the timed steps, p50/p90 step latency, the roofline of the
+dominant kernel family (from HIP events around each launch in a second, traced pass over the
+same steps), per-family kernel times, MFMA utilisation of the matrix-product stages, the HBM
+fraction of the assembly kernel, and the CPU oracle timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "candidate lists scored/sec at K=50 (B=64,L=10); MFMA util %; p50 latency"
+PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12     # dense bf16 matrix-core peak, 2516.6 TFLOP/s
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def algorithmic_work(c, U):
+    """Per-step algorithmic flops per kernel family and bytes of the assembly, from the shapes.
+
+    U is the list of distinct-item counts of the B requests.  Projection flops: an encoder block
+    over R rows costs 24 R d^2 (q|k|v 6, output 2, FFN 16 with F = 4d); an item block 28 U d^2;
+    the key/value cache 4 n T d^2.  Attention flops: 4 nq nk d per block.
+    """
+    d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
+    enc = lambda R: R * d * d * (2 * 3 + 2) + 4.0 * R * d * F   # noqa: E731
+    gemm = 0.0
+    gemm += n * B * enc(T) + 4.0 * n * B * T * d * d
+    gemm += sum(n * (u * d * d * (2 * 3 + 2 + 2 + 2) + 4.0 * u * d * F) for u in U)
+    gemm += n * B * enc(K * S)
+    gemm += n * B * enc(K)
+    attn = 4.0 * n * B * T * T * d
+    attn += sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U)
+    attn += 4.0 * n * B * K * S * S * d
+    attn += 4.0 * n * B * K * K * d
+    esz = 2 if c.dtype == "bf16" else 4
+    asm_bytes = B * K * S * d * esz + sum(U) * d * esz + B * K * c.L * 4
+    return {"gemm": gemm, "attention": attn}, asm_bytes
+
+
+def cpu_baseline(c, W, I, seconds: float):
+    """The float64 oracle, in its candidate-factorised order, on this host for a bounded time.
+
+    Whole lists of request 0 are evaluated one after another (context re-encoded for the list,
+    the item set re-encoded for each of its L occurrences, then SeqEnc) until `seconds` have
+    passed; lists/s is the count over the elapsed time.  The cross-sequence module and head,
+    which the oracle runs once per request over all K lists, are not part of the sample.
+    """
+    import numpy as np
+    import oracle
+    ev = oracle.evaluator
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    req = {k: (None if v is None else v[:1]) for k, v in I.items()}
+    lists_b = np.asarray(req["lists"][0])
+    done, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < seconds and done < c.K:
+        k = done
+        _, kv = ev.encode_context(c, W, ev.context_rows(c, W, req, 0))
+        rows = np.empty((c.L, c.d))
+        for j in range(c.L):
+            uniq, _ = ev.distinct_items(lists_b)
+            H = ev.encode_items(c, W, ev.item_rows(c, W, req, 0, uniq), kv)
+            rows[j] = H[int(np.searchsorted(uniq, lists_b[k, j]))]
+        ev.encode_sequence(c, W, ev.assemble_one(W, rows))
+        done += 1
+    dt = time.perf_counter() - t0
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": round(done / dt, 3), "unit": "lists/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {done} lists of request 0 (float64 numpy, candidate-factorised order: context "
+                      f"re-encoded per list, item set re-encoded per occurrence) in {dt:.1f} s on {cpu}"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=1, choices=[1, 2, 3, 4])
+    ap.add_argument("--K", type=int, default=None, help="lists per request for workload 2")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-trace", action="store_true", help="skip the traced pass (for profiler runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the joint pass shards over independent requests; "
+              f"see DESIGN.md); got --gpus {args.gpus}", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import gen
+    from paper_2603_02565_amd import flasheval as fe
+
+    if not torch.cuda.is_available():
+        print("bench.py needs an MI355X", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    c = gen.config(args.workload, K=args.K) if args.workload == 2 else gen.config(args.workload)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = fe.Evaluator(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, c.dtype, W)
+    bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
+    act = torch.bfloat16 if c.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    x = None if I["x"] is None else torch.from_numpy(I["x"]).to(dev).to(act)
+    pool = None if I["pool"] is None else torch.from_numpy(I["pool"]).to(dev).to(act)
+    ids = None if I["ctx_ids"] is None else torch.from_numpy(I["ctx_ids"]).to(dev)
+    lists = torch.from_numpy(I["lists"]).to(dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        ev.run(x=x, ctx_ids=ids, pool=pool, lists=lists)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: K whole passes, an event between consecutive passes
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for i in range(args.steps):
+        step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    total_ms = evs[0].elapsed_time(evs[-1])
+    ms_per_step = total_ms / args.steps
+    lists_per_s = c.B * c.K / (ms_per_step / 1e3)
+
+    U = bufs["n_uniq"].cpu().numpy().tolist()
+    flops, asm_bytes = algorithmic_work(c, U)
+
+    # ---- kernel-timing region: the same steps with HIP events around every launch
+    fam = {}
+    if not args.no_trace:
+        fe.fe_trace_enable(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        fam = fe.fe_trace_read()
+        fe.fe_trace_enable(False)
+
+    out = {
+        "metric": METRIC, "value": round(lists_per_s, 1), "unit": "lists/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": c.dtype,
+        "data": "synthetic (seeded; random-init weights)",
+        "config": {"workload": f"{c.name}: B={c.B} T={c.T} d={c.d} heads={c.n_heads} layers={c.n_layers} "
+                               f"F={c.ffn} M={c.M} K={c.K} L={c.L}",
+                   "B": c.B, "T": c.T, "d": c.d, "M": c.M, "K": c.K, "L": c.L, "parallelism": "none (1 GPU)"},
+        "p50_ms": round(float(np.percentile(per_step, 50)), 5),
+        "p90_ms": round(float(np.percentile(per_step, 90)), 5),
+        "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "U_mean": round(float(np.mean(U)), 2), "rho": round(c.K * c.L / float(np.mean(U)), 3),
+    }
+    if fam:
+        stages = {}
+        for name, (ms, n) in fam.items():
+            if n == 0:
+                continue
+            stages[name] = {"ms_per_step": round(ms / args.steps, 5), "launches_per_step": n // args.steps,
+                            "avg_launch_us": round(ms * 1e3 / n, 3)}
+        peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
+        for name in ("gemm", "attention"):
+            if name in stages:
+                tf = flops[name] / (fam[name][0] / args.steps / 1e3) / 1e12
+                stages[name].update(tflops=round(tf, 2), mfma_frac=round(tf / peak, 4))
+        if "assemble" in stages:
+            gbs = asm_bytes / (fam["assemble"][0] / args.steps / 1e3) / 1e9
+            stages["assemble"].update(GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
+        dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
+        dom_ms, dom_n = fam[dom]
+        avg_s = dom_ms / dom_n / 1e3
+        if dom in flops:
+            per_launch = flops[dom] / (dom_n / args.steps)
+            ach = per_launch / avg_s / 1e12
+            out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1),
+                               "unit": "TFLOP/s", "frac": round(ach / peak, 4), "traffic": None,
+                               "avg_launch_us": round(avg_s * 1e6, 3), "launches_per_step": dom_n // args.steps}
+        else:
+            per_launch = asm_bytes
+            ach = per_launch / avg_s / 1e9
+            out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                               "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                               "avg_launch_us": round(avg_s * 1e6, 3), "launches_per_step": dom_n // args.steps}
+        mm_ms = sum(fam[k][0] for k in ("gemm", "attention") if k in fam) / args.steps
+        out["mfma_util_matrix_stages"] = round((flops["gemm"] + flops["attention"]) / (mm_ms / 1e3) / 1e12 / peak, 4)
+        out["kernel_ms_per_step"] = round(sum(v[0] for v in fam.values()) / args.steps, 5)
+        out["stages"] = stages
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(c, W, I, args.cpu_seconds)
+    ev.close()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,748 @@
+// C ABI of libflasheval: argument validation, weight packing, workspace layout and the launch
+// sequence of each stage.  All device work is in the kernels of gemm.hip, attention.hip and
+// index.hip; this file only enqueues them.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "fe_common.h"
+#include "flasheval.h"
+#include "flasheval_trace.h"
+
+#include <mutex>
+
+namespace {
+
+thread_local std::string g_err;
+
+// ------------------------------------------------------------------------------------------
+// Kernel timing (flasheval_trace.h): events recorded around each launch while enabled.
+// ------------------------------------------------------------------------------------------
+enum Fam { F_GEMM = 0, F_ATTN, F_LN, F_DEDUP, F_GATHER, F_ASSEMBLE, F_SCORE, F_FILL, F_FFN };
+const char* const kFamName[FE_TRACE_FAMILIES] = {"gemm", "attention", "layernorm", "dedup", "gather",
+                                                 "assemble", "score_select", "fill", "ffn"};
+struct TraceRec { int fam; hipEvent_t a, b; };
+std::mutex g_trace_mu;
+bool g_trace_on = false;
+std::vector<TraceRec> g_trace;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t take_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+hipError_t traced(int fam, hipStream_t s, F&& launch) {
+  if (!g_trace_on) return launch();
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  hipEvent_t a = take_event(), b = take_event();
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, s);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, s);
+  if (e != hipSuccess) return e;
+  g_trace.push_back({fam, a, b});
+  return hipSuccess;
+}
+
+#define FE_LAUNCH(fam, stream, call) FE_HIP(traced(fam, stream, [&] { return (call); }))
+
+fe_status fail(fe_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define FE_HIP(call)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (call);                                                           \
+    if (e_ != hipSuccess) return fail(FE_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+struct EncW {
+  const float *ln1g, *ln1b;
+  const void* wqkv;
+  const float* bqkv;
+  const void* wo;
+  const float* bo;
+  const float *ln2g, *ln2b;
+  const void* w1;
+  const float* b1;
+  const void* w2;
+  const float* b2;
+};
+
+struct ItemW {
+  const float *ln1g, *ln1b;
+  const void* wqkv;
+  const float* bqkv;
+  const void* wo;
+  const float* bo;
+  const float *ln2g, *ln2b;
+  const void* wq;
+  const float* bq;
+  const void* wo2;
+  const float* bo2;
+  const float *ln3g, *ln3b;
+  const void* w1;
+  const float* b1;
+  const void* w2;
+  const float* b2;
+};
+
+}  // namespace
+
+struct fe_model {
+  fe_config cfg;
+  bool bf16;
+  int device;
+  void* dev = nullptr;
+  std::vector<EncW> ctx, seq, cross;
+  std::vector<ItemW> item;
+  const float *ctx_lnf_g, *ctx_lnf_b, *item_lnf_g, *item_lnf_b, *seq_lnf_g, *seq_lnf_b, *cross_lnf_g, *cross_lnf_b;
+  const void* wkv;    // [2n*d][d]: rows of block (l, 0) = wk_l^T, block (l, 1) = wv_l^T
+  const float* bkv;   // [2n*d]
+  const void* cls;
+  const void* pos;
+  const float* head_w;
+  const float* head_b;
+  const void* emb;
+};
+
+namespace {
+
+// ------------------------------------------------------------------------------------------
+// Parameter walk shared by fe_param_count and fe_model_create (host side only).
+// ------------------------------------------------------------------------------------------
+struct Packer {
+  const float* src = nullptr;  // null: count only
+  size_t consumed = 0;
+  bool bf16 = false;
+  std::vector<unsigned char> image;
+
+  size_t place(size_t bytes) {
+    size_t off = (image.size() + 255) & ~size_t(255);
+    image.resize(off + bytes);
+    return off;
+  }
+  static uint16_t to_bf16(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+  }
+  // fp32 vector of n values
+  size_t vec(size_t n) {
+    const float* p = src + consumed;
+    consumed += n;
+    if (!src) return 0;
+    size_t off = place(n * 4);
+    std::memcpy(&image[off], p, n * 4);
+    return off;
+  }
+  // act-type copy of n values in source order
+  size_t act(size_t n) {
+    const float* p = src + consumed;
+    consumed += n;
+    if (!src) return 0;
+    size_t off = place(n * (bf16 ? 2 : 4));
+    if (bf16) {
+      uint16_t* dst = reinterpret_cast<uint16_t*>(&image[off]);
+      for (size_t i = 0; i < n; ++i) dst[i] = to_bf16(p[i]);
+    } else {
+      std::memcpy(&image[off], p, n * 4);
+    }
+    return off;
+  }
+  // matrix [in][out] -> device layout at byte offset `off`:
+  //   fp32 models: transposed, Wt[out][in];
+  //   bf16 models: the B-operand fragments of v_mfma_f32_32x32x16_bf16, so that one wave reads
+  //   the operand of one instruction as 64 lanes x 16 contiguous bytes.  Block (nb, ks) holds
+  //   output columns 32nb..32nb+31 and inputs 16ks..16ks+15; lane l of the block holds
+  //   W[16ks + 8(l/32) + j][32nb + l%32] for j = 0..7.  Blocks are ordered nb-major, ks-minor.
+  void mat_into(size_t off, size_t in, size_t out) {
+    const float* p = src + consumed;
+    consumed += in * out;
+    if (!src) return;
+    if (bf16) {
+      uint16_t* dst = reinterpret_cast<uint16_t*>(&image[off]);
+      const size_t ksteps = in / 16;
+      for (size_t k = 0; k < in; ++k)
+        for (size_t n = 0; n < out; ++n) {
+          const size_t nb = n / 32, ks = k / 16, lane = ((k % 16) / 8) * 32 + n % 32, j = k % 8;
+          dst[((nb * ksteps + ks) * 64 + lane) * 8 + j] = to_bf16(p[k * out + n]);
+        }
+    } else {
+      for (size_t o = 0; o < out; ++o)
+        for (size_t i = 0; i < in; ++i) reinterpret_cast<float*>(&image[off])[o * in + i] = p[i * out + o];
+    }
+  }
+  size_t mat(size_t in, size_t out) {
+    size_t off = src ? place(in * out * (bf16 ? 2 : 4)) : 0;
+    mat_into(off, in, out);
+    return off;
+  }
+  void vec_into(size_t off, size_t n) {
+    const float* p = src + consumed;
+    consumed += n;
+    if (src) std::memcpy(&image[off], p, n * 4);
+  }
+};
+
+struct EncOff { size_t ln1g, ln1b, wqkv, bqkv, wo, bo, ln2g, ln2b, w1, b1, w2, b2; };
+struct ItemOff { size_t ln1g, ln1b, wqkv, bqkv, wo, bo, ln2g, ln2b, wq, bq, wo2, bo2, ln3g, ln3b, w1, b1, w2, b2; };
+struct Offsets {
+  std::vector<EncOff> ctx, seq, cross;
+  std::vector<ItemOff> item;
+  size_t ctx_lnf_g, ctx_lnf_b, item_lnf_g, item_lnf_b, seq_lnf_g, seq_lnf_b, cross_lnf_g, cross_lnf_b;
+  size_t wkv, bkv, cls, pos, head_w, head_b, emb;
+};
+
+EncOff pack_enc(Packer& P, size_t d, size_t F) {
+  EncOff o;
+  o.ln1g = P.vec(d); o.ln1b = P.vec(d);
+  o.wqkv = P.mat(d, 3 * d); o.bqkv = P.vec(3 * d);
+  o.wo = P.mat(d, d); o.bo = P.vec(d);
+  o.ln2g = P.vec(d); o.ln2b = P.vec(d);
+  o.w1 = P.mat(d, F); o.b1 = P.vec(F);
+  o.w2 = P.mat(F, d); o.b2 = P.vec(d);
+  return o;
+}
+
+Offsets pack_all(Packer& P, const fe_config& c) {
+  const size_t d = c.d, F = c.ffn_dim, n = c.n_layers;
+  const size_t esz = P.bf16 ? 2 : 4;
+  Offsets O;
+  for (size_t l = 0; l < n; ++l) O.ctx.push_back(pack_enc(P, d, F));
+  O.ctx_lnf_g = P.vec(d); O.ctx_lnf_b = P.vec(d);
+  O.wkv = P.src ? P.place(2 * n * d * d * esz) : 0;
+  O.bkv = P.src ? P.place(2 * n * d * 4) : 0;
+  for (size_t l = 0; l < n; ++l) {
+    P.mat_into(O.wkv + (2 * l) * d * d * esz, d, d);
+    P.vec_into(O.bkv + (2 * l) * d * 4, d);
+    P.mat_into(O.wkv + (2 * l + 1) * d * d * esz, d, d);
+    P.vec_into(O.bkv + (2 * l + 1) * d * 4, d);
+  }
+  for (size_t l = 0; l < n; ++l) {
+    ItemOff o;
+    o.ln1g = P.vec(d); o.ln1b = P.vec(d);
+    o.wqkv = P.mat(d, 3 * d); o.bqkv = P.vec(3 * d);
+    o.wo = P.mat(d, d); o.bo = P.vec(d);
+    o.ln2g = P.vec(d); o.ln2b = P.vec(d);
+    o.wq = P.mat(d, d); o.bq = P.vec(d);
+    o.wo2 = P.mat(d, d); o.bo2 = P.vec(d);
+    o.ln3g = P.vec(d); o.ln3b = P.vec(d);
+    o.w1 = P.mat(d, F); o.b1 = P.vec(F);
+    o.w2 = P.mat(F, d); o.b2 = P.vec(d);
+    O.item.push_back(o);
+  }
+  O.item_lnf_g = P.vec(d); O.item_lnf_b = P.vec(d);
+  for (size_t l = 0; l < n; ++l) O.seq.push_back(pack_enc(P, d, F));
+  O.seq_lnf_g = P.vec(d); O.seq_lnf_b = P.vec(d);
+  for (size_t l = 0; l < n; ++l) O.cross.push_back(pack_enc(P, d, F));
+  O.cross_lnf_g = P.vec(d); O.cross_lnf_b = P.vec(d);
+  O.cls = P.act(d);
+  O.pos = P.act((size_t)(c.max_L + 1) * d);
+  O.head_w = P.vec(d);
+  O.head_b = P.vec(1);
+  O.emb = c.vocab > 0 ? P.act((size_t)c.vocab * d) : 0;
+  return O;
+}
+
+fe_status check_config(const fe_config* c) {
+  if (!c) return fail(FE_EINVAL, "config is NULL");
+  if (c->dtype != FE_F32 && c->dtype != FE_BF16) return fail(FE_EINVAL, "dtype %d is not FE_F32 or FE_BF16", c->dtype);
+  if (c->d <= 0 || c->n_heads <= 0 || c->n_layers <= 0 || c->ffn_dim <= 0 || c->max_L <= 0 || c->vocab < 0)
+    return fail(FE_EINVAL, "config sizes must be positive");
+  if (c->d % c->n_heads) return fail(FE_EINVAL, "d=%d is not a multiple of n_heads=%d", c->d, c->n_heads);
+  const int dh = c->d / c->n_heads;
+  const bool bf = c->dtype == FE_BF16;
+  if (!(c->d == 32 || c->d == 64 || c->d == 128 || c->d == 256 || c->d == 512))
+    return fail(FE_EUNSUPPORTED, "d=%d not in {32,64,128,256,512}", c->d);
+  if (dh != 32 && dh != 64) return fail(FE_EUNSUPPORTED, "head width %d not in {32,64}", dh);
+  if (c->n_layers > 8) return fail(FE_EUNSUPPORTED, "n_layers=%d > 8", c->n_layers);
+  if (bf && c->d < 128) return fail(FE_EUNSUPPORTED, "bf16 models need d >= 128");
+  if (c->ffn_dim % (bf ? 128 : 32) || c->ffn_dim > 4096)
+    return fail(FE_EUNSUPPORTED, "ffn_dim=%d must be a multiple of %d and <= 4096", c->ffn_dim, bf ? 128 : 32);
+  if (c->max_L > 127) return fail(FE_EUNSUPPORTED, "max_L=%d > 127", c->max_L);
+  if (c->vocab > 131072) return fail(FE_EUNSUPPORTED, "vocab=%d > 131072", c->vocab);
+  return FE_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Workspace layout
+// ------------------------------------------------------------------------------------------
+struct Ws {
+  size_t status;                                        // int32 [2][B]: items, context
+  size_t c_xin, c_x, c_qkv, c_o, c_h;                   // context stage
+  size_t i_g0, i_g, i_qkv, i_o, i_q, i_h;               // item stage
+  size_t s_x, s_qkv, s_o, s_h, s_c;                     // sequence + cross stages
+  size_t total;
+};
+
+struct Bump {
+  size_t at;
+  size_t take(size_t bytes) {
+    size_t off = (at + 255) & ~size_t(255);
+    at = off + bytes;
+    return off;
+  }
+};
+
+Ws layout(const fe_model* m, long long B, long long T, long long M, long long K, long long L) {
+  const long long d = m->cfg.d, F = m->cfg.ffn_dim;
+  const size_t e = m->bf16 ? 2 : 4;
+  Ws w{};
+  Bump b0{0};
+  w.status = b0.take(2 * B * 4);
+  size_t base = b0.at, end = base;
+  {  // context
+    const long long R = B * T;
+    Bump b{base};
+    w.c_xin = b.take(R * d * e);
+    w.c_x = b.take(R * d * 4);
+    w.c_qkv = b.take(R * 3 * d * e);
+    w.c_o = b.take(R * d * e);
+    w.c_h = b.take(R * F * e);
+    end = std::max(end, b.at);
+  }
+  {  // items
+    const long long Ucap = std::min(M, K * L);
+    const long long R = B * Ucap;
+    Bump b{base};
+    w.i_g0 = b.take(R * d * e);
+    w.i_g = b.take(R * d * 4);
+    w.i_qkv = b.take(R * 3 * d * e);
+    w.i_o = b.take(R * d * e);
+    w.i_q = b.take(R * d * e);
+    w.i_h = b.take(R * F * e);
+    end = std::max(end, b.at);
+  }
+  {  // sequences (the cross module reuses these buffers; its rows B*K are fewer)
+    const long long R = B * K * (L + 1);
+    Bump b{base};
+    w.s_x = b.take(R * d * 4);
+    w.s_qkv = b.take(R * 3 * d * e);
+    w.s_o = b.take(R * d * e);
+    w.s_h = b.take(R * F * e);
+    w.s_c = b.take(B * K * d * 4);
+    end = std::max(end, b.at);
+  }
+  w.total = (end + 255) & ~size_t(255);
+  return w;
+}
+
+template <typename T> T* at(void* base, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(base) + off); }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+fe_status check_dims(const fe_model* m, long long B, long long T, long long M, long long K, long long L) {
+  if (!m) return fail(FE_EINVAL, "model is NULL");
+  if (B < 1 || T < 1 || M < 1 || K < 1 || L < 1) return fail(FE_EINVAL, "B, T, M, K, L must be >= 1");
+  if (L > m->cfg.max_L) return fail(FE_EINVAL, "L=%lld exceeds the model's max_L=%d", L, m->cfg.max_L);
+  if (T > 8192) return fail(FE_EUNSUPPORTED, "T=%lld > 8192", T);
+  if (K > 4096) return fail(FE_EUNSUPPORTED, "K=%lld > 4096", K);
+  if (M > 131072) return fail(FE_EUNSUPPORTED, "M=%lld > 131072", M);
+  const long long wide = std::max<long long>(3LL * m->cfg.d, m->cfg.ffn_dim);
+  const long long rows = std::max({B * T, B * std::min(M, K * L), B * K * (L + 1)});
+  if (rows * wide > INT_MAX || 2LL * m->cfg.n_layers * B * T * m->cfg.d > INT_MAX)
+    return fail(FE_EINVAL, "batch too large: element counts overflow int32");
+  return FE_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Blocks
+// ------------------------------------------------------------------------------------------
+GemmArgs gemm(const void* A, int lda, bool a_f32, int R, int K, int N, const void* Wt, const float* bias, void* C,
+              int ldc, bool c_f32, int epi) {
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.a_f32 = a_f32;
+  g.R = R; g.K = K; g.N = N;
+  g.Wt = Wt; g.bias = bias;
+  g.C = C; g.ldc = ldc; g.c_f32 = c_f32;
+  g.col_block = N; g.col_block_stride = 0;
+  g.epi = epi;
+  g.rows_per_batch = 1;
+  return g;
+}
+
+// One projection launch: packed-weight bf16 kernel or generic fp32 kernel.
+fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s);
+// X += FFN(LN(X)): fused on bf16 models, two generic launches through Hf on fp32 models.
+fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const float* lnb, const void* w1,
+                  const float* b1, const void* w2, const float* b2, void* Hf, const int32_t* nvalid, int rpb,
+                  hipStream_t s);
+
+struct Bufs {
+  float* X;      // fp32 residual stream [rows][d]
+  void* qkv;     // act [rows][3d]
+  void* O;       // act [rows][d]
+  void* Hf;      // act [rows][F]
+};
+
+// One pre-LN encoder block over nb batches of `per` rows; attention stays inside a batch.
+// `xin` is the block input (act or fp32); the output residual stream is written to b.X.
+fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const void* xin, bool xin_f32, const Bufs& b,
+                    const int32_t* nvalid, hipStream_t s) {
+  const int d = m->cfg.d, F = m->cfg.ffn_dim, R = nb * per;
+  const bool bf = m->bf16;
+  const size_t e = bf ? 2 : 4;
+  GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
+  g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
+  fe_status st0 = run_proj(m, g, s);
+  if (st0 != FE_OK) return st0;
+  AttnArgs a{};
+  a.Q = b.qkv; a.q_bs = (long long)per * 3 * d; a.q_rs = 3 * d;
+  a.K = static_cast<const char*>(b.qkv) + d * e; a.k_bs = a.q_bs; a.k_rs = 3 * d;
+  a.V = static_cast<const char*>(b.qkv) + 2 * d * e; a.v_bs = a.q_bs; a.v_rs = 3 * d;
+  a.O = b.O; a.o_bs = (long long)per * d; a.o_rs = d;
+  a.B = nb; a.nq = per; a.nk = per; a.n_heads = m->cfg.n_heads; a.dh = d / m->cfg.n_heads;
+  a.q_valid = nvalid; a.k_valid = nvalid;
+  a.scale = 1.0f / sqrtf((float)a.dh);
+  FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+  g = gemm(b.O, d, false, R, d, d, w.wo, w.bo, b.X, d, true, EPI_RESID);
+  g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = nvalid; g.rows_per_batch = per;
+  fe_status st = run_proj(m, g, s);
+  if (st != FE_OK) return st;
+  return run_ffn(m, b.X, R, w.ln2g, w.ln2b, w.w1, w.b1, w.w2, w.b2, b.Hf, nvalid, per, s);
+}
+
+fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s) {
+  if (m->bf16) FE_LAUNCH(F_GEMM, s, launch_proj(g, s));
+  else FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
+  return FE_OK;
+}
+
+fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const float* lnb, const void* w1,
+                  const float* b1, const void* w2, const float* b2, void* Hf, const int32_t* nvalid, int rpb,
+                  hipStream_t s) {
+  const int d = m->cfg.d, F = m->cfg.ffn_dim;
+  if (m->bf16) {
+    FfnArgs f{X, R, d, F, lng, lnb, w1, b1, w2, b2, nvalid, rpb};
+    FE_LAUNCH(F_FFN, s, launch_ffn(f, s));
+    return FE_OK;
+  }
+  GemmArgs g = gemm(X, d, true, R, d, F, w1, b1, Hf, F, false, EPI_RELU);
+  g.ln_g = lng; g.ln_b = lnb; g.nvalid = nvalid; g.rows_per_batch = rpb;
+  FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
+  g = gemm(Hf, F, false, R, F, d, w2, b2, X, d, true, EPI_RESID);
+  g.res = X; g.ldr = d; g.res_f32 = true; g.nvalid = nvalid; g.rows_per_batch = rpb;
+  FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
+  return FE_OK;
+}
+
+}  // namespace
+
+// ==========================================================================================
+// Exported functions
+// ==========================================================================================
+extern "C" {
+
+const char* fe_last_error(void) { return g_err.c_str(); }
+
+fe_status fe_trace_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  for (auto& r : g_trace) {
+    (void)hipEventSynchronize(r.b);
+    g_event_pool.push_back(r.a);
+    g_event_pool.push_back(r.b);
+  }
+  g_trace.clear();
+  g_trace_on = on != 0;
+  return FE_OK;
+}
+
+fe_status fe_trace_read(double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches) return fail(FE_EINVAL, "NULL output array");
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  for (int i = 0; i < FE_TRACE_FAMILIES; ++i) { total_ms[i] = 0.0; launches[i] = 0; }
+  fe_status st = FE_OK;
+  for (auto& r : g_trace) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess && st == FE_OK) st = fail(FE_EHIP, "trace event: %s", hipGetErrorString(e));
+    total_ms[r.fam] += ms;
+    launches[r.fam] += 1;
+    g_event_pool.push_back(r.a);
+    g_event_pool.push_back(r.b);
+  }
+  g_trace.clear();
+  return st;
+}
+
+const char* fe_trace_family(int i) { return (i >= 0 && i < FE_TRACE_FAMILIES) ? kFamName[i] : ""; }
+
+fe_status fe_param_count(const fe_config* cfg, size_t* n_floats) {
+  fe_status st = check_config(cfg);
+  if (st != FE_OK) return st;
+  if (!n_floats) return fail(FE_EINVAL, "n_floats is NULL");
+  Packer P;
+  pack_all(P, *cfg);
+  *n_floats = P.consumed;
+  return FE_OK;
+}
+
+fe_status fe_model_create(const fe_config* cfg, const float* params, size_t n_floats, fe_model** out) {
+  fe_status st = check_config(cfg);
+  if (st != FE_OK) return st;
+  if (!params || !out) return fail(FE_EINVAL, "params or out is NULL");
+  *out = nullptr;
+  size_t need = 0;
+  fe_param_count(cfg, &need);
+  if (n_floats != need) return fail(FE_EINVAL, "expected %zu parameter floats, got %zu", need, n_floats);
+  fe_model* m = new (std::nothrow) fe_model();
+  if (!m) return fail(FE_ENOMEM, "host allocation failed");
+  m->cfg = *cfg;
+  m->bf16 = cfg->dtype == FE_BF16;
+  if (hipGetDevice(&m->device) != hipSuccess) {
+    delete m;
+    return fail(FE_EHIP, "hipGetDevice failed");
+  }
+  Packer P;
+  P.src = params;
+  P.bf16 = m->bf16;
+  Offsets O = pack_all(P, *cfg);
+  hipError_t e = hipMalloc(&m->dev, P.image.size());
+  if (e != hipSuccess) {
+    delete m;
+    return fail(FE_ENOMEM, "hipMalloc(%zu) failed: %s", P.image.size(), hipGetErrorString(e));
+  }
+  e = hipMemcpy(m->dev, P.image.data(), P.image.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(m->dev);
+    delete m;
+    return fail(FE_EHIP, "hipMemcpy of weights failed: %s", hipGetErrorString(e));
+  }
+  char* base = static_cast<char*>(m->dev);
+  auto F = [&](size_t off) { return reinterpret_cast<const float*>(base + off); };
+  auto A = [&](size_t off) { return static_cast<const void*>(base + off); };
+  auto enc = [&](const EncOff& o) {
+    return EncW{F(o.ln1g), F(o.ln1b), A(o.wqkv), F(o.bqkv), A(o.wo), F(o.bo), F(o.ln2g), F(o.ln2b),
+                A(o.w1), F(o.b1), A(o.w2), F(o.b2)};
+  };
+  for (auto& o : O.ctx) m->ctx.push_back(enc(o));
+  for (auto& o : O.seq) m->seq.push_back(enc(o));
+  for (auto& o : O.cross) m->cross.push_back(enc(o));
+  for (auto& o : O.item)
+    m->item.push_back(ItemW{F(o.ln1g), F(o.ln1b), A(o.wqkv), F(o.bqkv), A(o.wo), F(o.bo), F(o.ln2g), F(o.ln2b),
+                            A(o.wq), F(o.bq), A(o.wo2), F(o.bo2), F(o.ln3g), F(o.ln3b), A(o.w1), F(o.b1),
+                            A(o.w2), F(o.b2)});
+  m->ctx_lnf_g = F(O.ctx_lnf_g); m->ctx_lnf_b = F(O.ctx_lnf_b);
+  m->item_lnf_g = F(O.item_lnf_g); m->item_lnf_b = F(O.item_lnf_b);
+  m->seq_lnf_g = F(O.seq_lnf_g); m->seq_lnf_b = F(O.seq_lnf_b);
+  m->cross_lnf_g = F(O.cross_lnf_g); m->cross_lnf_b = F(O.cross_lnf_b);
+  m->wkv = A(O.wkv); m->bkv = F(O.bkv);
+  m->cls = A(O.cls); m->pos = A(O.pos);
+  m->head_w = F(O.head_w); m->head_b = F(O.head_b);
+  m->emb = cfg->vocab > 0 ? A(O.emb) : nullptr;
+  *out = m;
+  return FE_OK;
+}
+
+void fe_model_destroy(fe_model* m) {
+  if (!m) return;
+  if (m->dev) (void)hipFree(m->dev);
+  delete m;
+}
+
+fe_status fe_workspace_size(const fe_model* m, int B, int T, int M, int K, int L, size_t* bytes) {
+  fe_status st = check_dims(m, B, T, M, K, L);
+  if (st != FE_OK) return st;
+  if (!bytes) return fail(FE_EINVAL, "bytes is NULL");
+  *bytes = layout(m, B, T, M, K, L).total;
+  return FE_OK;
+}
+
+fe_status fe_read_device_status(const fe_model* m, const void* ws, int B, void* stream, int32_t* host_out) {
+  if (!m || !ws || !host_out || B < 1) return fail(FE_EINVAL, "bad arguments to fe_read_device_status");
+  std::vector<int32_t> tmp(2 * (size_t)B);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  FE_HIP(hipMemcpyAsync(tmp.data(), ws, tmp.size() * 4, hipMemcpyDeviceToHost, s));
+  FE_HIP(hipStreamSynchronize(s));
+  for (int b = 0; b < B; ++b) host_out[b] = tmp[b] | tmp[B + b];
+  return FE_OK;
+}
+
+fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, const int32_t* ctx_ids, void* kv, void* ws,
+                            size_t ws_bytes, void* stream) {
+  fe_status st = check_dims(m, B, T, 1, 1, 1);
+  if (st != FE_OK) return st;
+  if ((x == nullptr) == (ctx_ids == nullptr)) return fail(FE_EINVAL, "give exactly one of x and ctx_ids");
+  if (ctx_ids && !m->emb) return fail(FE_EINVAL, "ctx_ids given but the model has no vocabulary");
+  if (!kv || !ws) return fail(FE_EINVAL, "kv or ws is NULL");
+  if (!aligned16(x) || !aligned16(ctx_ids) || !aligned16(kv) || !aligned16(ws))
+    return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const Ws w = layout(m, B, T, 1, 1, 1);
+  if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = m->bf16;
+  const int d = m->cfg.d, R = B * T;
+  int32_t* status_ctx = at<int32_t>(ws, w.status) + B;
+  FE_LAUNCH(F_FILL, s, launch_fill_i32(status_ctx, B, 0, s));
+  const void* src = x;
+  if (ctx_ids) {
+    FE_LAUNCH(F_GATHER, s, launch_gather_rows(m->emb, 0, m->cfg.vocab, ctx_ids, T, nullptr, B, T, d, at<char>(ws, w.c_xin), status_ctx,
+                              FE_DEV_BAD_TOKEN, bf, s));
+    src = at<char>(ws, w.c_xin);
+  }
+  Bufs b{at<float>(ws, w.c_x), at<char>(ws, w.c_qkv), at<char>(ws, w.c_o), at<char>(ws, w.c_h)};
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s);
+    if (st != FE_OK) return st;
+  }
+  // final LayerNorm of the context module fused into the key/value projections of all item layers
+  GemmArgs g = gemm(b.X, d, true, R, d, 2 * m->cfg.n_layers * d, m->wkv, m->bkv, kv, d, false, EPI_STORE);
+  g.ln_g = m->ctx_lnf_g; g.ln_b = m->ctx_lnf_b;
+  g.col_block = d; g.col_block_stride = (long long)R * d;
+  return run_proj(m, g, s);
+}
+
+fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, const int32_t* lists, int K, int L,
+                          const void* kv, int T, int32_t* uniq, int32_t* n_uniq, int32_t* slot, void* H, void* ws,
+                          size_t ws_bytes, void* stream) {
+  fe_status st = check_dims(m, B, T, M, K, L);
+  if (st != FE_OK) return st;
+  if (!pool && !m->emb) return fail(FE_EINVAL, "pool is NULL and the model has no vocabulary");
+  if (!pool && M != m->cfg.vocab) return fail(FE_EINVAL, "token-id items need M == vocab (%d)", m->cfg.vocab);
+  if (!lists || !kv || !uniq || !n_uniq || !slot || !H || !ws) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(pool) || !aligned16(lists) || !aligned16(kv) || !aligned16(H) || !aligned16(ws) ||
+      !aligned16(uniq) || !aligned16(slot))
+    return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const Ws w = layout(m, B, T, M, K, L);
+  if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = m->bf16;
+  const int d = m->cfg.d, F = m->cfg.ffn_dim, KL = K * L;
+  const int Ucap = std::min(M, KL);
+  const int R = B * Ucap;
+  const size_t e = bf ? 2 : 4;
+  int32_t* status_items = at<int32_t>(ws, w.status);
+  FE_LAUNCH(F_DEDUP, s, launch_dedup(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, s));
+  const void* table = pool ? pool : m->emb;
+  const long long table_bs = pool ? (long long)M * d : 0;
+  void* G0 = at<char>(ws, w.i_g0);
+  FE_LAUNCH(F_GATHER, s, launch_gather_rows(table, table_bs, M, uniq, Ucap, n_uniq, B, Ucap, d, G0, nullptr, 0, bf, s));
+  float* G = at<float>(ws, w.i_g);
+  void* qkv = at<char>(ws, w.i_qkv);
+  void* O = at<char>(ws, w.i_o);
+  void* Qc = at<char>(ws, w.i_q);
+  void* Hf = at<char>(ws, w.i_h);
+  const int dh = d / m->cfg.n_heads;
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const ItemW& iw = m->item[l];
+    const void* xin = l == 0 ? G0 : static_cast<const void*>(G);
+    const bool xin_f32 = l > 0;
+    GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, iw.wqkv, iw.bqkv, qkv, 3 * d, false, EPI_STORE);
+    g.ln_g = iw.ln1g; g.ln_b = iw.ln1b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+    st = run_proj(m, g, s);
+    if (st != FE_OK) return st;
+    AttnArgs a{};
+    a.Q = qkv; a.q_bs = (long long)Ucap * 3 * d; a.q_rs = 3 * d;
+    a.K = static_cast<const char*>(qkv) + d * e; a.k_bs = a.q_bs; a.k_rs = 3 * d;
+    a.V = static_cast<const char*>(qkv) + 2 * d * e; a.v_bs = a.q_bs; a.v_rs = 3 * d;
+    a.O = O; a.o_bs = (long long)Ucap * d; a.o_rs = d;
+    a.B = B; a.nq = Ucap; a.nk = Ucap; a.n_heads = m->cfg.n_heads; a.dh = dh;
+    a.q_valid = n_uniq; a.k_valid = n_uniq;
+    a.scale = 1.0f / sqrtf((float)dh);
+    FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+    g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
+    g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+    st = run_proj(m, g, s);
+    if (st != FE_OK) return st;
+    // cross-attention: the distinct elements are the queries, the context cache the keys/values
+    g = gemm(G, d, true, R, d, d, iw.wq, iw.bq, Qc, d, false, EPI_STORE);
+    g.ln_g = iw.ln2g; g.ln_b = iw.ln2b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+    st = run_proj(m, g, s);
+    if (st != FE_OK) return st;
+    AttnArgs c{};
+    c.Q = Qc; c.q_bs = (long long)Ucap * d; c.q_rs = d;
+    c.K = static_cast<const char*>(kv) + (size_t)(2 * l) * B * T * d * e; c.k_bs = (long long)T * d; c.k_rs = d;
+    c.V = static_cast<const char*>(kv) + (size_t)(2 * l + 1) * B * T * d * e; c.v_bs = (long long)T * d; c.v_rs = d;
+    c.O = O; c.o_bs = (long long)Ucap * d; c.o_rs = d;
+    c.B = B; c.nq = Ucap; c.nk = T; c.n_heads = m->cfg.n_heads; c.dh = dh;
+    c.q_valid = n_uniq; c.k_valid = nullptr;
+    c.scale = 1.0f / sqrtf((float)dh);
+    FE_LAUNCH(F_ATTN, s, launch_attention(c, bf, s));
+    g = gemm(O, d, false, R, d, d, iw.wo2, iw.bo2, G, d, true, EPI_RESID);
+    g.res = G; g.ldr = d; g.res_f32 = true; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+    st = run_proj(m, g, s);
+    if (st != FE_OK) return st;
+    st = run_ffn(m, G, R, iw.ln3g, iw.ln3b, iw.w1, iw.b1, iw.w2, iw.b2, Hf, n_uniq, Ucap, s);
+    if (st != FE_OK) return st;
+  }
+  FE_LAUNCH(F_LN, s, launch_layernorm_masked(G, 1, d, R, d, m->item_lnf_g, m->item_lnf_b, H, 0, d, n_uniq, Ucap, bf, s));
+  return FE_OK;
+}
+
+fe_status fe_assemble(const fe_model* m, int B, int K, int L, int U_cap, const int32_t* slot, const void* H, void* seq,
+                      void* stream) {
+  fe_status st = check_dims(m, B, 1, U_cap, K, L);
+  if (st != FE_OK) return st;
+  if (!slot || !H || !seq) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(slot) || !aligned16(H) || !aligned16(seq)) return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  FE_LAUNCH(F_ASSEMBLE, static_cast<hipStream_t>(stream), launch_assemble(slot, H, B, K, L, U_cap, m->cfg.d, m->cls, m->pos, seq, m->bf16,
+                         static_cast<hipStream_t>(stream)));
+  return FE_OK;
+}
+
+fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* seq, float* Cp, void* ws, size_t ws_bytes,
+                            void* stream) {
+  fe_status st = check_dims(m, B, 1, 1, K, L);
+  if (st != FE_OK) return st;
+  if (!seq || !Cp || !ws) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(seq) || !aligned16(Cp) || !aligned16(ws)) return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const Ws w = layout(m, B, 1, 1, K, L);
+  if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = m->bf16;
+  const int d = m->cfg.d, S = L + 1;
+  Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h)};
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    st = enc_block(m, m->seq[l], B * K, S, l == 0 ? seq : b.X, l > 0, b, nullptr, s);
+    if (st != FE_OK) return st;
+  }
+  // c_k = final LayerNorm of each list's [CLS] row (row 0 of every S-row group)
+  float* c = at<float>(ws, w.s_c);
+  FE_LAUNCH(F_LN, s, launch_layernorm(b.X, 1, (long long)S * d, B * K, d, m->seq_lnf_g, m->seq_lnf_b, c, 1, d, bf, s));
+  Bufs bc{c, b.qkv, b.O, b.Hf};
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s);
+    if (st != FE_OK) return st;
+  }
+  FE_LAUNCH(F_LN, s, launch_layernorm(c, 1, d, B * K, d, m->cross_lnf_g, m->cross_lnf_b, Cp, 1, d, bf, s));
+  return FE_OK;
+}
+
+fe_status fe_score_select(const fe_model* m, int B, int K, const float* Cp, float* scores, int32_t* best, void* stream) {
+  fe_status st = check_dims(m, B, 1, 1, K, 1);
+  if (st != FE_OK) return st;
+  if (!Cp || !scores || !best) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(Cp)) return fail(FE_EINVAL, "Cp must be 16-byte aligned");
+  FE_LAUNCH(F_SCORE, static_cast<hipStream_t>(stream), launch_score_select(Cp, B, K, m->cfg.d, m->head_w, m->head_b, scores, best, static_cast<hipStream_t>(stream)));
+  return FE_OK;
+}
+
+}  // extern "C"

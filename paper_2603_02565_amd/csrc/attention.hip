@@ -1,0 +1,178 @@
+// Multi-head scaled dot-product attention with a key padding mask and online softmax.
+//
+// One wave owns 16 queries of one (batch, head); a workgroup holds WAVES waves that share the
+// (batch, head) and walk the keys in blocks of 32.  For each block the wave computes the
+// transposed score tile S^T = K Q^T with matrix-core instructions (keys are rows, so every lane
+// ends up holding scores of ONE query), updates that query's running max / sum in fp32, and
+// multiplies P^T into the transposed output O^T = V^T P^T.  Keeping everything transposed means
+// the probabilities produced by one MFMA are already laid out as the B operand of the next, with
+// no LDS round trip; only V is transposed through LDS.  The key rows fed to the two score MFMAs
+// of a block are permuted so that lane group g holds keys 8g..8g+7 in order, which is exactly the
+// k-slot order the P V^T product expects.
+#include "fe_common.h"
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <typename T, int WAVES, int DH>
+__global__ __launch_bounds__(WAVES * 64) void k_attention(AttnArgs a) {
+  constexpr int VPAD = sizeof(T) == 2 ? 8 : 4;
+  constexpr int VLD = 32 + VPAD;
+  constexpr int NB = DH / 16;            // 16-row blocks of O^T
+  __shared__ __attribute__((aligned(16))) T Vt[DH * VLD];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, q_in = lane & 15;
+  // flattened grid: x = (query-tile group) + groups * (head + n_heads * batch)
+  const int groups = (a.nq + WAVES * 16 - 1) / (WAVES * 16);
+  const int qg = blockIdx.x % groups, bh = blockIdx.x / groups;
+  const int h = bh % a.n_heads, b = bh / a.n_heads;
+  int nq = a.nq, nk = a.nk;
+  if (a.q_valid) nq = min(nq, a.q_valid[b]);
+  if (a.k_valid) nk = min(nk, a.k_valid[b]);
+  if (qg * WAVES * 16 >= nq || nk <= 0) return;   // uniform over the workgroup
+  const int q0 = (qg * WAVES + wave) * 16;
+  const bool active = q0 < nq;
+
+  const T* Qb = static_cast<const T*>(a.Q) + b * a.q_bs + h * DH;
+  const T* Kb = static_cast<const T*>(a.K) + b * a.k_bs + h * DH;
+  const T* Vb = static_cast<const T*>(a.V) + b * a.v_bs + h * DH;
+  const int qrow = q0 + q_in;
+  const bool qok = active && qrow < nq;
+  const float sl2 = a.scale * kLog2e;
+
+  // Q^T as the B operand of S^T = K Q^T
+  bf16x8 qf8[DH / 32];
+  float qf1[DH / 4];
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+      qf8[c] = qok ? *reinterpret_cast<const bf16x8*>(Qb + (long long)qrow * a.q_rs + c * 32 + g * 8) : bf16x8{};
+  } else {
+#pragma unroll
+    for (int s = 0; s < DH / 4; ++s) qf1[s] = qok ? (float)Qb[(long long)qrow * a.q_rs + s * 4 + g] : 0.f;
+  }
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kb = 0; kb < nk; kb += 32) {
+    __syncthreads();
+    // ---- V block -> LDS, transposed (zeros past the last valid key)
+    constexpr int VEC = 16 / sizeof(T);
+    for (int e = threadIdx.x; e < 32 * DH / VEC; e += WAVES * 64) {
+      const int key = e / (DH / VEC), d0 = (e % (DH / VEC)) * VEC;
+      T v[VEC];
+      if (kb + key < nk) {
+        *reinterpret_cast<uint4*>(v) = *reinterpret_cast<const uint4*>(Vb + (long long)(kb + key) * a.v_rs + d0);
+      } else {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = from_f32<T>(0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) Vt[(d0 + i) * VLD + key] = v[i];
+    }
+    __syncthreads();
+    if (!active) continue;
+
+    // ---- S^T for keys kb + kappa_j(r), r = lane row of the A operand
+    const int r = lane & 15;
+    const int key0 = kb + (r >> 2) * 8 + (r & 3);
+    const int key1 = key0 + 4;
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        const bf16x8 k0 = key0 < nk ? *reinterpret_cast<const bf16x8*>(Kb + (long long)key0 * a.k_rs + c * 32 + g * 8) : bf16x8{};
+        const bf16x8 k1 = key1 < nk ? *reinterpret_cast<const bf16x8*>(Kb + (long long)key1 * a.k_rs + c * 32 + g * 8) : bf16x8{};
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf8[c], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf8[c], s1, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int s = 0; s < DH / 4; ++s) {
+        const float k0 = key0 < nk ? (float)Kb[(long long)key0 * a.k_rs + s * 4 + g] : 0.f;
+        const float k1 = key1 < nk ? (float)Kb[(long long)key1 * a.k_rs + s * 4 + g] : 0.f;
+        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(k0, qf1[s], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(k1, qf1[s], s1, 0, 0, 0);
+      }
+    }
+    // lane now holds scores of query q_in for keys kb + 8g + j, j = 0..7
+    float p[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      p[j] = (kb + g * 8 + j < nk) ? s0[j] * sl2 : -INFINITY;
+      p[4 + j] = (kb + g * 8 + 4 + j < nk) ? s1[j] * sl2 : -INFINITY;
+    }
+    float mx = p[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) mx = fmaxf(mx, p[j]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) { p[j] = exp2f(p[j] - m_new); psum += p[j]; }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) o[i] *= alpha;
+
+    // ---- O^T += V^T P^T
+    if constexpr (sizeof(T) == 2) {
+      bf16x8 pb;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pb[j] = (bf16)p[j];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vt[(i * 16 + (lane & 15)) * VLD + g * 8]);
+        o[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[i], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const float vf = Vt[(i * 16 + (lane & 15)) * VLD + g * 8 + s];
+          o[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, p[s], o[i], 0, 0, 0);
+        }
+      }
+    }
+  }
+  if (!active) return;
+  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+  l_tot += __shfl_xor(l_tot, 32, 64);
+  if (!qok) return;
+  const float inv = 1.f / l_tot;
+  T* Ob = static_cast<T*>(a.O) + b * a.o_bs + (long long)qrow * a.o_rs + h * DH;
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Ob[i * 16 + g * 4 + j] = from_f32<T>(o[i][j] * inv);
+}
+
+template <typename T, int DH>
+hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
+  const int qt = (a.nq + 15) / 16;
+  const long long bh = (long long)a.n_heads * a.B;
+  if (qt >= 4) {
+    hipLaunchKernelGGL((k_attention<T, 4, DH>), dim3((unsigned)(((qt + 3) / 4) * bh)), dim3(256), 0, s, a);
+  } else if (qt >= 2) {
+    hipLaunchKernelGGL((k_attention<T, 2, DH>), dim3((unsigned)(((qt + 1) / 2) * bh)), dim3(128), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_attention<T, 1, DH>), dim3((unsigned)(qt * bh)), dim3(64), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnArgs& a, bool bf16_model, hipStream_t s) {
+  if (a.B <= 0 || a.nq <= 0) return hipSuccess;
+  if (bf16_model) return a.dh == 64 ? launch_t<bf16, 64>(a, s) : launch_t<bf16, 32>(a, s);
+  return a.dh == 64 ? launch_t<float, 64>(a, s) : launch_t<float, 32>(a, s);
+}

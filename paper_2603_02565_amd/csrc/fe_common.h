@@ -1,0 +1,101 @@
+// Internal declarations shared by the HIP kernels and the C-ABI layer of libflasheval.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+#define FE_DEV __device__ __forceinline__
+
+FE_DEV float to_f32(float v) { return v; }
+FE_DEV float to_f32(bf16 v) { return (float)v; }
+template <typename T> FE_DEV T from_f32(float v);
+template <> FE_DEV float from_f32<float>(float v) { return v; }
+template <> FE_DEV bf16 from_f32<bf16>(float v) { return (bf16)v; }  // round to nearest even
+
+FE_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+FE_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// ------------------------------------------------------------------------------------------
+// Host-side launch descriptors (one per kernel family).
+// ------------------------------------------------------------------------------------------
+
+enum fe_epi { EPI_STORE = 0, EPI_RELU = 1, EPI_RESID = 2 };
+
+// C = epi( pro(A) x W + bias ).  A is [R][K] with row stride lda (elements); pro(A) is the
+// LayerNorm of each A row (over K) when ln_g != nullptr.  W is given transposed, Wt [N][K]
+// (k contiguous).  Output column n of row r goes to
+//   C + (n / col_block) * col_block_stride + r * ldc + (n % col_block).
+// EPI_RESID: C is fp32 and receives res[r*ldr + n] + acc + bias (res may alias C).
+// Rows r with (r % rows_per_batch) >= nvalid[r / rows_per_batch] are padding: tiles made
+// only of padding are skipped and padding rows are not stored (nvalid == nullptr: all valid).
+struct GemmArgs {
+  const void* A; int lda; int a_f32;   // a_f32: A holds fp32 values, else act
+  int R, K, N;
+  const void* Wt;                      // act [N][K]
+  const float* bias;                   // [N] or nullptr
+  const float* ln_g; const float* ln_b;
+  void* C; int ldc; int c_f32;         // c_f32: store fp32, else act
+  int col_block; long long col_block_stride;
+  int epi;
+  const void* res; int ldr; int res_f32;
+  const int32_t* nvalid; int rows_per_batch;
+};
+
+// O = softmax(Q K^T * scale) V per (batch, head).  Q rows of batch b start at
+// Q + b*q_bs (row stride q_rs), likewise K, V, O.  nq/nk rows per batch; the optional
+// nvalid[b] caps both the query rows computed and the keys attended (key padding mask).
+struct AttnArgs {
+  const void* Q; long long q_bs; int q_rs;
+  const void* K; long long k_bs; int k_rs;
+  const void* V; long long v_bs; int v_rs;
+  void* O; long long o_bs; int o_rs;
+  int B, nq, nk, n_heads, dh;
+  const int32_t* q_valid;   // [B] or nullptr
+  const int32_t* k_valid;   // [B] or nullptr
+  float scale;
+};
+
+// X += W2 ReLU(LN(X) W1 + b1) + b2 over R rows of fp32 X [R][D] (bf16 models; weights packed
+// in MFMA B-operand order).  Padding rows (per nvalid) are neither read nor written.
+struct FfnArgs {
+  float* X; int R, D, F;
+  const float* ln_g; const float* ln_b;
+  const void* W1p; const float* b1;
+  const void* W2p; const float* b2;
+  const int32_t* nvalid; int rows_per_batch;
+};
+
+hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s);   // fp32 models
+hipError_t launch_proj(const GemmArgs& a, hipStream_t s);                    // bf16 models, K = d
+hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);                      // bf16 models
+hipError_t launch_attention(const AttnArgs& a, bool bf16_model, hipStream_t s);
+hipError_t launch_layernorm(const void* X, int x_f32, long long x_rs, int R, int d, const float* g,
+                            const float* b, void* Y, int y_f32, long long y_rs, bool bf16_model,
+                            hipStream_t s);
+hipError_t launch_layernorm_masked(const void* X, int x_f32, long long x_rs, int R, int d, const float* g,
+                                   const float* b, void* Y, int y_f32, long long y_rs, const int32_t* nvalid,
+                                   int rpb, bool bf16_model, hipStream_t s);
+hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s);
+hipError_t launch_dedup(const int32_t* lists, int B, int KL, int M, int U_cap, int32_t* uniq,
+                        int32_t* n_uniq, int32_t* slot, int32_t* status, hipStream_t s);
+hipError_t launch_gather_rows(const void* table, long long table_bs, int n_rows_table, const int32_t* idx,
+                              int idx_bs, const int32_t* nvalid, int B, int rows, int d, void* out,
+                              int32_t* status, int status_bit, bool bf16_model, hipStream_t s);
+hipError_t launch_assemble(const int32_t* slot, const void* H, int B, int K, int L, int U_cap, int d,
+                           const void* cls, const void* pos, void* seq, bool bf16_model, hipStream_t s);
+hipError_t launch_score_select(const float* Cp, int B, int K, int d, const float* w, const float* bias,
+                               float* scores, int32_t* best, hipStream_t s);

@@ -1,0 +1,218 @@
+// fp32 row-tile matrix product with a LayerNorm prologue and bias / ReLU / residual epilogues,
+// plus the standalone row LayerNorm used by both model types.
+//
+// On fp32 models every projection of the joint pass (q|k|v, attention output, FFN up and down,
+// the context-side key/value cache) is one call of k_gemm: C = epi(LN(A) x W + b), on the
+// v_mfma_f32_16x16x4_f32 matrix cores.  (bf16 models use the fused kernels of fused.hip.)  Operand tiles are staged through LDS; the LayerNorm
+// statistics of a row tile are computed once in fp32 before the k loop and applied while the
+// A tile is copied into LDS, so the normalised activations never round-trip through HBM.
+#include "fe_common.h"
+
+namespace {
+
+template <typename T> struct Tile;
+// bf16: 64x64 output tile, 4 waves in a 2x2 grid of 32x32 MFMA blocks, k staged 64 at a time.
+template <> struct Tile<bf16> { static constexpr int TM = 64, TN = 64, KC = 64, PAD = 8; };
+// fp32: 64x32 output tile, each wave 16 rows x two 16x16 MFMA blocks, k staged 32 at a time.
+template <> struct Tile<float> { static constexpr int TM = 64, TN = 32, KC = 32, PAD = 4; };
+
+FE_DEV void load4(const void* p, bool f32, float* v) {
+  if (f32) {
+    float4 t = *reinterpret_cast<const float4*>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else {
+    bf16x4 t = *reinterpret_cast<const bf16x4*>(p);
+    v[0] = (float)t[0]; v[1] = (float)t[1]; v[2] = (float)t[2]; v[3] = (float)t[3];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  constexpr int TM = Tile<T>::TM, TN = Tile<T>::TN, KC = Tile<T>::KC, LDS_LD = KC + Tile<T>::PAD;
+  __shared__ __attribute__((aligned(16))) T As[TM * LDS_LD];
+  __shared__ __attribute__((aligned(16))) T Bs[TN * LDS_LD];
+  __shared__ float s_mean[TM], s_rstd[TM];
+  __shared__ int s_valid[TM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row0 = blockIdx.x * TM, col0 = blockIdx.y * TN;
+  const bool a_f32 = a.a_f32 || sizeof(T) == 4;   // act-typed input of an fp32 model is fp32 too
+  const size_t asz = a_f32 ? 4 : sizeof(T);
+  const char* A = static_cast<const char*>(a.A);
+
+  int my_valid = 0;
+  if (tid < TM) {
+    const int r = row0 + tid;
+    my_valid = r < a.R;
+    if (my_valid && a.nvalid) my_valid = (r % a.rows_per_batch) < a.nvalid[r / a.rows_per_batch];
+    s_valid[tid] = my_valid;
+  }
+  if (!__syncthreads_or(my_valid)) return;   // tile made only of padding rows
+
+  const bool ln = a.ln_g != nullptr;
+  if (ln) {
+    // wave w owns tile rows 16w..16w+15; two-pass mean / biased variance in fp32
+    for (int i = 0; i < TM / 4; ++i) {
+      const int rr = wave * (TM / 4) + i;
+      const int r = row0 + rr;
+      float mean = 0.f, rstd = 0.f;
+      if (s_valid[rr]) {
+        const char* rowp = A + (size_t)r * a.lda * asz;
+        float vals[8];
+        int nv = 0;
+        float sum = 0.f;
+        for (int k = lane * 4; k < a.K; k += 256) {
+          float v4[4];
+          load4(rowp + (size_t)k * asz, a_f32, v4);
+          for (int j = 0; j < 4; ++j) { vals[nv * 4 + j] = v4[j]; sum += v4[j]; }
+          ++nv;
+        }
+        mean = wave_sum(sum) / (float)a.K;
+        float sq = 0.f;
+        for (int t = 0; t < nv * 4; ++t) { const float dlt = vals[t] - mean; sq += dlt * dlt; }
+        rstd = rsqrtf(wave_sum(sq) / (float)a.K + 1e-5f);
+      }
+      if (lane == 0) { s_mean[rr] = mean; s_rstd[rr] = rstd; }
+    }
+    __syncthreads();
+  }
+
+  f32x16 acc16 = {};
+  f32x4 acc4a = {}, acc4b = {};
+
+  const T* Wt = static_cast<const T*>(a.Wt);
+  for (int k0 = 0; k0 < a.K; k0 += KC) {
+    // ---- stage A (LayerNorm applied, rounded to the operand type) in groups of 4 along k
+    for (int gi = tid; gi < TM * KC / 4; gi += 256) {
+      const int rr = gi / (KC / 4), kk = (gi % (KC / 4)) * 4;
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (s_valid[rr]) {
+        load4(A + ((size_t)(row0 + rr) * a.lda + k0 + kk) * asz, a_f32, v);
+        if (ln) {
+          const float mu = s_mean[rr], rs = s_rstd[rr];
+          for (int j = 0; j < 4; ++j) v[j] = (v[j] - mu) * rs * a.ln_g[k0 + kk + j] + a.ln_b[k0 + kk + j];
+        }
+      }
+      T* dst = &As[rr * LDS_LD + kk];
+      for (int j = 0; j < 4; ++j) dst[j] = from_f32<T>(v[j]);
+    }
+    // ---- stage W^T rows col0..col0+TN, 16 bytes per load
+    constexpr int VB = 16 / sizeof(T);
+    for (int gi = tid; gi < TN * KC / VB; gi += 256) {
+      const int cc = gi / (KC / VB), kk = (gi % (KC / VB)) * VB;
+      const uint4 w = *reinterpret_cast<const uint4*>(Wt + (size_t)(col0 + cc) * a.K + k0 + kk);
+      *reinterpret_cast<uint4*>(&Bs[cc * LDS_LD + kk]) = w;
+    }
+    __syncthreads();
+    if constexpr (sizeof(T) == 2) {
+      const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+      for (int ks = 0; ks < KC; ks += 16) {
+        const bf16x8 af = *reinterpret_cast<const bf16x8*>(&As[(wm * 32 + (lane & 31)) * LDS_LD + ks + (lane >> 5) * 8]);
+        const bf16x8 bf = *reinterpret_cast<const bf16x8*>(&Bs[(wn * 32 + (lane & 31)) * LDS_LD + ks + (lane >> 5) * 8]);
+        acc16 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf, acc16, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KC; ks += 4) {
+        const float af = As[(wave * 16 + (lane & 15)) * LDS_LD + ks + (lane >> 4)];
+        const float b0 = Bs[(lane & 15) * LDS_LD + ks + (lane >> 4)];
+        const float b1 = Bs[(16 + (lane & 15)) * LDS_LD + ks + (lane >> 4)];
+        acc4a = __builtin_amdgcn_mfma_f32_16x16x4f32(af, b0, acc4a, 0, 0, 0);
+        acc4b = __builtin_amdgcn_mfma_f32_16x16x4f32(af, b1, acc4b, 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue
+  auto emit = [&](int rr, int cc, float v) {
+    if (!s_valid[rr]) return;
+    const int r = row0 + rr, n = col0 + cc;
+    if (a.bias) v += a.bias[n];
+    const long long off = (long long)(n / a.col_block) * a.col_block_stride + (long long)r * a.ldc + (n % a.col_block);
+    if (a.epi == EPI_RESID) {
+      const long long roff = (long long)r * a.ldr + n;
+      const float res = a.res_f32 ? static_cast<const float*>(a.res)[roff] : to_f32(static_cast<const T*>(a.res)[roff]);
+      static_cast<float*>(a.C)[off] = res + v;
+      return;
+    }
+    if (a.epi == EPI_RELU) v = fmaxf(v, 0.f);
+    if (a.c_f32) static_cast<float*>(a.C)[off] = v;
+    else static_cast<T*>(a.C)[off] = from_f32<T>(v);
+  };
+  if constexpr (sizeof(T) == 2) {
+    const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      emit(wm * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3), wn * 32 + (lane & 31), acc16[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      emit(wave * 16 + (lane >> 4) * 4 + i, lane & 15, acc4a[i]);
+      emit(wave * 16 + (lane >> 4) * 4 + i, 16 + (lane & 15), acc4b[i]);
+    }
+  }
+}
+
+// One wave per row: Y = LN(X), padding rows (per nvalid) written as zeros.
+template <typename T>
+__global__ __launch_bounds__(256) void k_layernorm(const void* X, int x_f32, long long x_rs, int R, int d,
+                                                   const float* g, const float* b, void* Y, int y_f32,
+                                                   long long y_rs, const int32_t* nvalid, int rpb) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= R) return;
+  const bool valid = !nvalid || (r % rpb) < nvalid[r / rpb];
+  float vals[16];
+  int nv = 0;
+  float sum = 0.f;
+  x_f32 = x_f32 || sizeof(T) == 4;
+  const size_t xs = x_f32 ? 4 : sizeof(T);
+  const char* xr = static_cast<const char*>(X) + (size_t)r * x_rs * xs;
+  for (int k = lane * 4; k < d; k += 256) {
+    float v4[4];
+    load4(xr + (size_t)k * xs, x_f32, v4);
+    for (int j = 0; j < 4; ++j) { vals[nv * 4 + j] = v4[j]; sum += v4[j]; }
+    ++nv;
+  }
+  const float mean = wave_sum(sum) / (float)d;
+  float sq = 0.f;
+  for (int t = 0; t < nv * 4; ++t) { const float dl = vals[t] - mean; sq += dl * dl; }
+  const float rstd = rsqrtf(wave_sum(sq) / (float)d + 1e-5f);
+  nv = 0;
+  for (int k = lane * 4; k < d; k += 256, ++nv) {
+    for (int j = 0; j < 4; ++j) {
+      const float y = valid ? (vals[nv * 4 + j] - mean) * rstd * g[k + j] + b[k + j] : 0.f;
+      if (y_f32) static_cast<float*>(Y)[(size_t)r * y_rs + k + j] = y;
+      else static_cast<T*>(Y)[(size_t)r * y_rs + k + j] = from_f32<T>(y);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s) {
+  if (a.R <= 0) return hipSuccess;
+  if (bf16_model) return hipErrorInvalidValue;   // bf16 weights are packed for k_proj / k_ffn
+  dim3 grid((a.R + Tile<float>::TM - 1) / Tile<float>::TM, a.N / Tile<float>::TN);
+  hipLaunchKernelGGL(k_gemm<float>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm_masked(const void* X, int x_f32, long long x_rs, int R, int d, const float* g,
+                                   const float* b, void* Y, int y_f32, long long y_rs, const int32_t* nvalid,
+                                   int rpb, bool bf16_model, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  dim3 grid((R + 3) / 4);
+  if (bf16_model)
+    hipLaunchKernelGGL(k_layernorm<bf16>, grid, dim3(256), 0, s, X, x_f32, x_rs, R, d, g, b, Y, y_f32, y_rs, nvalid, rpb);
+  else
+    hipLaunchKernelGGL(k_layernorm<float>, grid, dim3(256), 0, s, X, x_f32, x_rs, R, d, g, b, Y, y_f32, y_rs, nvalid, rpb);
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm(const void* X, int x_f32, long long x_rs, int R, int d, const float* g, const float* b,
+                            void* Y, int y_f32, long long y_rs, bool bf16_model, hipStream_t s) {
+  return launch_layernorm_masked(X, x_f32, x_rs, R, d, g, b, Y, y_f32, y_rs, nullptr, 1, bf16_model, s);
+}

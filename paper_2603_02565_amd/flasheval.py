@@ -1,0 +1,272 @@
+"""Python binding of libflasheval (ctypes).  Argument marshalling only: every step of the pass
+runs in the library's HIP kernels.  Functions carry the names of the C ABI in
+include/flasheval.h and take torch tensors that live on the current HIP device; the stream is
+torch's current stream unless one is given.
+
+There is no fallback: if libflasheval.so has not been built, `load_library` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libflasheval.so")
+
+FE_OK, FE_EINVAL, FE_EUNSUPPORTED, FE_ENOMEM, FE_EHIP = range(5)
+FE_F32, FE_BF16 = 0, 1
+FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
+
+EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_last_error",
+            "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
+            "fe_score_select", "fe_trace_enable", "fe_trace_read", "fe_trace_family")
+FE_TRACE_FAMILIES = 9
+
+
+class FeError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where} -> status {status}: {msg}")
+        self.status = status
+
+
+class fe_config(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("ffn_dim", ctypes.c_int32), ("max_L", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libflasheval.so (once).  Raises if it is missing: build it with __graft_entry__.build()."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing; build the HIP library first (python -c "
+                           "'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(path)
+    P, I, Z, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_int
+    cfgp = ctypes.POINTER(fe_config)
+    sig = {
+        "fe_param_count": (S, [cfgp, ctypes.POINTER(Z)]),
+        "fe_model_create": (S, [cfgp, P, Z, ctypes.POINTER(P)]),
+        "fe_model_destroy": (None, [P]),
+        "fe_workspace_size": (S, [P, I, I, I, I, I, ctypes.POINTER(Z)]),
+        "fe_last_error": (ctypes.c_char_p, []),
+        "fe_read_device_status": (S, [P, P, I, P, P]),
+        "fe_encode_context": (S, [P, I, I, P, P, P, P, Z, P]),
+        "fe_encode_items": (S, [P, I, I, P, P, I, I, P, I, P, P, P, P, P, Z, P]),
+        "fe_assemble": (S, [P, I, I, I, I, P, P, P, P]),
+        "fe_cross_sequence": (S, [P, I, I, I, P, P, P, Z, P]),
+        "fe_score_select": (S, [P, I, I, P, P, P, P]),
+        "fe_trace_enable": (S, [I]),
+        "fe_trace_read": (S, [P, P]),
+        "fe_trace_family": (ctypes.c_char_p, [I]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str) -> None:
+    if status != FE_OK:
+        raise FeError(status, where, load_library().fe_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+# ---------------------------------------------------------------------------------------------
+# Parameter order of fe_model_create (as documented in include/flasheval.h)
+# ---------------------------------------------------------------------------------------------
+
+_ENC = ("ln1.g", "ln1.b", "wqkv", "bqkv", "wo", "bo", "ln2.g", "ln2.b", "w1", "b1", "w2", "b2")
+_ITEM = ("ln1.g", "ln1.b", "wqkv", "bqkv", "wo", "bo", "ln2.g", "ln2.b", "wq", "bq", "wo2", "bo2",
+         "ln3.g", "ln3.b", "w1", "b1", "w2", "b2")
+
+
+def param_names(n_layers: int, vocab: int) -> List[str]:
+    names: List[str] = []
+    names += [f"ctx.{l}.{p}" for l in range(n_layers) for p in _ENC]
+    names += ["ctx.lnf.g", "ctx.lnf.b"]
+    names += [f"ctx.kv.{l}.{p}" for l in range(n_layers) for p in ("wk", "bk", "wv", "bv")]
+    names += [f"item.{l}.{p}" for l in range(n_layers) for p in _ITEM]
+    names += ["item.lnf.g", "item.lnf.b"]
+    names += [f"seq.{l}.{p}" for l in range(n_layers) for p in _ENC]
+    names += ["seq.lnf.g", "seq.lnf.b"]
+    names += [f"cross.{l}.{p}" for l in range(n_layers) for p in _ENC]
+    names += ["cross.lnf.g", "cross.lnf.b"]
+    names += ["cls", "pos", "head.w", "head.b"]
+    if vocab:
+        names.append("emb")
+    return names
+
+
+def pack_params(params: Dict[str, np.ndarray], n_layers: int, vocab: int) -> np.ndarray:
+    """Flat float32 array of every parameter in fe_model_create order."""
+    return np.concatenate([np.ascontiguousarray(params[n], dtype=np.float32).reshape(-1)
+                           for n in param_names(n_layers, vocab)])
+
+
+# ---------------------------------------------------------------------------------------------
+# C functions (same names as the ABI)
+# ---------------------------------------------------------------------------------------------
+
+def fe_param_count(cfg: fe_config) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().fe_param_count(ctypes.byref(cfg), ctypes.byref(n)), "fe_param_count")
+    return n.value
+
+
+def fe_model_create(cfg: fe_config, flat: np.ndarray) -> int:
+    flat = np.ascontiguousarray(flat, dtype=np.float32)
+    h = ctypes.c_void_p()
+    _check(load_library().fe_model_create(ctypes.byref(cfg), flat.ctypes.data, flat.size, ctypes.byref(h)),
+           "fe_model_create")
+    return h.value
+
+
+def fe_model_destroy(model: int) -> None:
+    load_library().fe_model_destroy(model)
+
+
+def fe_workspace_size(model: int, B: int, T: int, M: int, K: int, L: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().fe_workspace_size(model, B, T, M, K, L, ctypes.byref(n)), "fe_workspace_size")
+    return n.value
+
+
+def fe_read_device_status(model: int, ws, B: int, stream=None) -> np.ndarray:
+    out = np.zeros(B, dtype=np.int32)
+    _check(load_library().fe_read_device_status(model, _ptr(ws), B, _stream(stream), out.ctypes.data),
+           "fe_read_device_status")
+    return out
+
+
+def fe_encode_context(model: int, B: int, T: int, x, ctx_ids, kv, ws, stream=None) -> None:
+    _check(load_library().fe_encode_context(model, B, T, _ptr(x), _ptr(ctx_ids), _ptr(kv), _ptr(ws),
+                                            ws.numel() * ws.element_size(), _stream(stream)), "fe_encode_context")
+
+
+def fe_encode_items(model: int, B: int, M: int, pool, lists, K: int, L: int, kv, T: int, uniq, n_uniq, slot, H, ws,
+                    stream=None) -> None:
+    _check(load_library().fe_encode_items(model, B, M, _ptr(pool), _ptr(lists), K, L, _ptr(kv), T, _ptr(uniq),
+                                          _ptr(n_uniq), _ptr(slot), _ptr(H), _ptr(ws),
+                                          ws.numel() * ws.element_size(), _stream(stream)), "fe_encode_items")
+
+
+def fe_assemble(model: int, B: int, K: int, L: int, U_cap: int, slot, H, seq, stream=None) -> None:
+    _check(load_library().fe_assemble(model, B, K, L, U_cap, _ptr(slot), _ptr(H), _ptr(seq), _stream(stream)),
+           "fe_assemble")
+
+
+def fe_cross_sequence(model: int, B: int, K: int, L: int, seq, Cp, ws, stream=None) -> None:
+    _check(load_library().fe_cross_sequence(model, B, K, L, _ptr(seq), _ptr(Cp), _ptr(ws),
+                                            ws.numel() * ws.element_size(), _stream(stream)), "fe_cross_sequence")
+
+
+def fe_score_select(model: int, B: int, K: int, Cp, scores, best, stream=None) -> None:
+    _check(load_library().fe_score_select(model, B, K, _ptr(Cp), _ptr(scores), _ptr(best), _stream(stream)),
+           "fe_score_select")
+
+
+def fe_trace_enable(on: bool) -> None:
+    _check(load_library().fe_trace_enable(1 if on else 0), "fe_trace_enable")
+
+
+def fe_trace_read() -> Dict[str, Tuple[float, int]]:
+    """{family: (summed kernel ms, launches)} since the last read; synchronises the traced events."""
+    ms = np.zeros(FE_TRACE_FAMILIES, dtype=np.float64)
+    n = np.zeros(FE_TRACE_FAMILIES, dtype=np.int64)
+    lib = load_library()
+    _check(lib.fe_trace_read(ms.ctypes.data, n.ctypes.data), "fe_trace_read")
+    return {lib.fe_trace_family(i).decode(): (float(ms[i]), int(n[i])) for i in range(FE_TRACE_FAMILIES)}
+
+
+# ---------------------------------------------------------------------------------------------
+# Convenience: one model plus the buffers of one batch shape
+# ---------------------------------------------------------------------------------------------
+
+class Evaluator:
+    """Owns a model handle and, per batch shape, the device buffers of the five calls.
+
+    `params` maps the parameter names of `param_names` to float arrays; `dtype` is "f32" or
+    "bf16".  All tensors are allocated with torch on the current device.
+    """
+
+    def __init__(self, d: int, n_heads: int, n_layers: int, ffn_dim: int, max_L: int, vocab: int, dtype: str,
+                 params: Dict[str, np.ndarray]):
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("Evaluator needs a HIP device")
+        self.cfg = fe_config(d, n_heads, n_layers, ffn_dim, max_L, vocab, FE_BF16 if dtype == "bf16" else FE_F32)
+        self.d, self.n_layers, self.vocab = d, n_layers, vocab
+        self.act = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.handle = fe_model_create(self.cfg, pack_params(params, n_layers, vocab))
+        self.buffers = None
+
+    def close(self) -> None:
+        if self.handle:
+            fe_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def allocate(self, B: int, T: int, M: int, K: int, L: int) -> Dict:
+        import torch
+        dev = torch.device("cuda", torch.cuda.current_device())
+        d, n = self.d, self.n_layers
+        U_cap = min(M, K * L)
+        ws_bytes = fe_workspace_size(self.handle, B, T, M, K, L)
+        i32 = torch.int32
+        self.buffers = dict(
+            shape=(B, T, M, K, L), U_cap=U_cap,
+            kv=torch.empty((n, 2, B, T, d), dtype=self.act, device=dev),
+            uniq=torch.empty((B, U_cap), dtype=i32, device=dev),
+            n_uniq=torch.empty((B,), dtype=i32, device=dev),
+            slot=torch.empty((B, K, L), dtype=i32, device=dev),
+            H=torch.empty((B, U_cap, d), dtype=self.act, device=dev),
+            seq=torch.empty((B, K, L + 1, d), dtype=self.act, device=dev),
+            Cp=torch.empty((B, K, d), dtype=torch.float32, device=dev),
+            scores=torch.empty((B, K), dtype=torch.float32, device=dev),
+            best=torch.empty((B,), dtype=i32, device=dev),
+            ws=torch.empty((ws_bytes,), dtype=torch.uint8, device=dev),
+        )
+        return self.buffers
+
+    def run(self, x=None, ctx_ids=None, pool=None, lists=None, stream=None) -> Dict:
+        """Enqueue the five calls on device tensors already resident on the GPU."""
+        b = self.buffers
+        B, T, M, K, L = b["shape"]
+        h = self.handle
+        fe_encode_context(h, B, T, x, ctx_ids, b["kv"], b["ws"], stream)
+        fe_encode_items(h, B, M, pool, lists, K, L, b["kv"], T, b["uniq"], b["n_uniq"], b["slot"], b["H"], b["ws"],
+                        stream)
+        fe_assemble(h, B, K, L, b["U_cap"], b["slot"], b["H"], b["seq"], stream)
+        fe_cross_sequence(h, B, K, L, b["seq"], b["Cp"], b["ws"], stream)
+        fe_score_select(h, B, K, b["Cp"], b["scores"], b["best"], stream)
+        return b

@@ -1,0 +1,94 @@
+"""Helpers for GPU tests: upload a generated workload, run the five C-ABI calls, fetch results.
+
+Tolerances follow the pass's precision: normwise per request and tensor,
+max|gpu - ref| <= rtol * max|ref|, with rtol 1e-4 for fp32 models and 2e-2 for bf16 models
+(bf16 operands, fp32 accumulation).  Integer outputs compare bit for bit.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from paper_2603_02565_amd import flasheval as fe
+
+RTOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rtol_for(cfg) -> float:
+    return RTOL[cfg.dtype]
+
+
+def normwise(gpu, ref) -> float:
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    scale = float(np.max(np.abs(ref))) if ref.size else 0.0
+    err = float(np.max(np.abs(gpu - ref))) if ref.size else 0.0
+    return err / scale if scale > 0 else err
+
+
+def score_scale(W, Cp_ref) -> float:
+    """Magnitude of the score head's dot products: max_k sum_i |C'_ki w_i| + |b|.
+
+    A score is a sum of d terms that largely cancel, so its own size says nothing about how
+    precisely it can be formed; the forward-error bound of a dot product is relative to the
+    sum of the terms' magnitudes.  Scores are compared against rtol times this scale.
+    """
+    Cp = np.asarray(Cp_ref, np.float64)
+    w = np.asarray(W["head.w"], np.float64)
+    return float(np.max(np.abs(Cp) @ np.abs(w)) + abs(float(W["head.b"][0])))
+
+
+def make_evaluator(cfg, W) -> fe.Evaluator:
+    return fe.Evaluator(cfg.d, cfg.n_heads, cfg.n_layers, cfg.ffn, cfg.max_L, cfg.vocab, cfg.dtype, W)
+
+
+def upload(cfg, I: Dict) -> Dict[str, Optional[torch.Tensor]]:
+    act = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", torch.cuda.current_device())
+    out = {}
+    for k in ("x", "pool"):
+        out[k] = None if I.get(k) is None else torch.from_numpy(np.ascontiguousarray(I[k])).to(dev).to(act)
+    out["ctx_ids"] = None if I.get("ctx_ids") is None else torch.from_numpy(
+        np.ascontiguousarray(I["ctx_ids"], dtype=np.int32)).to(dev)
+    out["lists"] = torch.from_numpy(np.ascontiguousarray(I["lists"], dtype=np.int32)).to(dev)
+    return out
+
+
+def fetch(bufs: Dict) -> Dict[str, np.ndarray]:
+    torch.cuda.synchronize()
+    res = {}
+    for k in ("kv", "uniq", "n_uniq", "slot", "H", "seq", "Cp", "scores", "best"):
+        t = bufs[k]
+        res[k] = (t.float() if t.is_floating_point() else t).cpu().numpy()
+    return res
+
+
+def run_pass(cfg, W, I, ev: Optional[fe.Evaluator] = None) -> Dict[str, np.ndarray]:
+    """Full pass of a generated workload; returns host copies of every output tensor."""
+    own = ev is None
+    if own:
+        ev = make_evaluator(cfg, W)
+    B, K, L = I["lists"].shape
+    T = (I["x"] if I.get("x") is not None else I["ctx_ids"]).shape[1]
+    ev.allocate(B, T, cfg.M, K, L)
+    d = upload(cfg, I)
+    bufs = ev.run(x=d["x"], ctx_ids=d["ctx_ids"], pool=d["pool"], lists=d["lists"])
+    out = fetch(bufs)
+    out["status"] = fe.fe_read_device_status(ev.handle, bufs["ws"], B)
+    if own:
+        ev.close()
+    return out
+
+
+def check_selection(best_gpu: int, scores_ref: np.ndarray, tol: float) -> None:
+    """Selection parity: exact when the oracle's top-2 margin exceeds 2*tol, else any near-max list."""
+    ref = np.asarray(scores_ref, np.float64)
+    order = np.argsort(-ref, kind="stable")
+    top = ref[order[0]]
+    margin = top - ref[order[1]] if ref.size > 1 else np.inf
+    if margin > 2 * tol:
+        assert best_gpu == int(order[0]), (best_gpu, int(order[0]), margin, tol)
+    else:
+        assert 0 <= best_gpu < ref.size and ref[best_gpu] >= top - tol, (best_gpu, top, ref[best_gpu], tol)

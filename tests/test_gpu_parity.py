@@ -1,0 +1,266 @@
+"""Parity of the HIP path (through the C ABI) with the float64 oracle, stage by stage and end to end."""
+import numpy as np
+import pytest
+import torch
+
+import gen
+import oracle
+from paper_2603_02565_amd import flasheval as fe
+from tests.gpu_harness import (check_selection, fetch, make_evaluator, normwise, rtol_for, run_pass, score_scale,
+                               upload)
+
+pytestmark = pytest.mark.gpu
+
+
+def _stage_refs(cfg, W, I, b):
+    return oracle.evaluate_cached(cfg, W, I, requests=[b], stages=True)[b]
+
+
+def _compare_request(cfg, W, out, ref, b, check_kv=True):
+    tol = rtol_for(cfg)
+    if check_kv:
+        for l in range(cfg.n_layers):
+            assert normwise(out["kv"][l, 0, b], ref["kv"][l][0]) <= tol, ("K cache", l)
+            assert normwise(out["kv"][l, 1, b], ref["kv"][l][1]) <= tol, ("V cache", l)
+    U = len(ref["uniq"])
+    assert out["n_uniq"][b] == U
+    assert np.array_equal(out["uniq"][b, :U], ref["uniq"])
+    assert np.all(out["uniq"][b, U:] == -1)
+    assert np.array_equal(out["slot"][b], ref["slot"])
+    assert normwise(out["H"][b, :U], ref["H"]) <= tol, "H"
+    assert np.all(out["H"][b, U:] == 0)
+    assert normwise(out["seq"][b], ref["seq"]) <= tol, "seq"
+    assert normwise(out["Cp"][b], ref["Cp"]) <= tol, "Cp"
+    stol = tol * score_scale(W, ref["Cp"])
+    assert np.max(np.abs(out["scores"][b] - ref["scores"])) <= stol, "scores"
+    check_selection(int(out["best"][b]), ref["scores"], stol)
+
+
+def test_cfg0_all_stages_fp32():
+    c = gen.config(0)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    ref = _stage_refs(c, W, I, 0)
+    _compare_request(c, W, out, ref, 0)
+    naive = oracle.evaluate_naive(c, W, I)[0]
+    assert normwise(out["scores"][0], naive["scores"]) <= 1e-4
+    assert int(out["best"][0]) == naive["best"]
+    assert out["status"][0] == 0
+
+
+@pytest.mark.parametrize("b", [0, 37, 63])
+def test_cfg1_end_to_end(cfg1_out, b):
+    c, W, I, out = cfg1_out
+    _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+
+
+def test_cfg1_distinct_sets_all_requests(cfg1_out):
+    c, W, I, out = cfg1_out
+    for b in range(c.B):
+        u, inv = np.unique(I["lists"][b], return_inverse=True)
+        assert out["n_uniq"][b] == len(u)
+        assert np.array_equal(out["uniq"][b, :len(u)], u)
+        assert np.array_equal(out["slot"][b].reshape(-1), inv.reshape(-1))
+    assert np.all(out["status"] == 0)
+
+
+def test_cfg1_naive_oracle_request0(cfg1_out):
+    """Request 0 against the candidate-factorised oracle itself (context per list, items per occurrence)."""
+    c, W, I, out = cfg1_out
+    naive = oracle.evaluate_naive(c, W, I, requests=[0])[0]
+    stol = rtol_for(c) * score_scale(W, naive["Cp"])
+    assert np.max(np.abs(out["scores"][0] - naive["scores"])) <= stol
+    check_selection(int(out["best"][0]), naive["scores"], stol)
+
+
+@pytest.fixture(scope="module")
+def cfg1_out():
+    c = gen.config(1)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    return c, W, I, run_pass(c, W, I)
+
+
+@pytest.mark.parametrize("K", gen.K_SWEEP)
+def test_cfg2_k_sweep(K):
+    c = gen.config(2, K=K)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in (0, c.B - 1):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b, check_kv=(b == 0))
+
+
+def test_cfg3_long_context():
+    c = gen.config(3)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in (0, c.B - 1):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+
+
+def test_cfg4_text_hypotheses():
+    c = gen.config(4)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in (0, c.B - 1):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+    assert np.all(out["status"] == 0)
+
+
+# ------------------------------------------------------------------------- stage-isolated parity
+
+def test_assemble_bit_exact_on_oracle_inputs():
+    """fe_assemble on H and slot given by the oracle: the gather is exact; the position add rounds once."""
+    c = gen.config(1, B=4)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = make_evaluator(c, W)
+    bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
+    U_cap = bufs["U_cap"]
+    H = np.zeros((c.B, U_cap, c.d), np.float32)
+    slot = np.zeros((c.B, c.K, c.L), np.int32)
+    for b in range(c.B):
+        ref = _stage_refs(c, W, I, b)
+        H[b, :len(ref["uniq"])] = ref["H"]
+        slot[b] = ref["slot"]
+    Hb = torch.from_numpy(H).cuda().to(torch.bfloat16)
+    sl = torch.from_numpy(slot).cuda()
+    fe.fe_assemble(ev.handle, c.B, c.K, c.L, U_cap, sl, Hb, bufs["seq"])
+    seq = bufs["seq"].float().cpu().numpy()
+    Hr = Hb.float().cpu().numpy().astype(np.float64)
+    pos = W["pos"].astype(np.float64)
+    want = np.empty_like(seq, dtype=np.float64)
+    for b in range(c.B):
+        want[b, :, 0] = W["cls"].astype(np.float64) + pos[0]
+        want[b, :, 1:] = Hr[b][slot[b]] + pos[1:c.L + 1]
+    # one bf16 rounding of an exactly formed fp32 sum
+    want_bf16 = torch.from_numpy(want.astype(np.float32)).to(torch.bfloat16).float().numpy()
+    assert np.array_equal(seq, want_bf16)
+    ev.close()
+
+
+def test_score_select_on_oracle_inputs():
+    c = gen.config(1, B=3)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = make_evaluator(c, W)
+    bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
+    Cp = np.random.default_rng(5).standard_normal((c.B, c.K, c.d)).astype(np.float32)
+    Cp[1, 7] = Cp[1, 3]                        # tie between lists 3 and 7
+    Cp[2] = Cp[2, 0]                           # every list identical
+    Cp[1, 40:] = np.nan                        # NaN scores never win
+    Cpt = torch.from_numpy(Cp).cuda()
+    fe.fe_score_select(ev.handle, c.B, c.K, Cpt, bufs["scores"], bufs["best"])
+    s = bufs["scores"].cpu().numpy()
+    best = bufs["best"].cpu().numpy()
+    for b in range(c.B):
+        ref = oracle.score(W, Cp[b].astype(np.float64))
+        ok = ~np.isnan(ref)
+        assert np.array_equal(np.isnan(s[b]), ~ok)
+        assert normwise(s[b][ok], ref[ok]) <= 1e-5
+    assert best[2] == 0
+    assert best[1] == oracle.select(s[1].astype(np.float64))
+    assert best[0] == oracle.select(s[0].astype(np.float64))
+    ev.close()
+
+
+# ------------------------------------------------------------------------- invariants and edge cases
+
+def test_permuting_lists_permutes_scores():
+    c = gen.config(1, B=2)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = make_evaluator(c, W)
+    a = run_pass(c, W, I, ev)
+    perm = np.random.default_rng(9).permutation(c.K)
+    J = dict(I, lists=np.ascontiguousarray(I["lists"][:, perm]))
+    p = run_pass(c, W, J, ev)
+    ev.close()
+    for b in range(c.B):
+        # the distinct set and H are unchanged by a list permutation: bitwise
+        assert np.array_equal(p["H"][b], a["H"][b])
+        assert np.array_equal(p["seq"][b], a["seq"][b][perm])
+        assert np.max(np.abs(p["scores"][b] - a["scores"][b][perm])) <= rtol_for(c) * score_scale(W, a["Cp"][b])
+
+
+def test_identical_lists_identical_scores():
+    c = gen.config(1, B=2)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    J = dict(I, lists=np.ascontiguousarray(np.broadcast_to(I["lists"][:, :1], I["lists"].shape)))
+    out = run_pass(c, W, J)
+    for b in range(c.B):
+        assert np.all(out["scores"][b] == out["scores"][b][0])
+        assert out["best"][b] == 0
+
+
+def test_two_runs_bitwise_identical():
+    c = gen.config(1, B=4)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = make_evaluator(c, W)
+    a = run_pass(c, W, I, ev)
+    b = run_pass(c, W, I, ev)
+    ev.close()
+    for k in ("kv", "H", "seq", "Cp", "scores", "best", "slot", "uniq"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("K,L", [(1, 1), (1, 10), (3, 1), (33, 7)])
+def test_small_and_ragged_shapes(K, L):
+    c = gen.config(1, B=3, K=K, L=L)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in range(c.B):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b, check_kv=(b == 0))
+
+
+def test_ragged_context_and_pool():
+    """T and U not multiples of any tile: T=37, M=23 < K*L."""
+    c = gen.config(1, B=2, T=37, M=23, K=9, L=6)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in range(c.B):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+
+
+def test_bad_index_sets_status_and_zero_row():
+    c = gen.config(1, B=2, K=5)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    lists = I["lists"].copy()
+    lists[1, 2, 3] = c.M + 5
+    lists[1, 4, 0] = -1
+    out = run_pass(c, W, dict(I, lists=lists))
+    assert out["status"][0] == 0
+    assert out["status"][1] & fe.FE_DEV_BAD_INDEX
+    assert out["slot"][1, 2, 3] == -1 and out["slot"][1, 4, 0] == -1
+    assert np.all(out["seq"][1, 2, 4] == 0) and np.all(out["seq"][1, 4, 1] == 0)
+
+
+def test_nan_context_selects_minus_one():
+    c = gen.config(1, B=2, K=5)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    x = I["x"].copy()
+    x[1] = np.nan
+    out = run_pass(c, W, dict(I, x=x))
+    assert out["best"][1] == -1
+    assert out["best"][0] >= 0
+
+
+def test_host_validation_errors():
+    c = gen.config(1, B=2, K=5)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = make_evaluator(c, W)
+    bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
+    d = upload(c, I)
+    with pytest.raises(fe.FeError) as e:           # both x and ctx_ids
+        fe.fe_encode_context(ev.handle, c.B, c.T, d["x"], d["lists"], bufs["kv"], bufs["ws"])
+    assert e.value.status == fe.FE_EINVAL
+    small = bufs["ws"][:1024]
+    with pytest.raises(fe.FeError) as e:           # workspace too small
+        fe.fe_encode_context(ev.handle, c.B, c.T, d["x"], None, bufs["kv"], small)
+    assert e.value.status == fe.FE_EINVAL
+    with pytest.raises(fe.FeError) as e:           # L beyond the position table
+        fe.fe_assemble(ev.handle, c.B, c.K, c.max_L + 1, bufs["U_cap"], bufs["slot"], bufs["H"], bufs["seq"])
+    assert e.value.status == fe.FE_EINVAL
+    with pytest.raises(fe.FeError) as e:           # misaligned pointer
+        fe.fe_assemble(ev.handle, c.B, c.K, c.L, bufs["U_cap"], bufs["slot"].data_ptr() + 4, bufs["H"], bufs["seq"])
+    assert e.value.status == fe.FE_EINVAL
+    with pytest.raises(fe.FeError) as e:
+        fe.fe_workspace_size(ev.handle, c.B, 9000, c.M, c.K, c.L)
+    assert e.value.status == fe.FE_EUNSUPPORTED
+    ev.close()
