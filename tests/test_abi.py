@@ -1,0 +1,87 @@
+"""C ABI checks that need no GPU: the library loads, exports what the headers declare, and the
+host-only entry points validate configurations.  No kernel is launched here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import gen
+from paper_2603_02565_amd import flasheval as fe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in ("flasheval.h", "flasheval_trace.h"):
+        with open(os.path.join(ROOT, "include", h)) as f:
+            text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        names |= set(re.findall(r"\b(fe_[a-z_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_function():
+    lib = fe.load_library()
+    declared = _declared()
+    assert {"fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
+            "fe_score_select"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert declared == set(fe.EXPORTED)
+
+
+def _cfg(c, **kw):
+    f = fe.fe_config(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, fe.FE_BF16 if c.dtype == "bf16" else fe.FE_F32)
+    for k, v in kw.items():
+        setattr(f, k, v)
+    return f
+
+
+@pytest.mark.parametrize("cid", [0, 1, 3, 4])
+def test_param_count_matches_generator(cid):
+    c = gen.config(cid)
+    W = gen.make_weights(c)
+    assert fe.fe_param_count(_cfg(c)) == sum(v.size for v in W.values())
+    assert sorted(fe.param_names(c.n_layers, c.vocab)) == sorted(W)
+    flat = fe.pack_params(W, c.n_layers, c.vocab)
+    assert flat.dtype == np.float32 and flat.size == fe.fe_param_count(_cfg(c))
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("d", 96, fe.FE_EUNSUPPORTED),          # width outside the supported set
+    ("n_heads", 3, fe.FE_EINVAL),           # d not divisible by heads
+    ("n_heads", 1, fe.FE_EUNSUPPORTED),     # head width 128
+    ("n_layers", 0, fe.FE_EINVAL),
+    ("n_layers", 9, fe.FE_EUNSUPPORTED),
+    ("ffn_dim", 320, fe.FE_EUNSUPPORTED),   # not a multiple of 128 on a bf16 model
+    ("max_L", 128, fe.FE_EUNSUPPORTED),
+    ("dtype", 7, fe.FE_EINVAL),
+])
+def test_config_validation(field, value, status):
+    c = gen.config(1)
+    with pytest.raises(fe.FeError) as e:
+        fe.fe_param_count(_cfg(c, **{field: value}))
+    assert e.value.status == status
+    assert fe.load_library().fe_last_error().decode()
+
+
+def test_bf16_needs_width_128():
+    c = gen.config(0)
+    with pytest.raises(fe.FeError) as e:
+        fe.fe_param_count(_cfg(c, dtype=fe.FE_BF16))
+    assert e.value.status == fe.FE_EUNSUPPORTED
+
+
+def test_null_config_is_einval():
+    n = ctypes.c_size_t()
+    assert fe.load_library().fe_param_count(None, ctypes.byref(n)) == fe.FE_EINVAL
+
+
+def test_trace_toggle_without_launches():
+    fe.fe_trace_enable(True)
+    out = fe.fe_trace_read()
+    fe.fe_trace_enable(False)
+    assert set(out) == {"gemm", "attention", "layernorm", "dedup", "gather", "assemble", "score_select", "fill", "ffn"}
+    assert all(v == (0.0, 0) for v in out.values())
