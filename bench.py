@@ -33,24 +33,23 @@ PEAK_HBM_GBS = 8000.0
 def algorithmic_work(c, U):
     """Per-step algorithmic flops per kernel family and bytes of the assembly, from the shapes.
 
-    U is the list of distinct-item counts of the B requests.  Projection flops: an encoder block
-    over R rows costs 24 R d^2 (q|k|v 6, output 2, FFN 16 with F = 4d); an item block 28 U d^2;
-    the key/value cache 4 n T d^2.  Attention flops: 4 nq nk d per block.
+    U is the list of distinct-item counts of the B requests.  Projection flops ("gemm"): an
+    encoder block over R rows costs 8 R d^2 (q|k|v 6, output 2), an item block 12 U d^2 (plus
+    the cross-attention query and output projections), the key/value cache 4 n T d^2.  FFN
+    flops ("ffn"): 4 R d F per block.  Attention flops: 4 nq nk d per block (QK^T and PV).
     """
     d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
-    enc = lambda R: R * d * d * (2 * 3 + 2) + 4.0 * R * d * F   # noqa: E731
-    gemm = 0.0
-    gemm += n * B * enc(T) + 4.0 * n * B * T * d * d
-    gemm += sum(n * (u * d * d * (2 * 3 + 2 + 2 + 2) + 4.0 * u * d * F) for u in U)
-    gemm += n * B * enc(K * S)
-    gemm += n * B * enc(K)
+    rows_enc = B * T + B * K * S + B * K            # context, sequence and cross blocks
+    rows_item = sum(U)
+    proj = n * 8.0 * d * d * rows_enc + n * 12.0 * d * d * rows_item + 4.0 * n * B * T * d * d
+    ffn = n * 4.0 * d * F * (rows_enc + rows_item)
     attn = 4.0 * n * B * T * T * d
     attn += sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U)
     attn += 4.0 * n * B * K * S * S * d
     attn += 4.0 * n * B * K * K * d
     esz = 2 if c.dtype == "bf16" else 4
     asm_bytes = B * K * S * d * esz + sum(U) * d * esz + B * K * c.L * 4
-    return {"gemm": gemm, "attention": attn}, asm_bytes
+    return {"gemm": proj, "ffn": ffn, "attention": attn}, asm_bytes
 
 
 def cpu_baseline(c, W, I, seconds: float):
@@ -191,7 +190,9 @@ def main() -> int:
             stages[name] = {"ms_per_step": round(ms / args.steps, 5), "launches_per_step": n // args.steps,
                             "avg_launch_us": round(ms * 1e3 / n, 3)}
         peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
-        for name in ("gemm", "attention"):
+        if "ffn" not in stages:                       # fp32 models run the FFN as two projections
+            flops = dict(flops, gemm=flops["gemm"] + flops["ffn"], ffn=0.0)
+        for name in ("gemm", "ffn", "attention"):
             if name in stages:
                 tf = flops[name] / (fam[name][0] / args.steps / 1e3) / 1e12
                 stages[name].update(tflops=round(tf, 2), mfma_frac=round(tf / peak, 4))
@@ -201,7 +202,7 @@ def main() -> int:
         dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
         dom_ms, dom_n = fam[dom]
         avg_s = dom_ms / dom_n / 1e3
-        if dom in flops:
+        if dom in flops and flops[dom] > 0:
             per_launch = flops[dom] / (dom_n / args.steps)
             ach = per_launch / avg_s / 1e12
             out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1),
@@ -213,8 +214,9 @@ def main() -> int:
             out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
                                "avg_launch_us": round(avg_s * 1e6, 3), "launches_per_step": dom_n // args.steps}
-        mm_ms = sum(fam[k][0] for k in ("gemm", "attention") if k in fam) / args.steps
-        out["mfma_util_matrix_stages"] = round((flops["gemm"] + flops["attention"]) / (mm_ms / 1e3) / 1e12 / peak, 4)
+        mm_ms = sum(fam[k][0] for k in ("gemm", "ffn", "attention") if k in fam) / args.steps
+        mm_flops = flops["gemm"] + flops["ffn"] + flops["attention"]
+        out["mfma_util_matrix_stages"] = round(mm_flops / (mm_ms / 1e3) / 1e12 / peak, 4)
         out["kernel_ms_per_step"] = round(sum(v[0] for v in fam.values()) / args.steps, 5)
         out["stages"] = stages
     if not args.no_cpu_baseline:

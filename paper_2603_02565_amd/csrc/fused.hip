@@ -17,90 +17,88 @@ namespace {
 constexpr int WG = 256;
 constexpr int APAD = 8;  // bf16 elements of padding per LDS row
 
+// Copy LayerNorm gains and offsets (D floats each) into LDS; visible after the next barrier.
+template <int D>
+FE_DEV void copy_ln_params(const float* g, const float* b, float* s_g, float* s_b) {
+  if (!g) return;
+  for (int i = threadIdx.x; i < D / 4; i += WG) {
+    reinterpret_cast<float4*>(s_g)[i] = reinterpret_cast<const float4*>(g)[i];
+    reinterpret_cast<float4*>(s_b)[i] = reinterpret_cast<const float4*>(b)[i];
+  }
+}
+
 // Stage rows row0..row0+TM-1 of A (fp32 or bf16, row stride lda) into LDS as bf16, as
-// LayerNorm(A) when g != nullptr.  Rows whose s_valid flag is 0 are written as zeros.
-template <int TM, int D>
-FE_DEV void stage_rows(const void* A, bool a_f32, long long lda, int row0, const int* s_valid, const float* g,
-                       const float* b, bf16* As) {
-  constexpr int TPR = WG / TM;             // threads per row
+// LayerNorm(A) when g != nullptr (g, b point at the LDS copies of the gains and offsets).
+// Rows whose s_valid flag is 0 are written as zeros.  The global loads of a thread (its row
+// slice) are unconditional vector loads, so they are in flight together.
+template <int TM, int D, typename TA>
+FE_DEV void stage_rows_t(const TA* A, long long lda, int row0, const int* s_valid, const float* g, const float* b,
+                         bf16* As) {
+  constexpr int TPR = WG / TM;                   // threads per row
+  constexpr int VE = 16 / sizeof(TA);            // elements per 16-byte vector
+  constexpr int NV = D / (VE * TPR);             // vectors per thread
+  static_assert(NV >= 1, "row too short for this tile");
   constexpr int LD = D + APAD;
   const int tid = threadIdx.x;
   const int rr = tid / TPR, part = tid % TPR;
   const bool valid = s_valid[rr];
-  const long long r = row0 + rr;
-  if (a_f32) {
-    constexpr int NV = D / (4 * TPR);      // float4 vectors per thread
-    float v[NV * 4];
-    const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(A) + r * lda);
+  // padding rows read row0 (always a valid row of the tile) and are zeroed below
+  const long long r = valid ? row0 + rr : row0;
+  float v[NV * VE];
+  const uint4* src = reinterpret_cast<const uint4*>(A + r * lda);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      float4 t = valid ? src[i * TPR + part] : make_float4(0.f, 0.f, 0.f, 0.f);
-      v[4 * i] = t.x; v[4 * i + 1] = t.y; v[4 * i + 2] = t.z; v[4 * i + 3] = t.w;
-    }
-    float mean = 0.f, rstd = 1.f;
-    if (g) {
-      float s = 0.f;
+  for (int i = 0; i < NV; ++i) {
+    const uint4 t = src[i * TPR + part];
+    const TA* e = reinterpret_cast<const TA*>(&t);
 #pragma unroll
-      for (int i = 0; i < NV * 4; ++i) s += v[i];
+    for (int j = 0; j < VE; ++j) v[i * VE + j] = (float)e[j];
+  }
+  if (g) {
+    float s = 0.f;
 #pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
-      mean = s / (float)D;
-      float q = 0.f;
+    for (int i = 0; i < NV * VE; ++i) s += v[i];
 #pragma unroll
-      for (int i = 0; i < NV * 4; ++i) { const float t = v[i] - mean; q += t * t; }
+    for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
+    const float mean = s / (float)D;
+    float q = 0.f;
 #pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) q += __shfl_xor(q, o, 64);
-      rstd = rsqrtf(q / (float)D + 1e-5f);
-    }
+    for (int i = 0; i < NV * VE; ++i) { const float t = v[i] - mean; q += t * t; }
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int k = (i * TPR + part) * 4;
+    for (int o = 1; o < TPR; o <<= 1) q += __shfl_xor(q, o, 64);
+    const float rstd = rsqrtf(q / (float)D + 1e-5f);
+    const float4* g4 = reinterpret_cast<const float4*>(g);   // LDS copies (copy_ln_params)
+    const float4* b4 = reinterpret_cast<const float4*>(b);
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+      for (int h = 0; h < VE / 4; ++h) {
+        const int idx = (i * TPR + part) * (VE / 4) + h;
+        const float4 gg = g4[idx], bb = b4[idx];
+        float* x = &v[i * VE + 4 * h];
+        x[0] = (x[0] - mean) * rstd * gg.x + bb.x;
+        x[1] = (x[1] - mean) * rstd * gg.y + bb.y;
+        x[2] = (x[2] - mean) * rstd * gg.z + bb.z;
+        x[3] = (x[3] - mean) * rstd * gg.w + bb.w;
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int k = (i * TPR + part) * VE;
+#pragma unroll
+    for (int h = 0; h < VE / 4; ++h) {
       bf16x4 o;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float y = g ? (v[4 * i + j] - mean) * rstd * g[k + j] + b[k + j] : v[4 * i + j];
-        o[j] = valid ? (bf16)y : (bf16)0.f;
-      }
-      *reinterpret_cast<bf16x4*>(&As[rr * LD + k]) = o;
-    }
-  } else {
-    constexpr int NV = D / (8 * TPR);      // 8 x bf16 vectors per thread
-    static_assert(NV >= 1, "row too short for this tile");
-    float v[NV * 8];
-    const bf16x8* src = reinterpret_cast<const bf16x8*>(static_cast<const bf16*>(A) + r * lda);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      bf16x8 t = valid ? src[i * TPR + part] : bf16x8{};
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[8 * i + j] = (float)t[j];
-    }
-    float mean = 0.f, rstd = 1.f;
-    if (g) {
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < NV * 8; ++i) s += v[i];
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
-      mean = s / (float)D;
-      float q = 0.f;
-#pragma unroll
-      for (int i = 0; i < NV * 8; ++i) { const float t = v[i] - mean; q += t * t; }
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) q += __shfl_xor(q, o, 64);
-      rstd = rsqrtf(q / (float)D + 1e-5f);
-    }
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int k = (i * TPR + part) * 8;
-      bf16x8 o;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float y = g ? (v[8 * i + j] - mean) * rstd * g[k + j] + b[k + j] : v[8 * i + j];
-        o[j] = valid ? (bf16)y : (bf16)0.f;
-      }
-      *reinterpret_cast<bf16x8*>(&As[rr * LD + k]) = o;
+      for (int j = 0; j < 4; ++j) o[j] = valid ? (bf16)v[i * VE + 4 * h + j] : (bf16)0.f;
+      *reinterpret_cast<bf16x4*>(&As[rr * LD + k + 4 * h]) = o;
     }
   }
+}
+
+template <int TM, int D>
+FE_DEV void stage_rows(const void* A, bool a_f32, long long lda, int row0, const int* s_valid, const float* g,
+                       const float* b, bf16* As) {
+  if (a_f32) stage_rows_t<TM, D>(static_cast<const float*>(A), lda, row0, s_valid, g, b, As);
+  else stage_rows_t<TM, D>(static_cast<const bf16*>(A), lda, row0, s_valid, g, b, As);
 }
 
 FE_DEV bf16x8 a_frag(const bf16* As, int ld, int row_base, int k0, int lane) {
@@ -128,72 +126,133 @@ FE_DEV bool mark_rows(int row0, int R, const int32_t* nvalid, int rpb, int* s_va
 
 // ------------------------------------------------------------------------------------------
 // C = epi(LN(A) W + bias) for K = D, any N that is a multiple of 32.
+//
+// Wave w owns the 32-column blocks w, w+4, w+8, ...; they are processed NBW at a time.  The
+// weight fragments are streamed through registers in stages of 16 fragments (NBW column
+// blocks x KB k-steps), double-buffered: the loads of stage t+1 are issued before the matrix
+// instructions of stage t, and stage 0 is requested before the A tile is staged, so its
+// latency hides behind the row loads and the LayerNorm.
 // ------------------------------------------------------------------------------------------
-template <int TM, int D>
+template <int TM, int D, int EPI>
 __global__ __launch_bounds__(WG) void k_proj(GemmArgs a) {
-  constexpr int RB = TM / 32, KS = D / 16, LD = D + APAD, NBW = 4 / RB;   // 4 accumulator blocks per wave
+  constexpr int RB = TM / 32, KS = D / 16, LD = D + APAD, NBW = 4 / RB;
+  constexpr int KB = 16 / NBW < KS ? 16 / NBW : KS;   // k-steps per stage
+  constexpr int NSK = KS / KB;                         // stages per column group
   __shared__ __attribute__((aligned(16))) bf16 As[TM * LD];
+  __shared__ __attribute__((aligned(16))) float s_g[D], s_b[D];
+  __shared__ __attribute__((aligned(16))) float Cs[4 * TM * 33];   // per-wave output staging
   __shared__ int s_valid[TM];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int row0 = blockIdx.x * TM;
-  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
-  stage_rows<TM, D>(a.A, a.a_f32, a.lda, row0, s_valid, a.ln_g, a.ln_b, As);
-  __syncthreads();
-
   const bf16* Wp = static_cast<const bf16*>(a.Wt);
   const int ncb = a.N / 32;
-  for (int cb0 = wave; cb0 < ncb; cb0 += 4 * NBW) {
-    f32x16 acc[RB][NBW];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) acc[rb][j] = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      bf16x8 af[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) af[rb] = a_frag(As, LD, rb * 32, ks * 16, lane);
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) {
-        const int cb = cb0 + 4 * j;
-        if (cb < ncb) {
-          const bf16x8 bfr = b_frag(Wp, KS, cb, ks, lane);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) acc[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[rb], bfr, acc[rb][j], 0, 0, 0);
-        }
-      }
-    }
+  const int ngroups = wave < ncb ? (ncb - wave + 4 * NBW - 1) / (4 * NBW) : 0;
+  const int nstages = ngroups * NSK;
+
+  bf16x8 cur[NBW][KB], nxt[NBW][KB];
+  auto load_stage = [&](int t, bf16x8 (&buf)[NBW][KB]) {
+    const int gi = t / NSK, sk = t % NSK;
 #pragma unroll
     for (int j = 0; j < NBW; ++j) {
-      const int cb = cb0 + 4 * j;
-      if (cb >= ncb) continue;
-      const int n = cb * 32 + (lane & 31);
-      const float bias = a.bias ? a.bias[n] : 0.f;
-      const long long cofs = (long long)(n / a.col_block) * a.col_block_stride + (n % a.col_block);
+      const int cb = min(wave + 4 * (gi * NBW + j), ncb - 1);   // clamped: always a real block
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk) buf[j][kk] = b_frag(Wp, KS, cb, sk * KB + kk, lane);
+    }
+  };
+  if (nstages > 0) load_stage(0, cur);
+
+  copy_ln_params<D>(a.ln_g, a.ln_b, s_g, s_b);
+  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
+  stage_rows<TM, D>(a.A, a.a_f32, a.lda, row0, s_valid, a.ln_g ? s_g : nullptr, s_b, As);
+  __syncthreads();
+
+  f32x16 acc[RB][NBW];
+  for (int t = 0; t < nstages; ++t) {
+    const int gi = t / NSK, sk = t % NSK;
+    if (t + 1 < nstages) load_stage(t + 1, nxt);
+    if (sk == 0) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int rr = rb * 32 + acc_row(i, lane);
+        for (int j = 0; j < NBW; ++j) acc[rb][j] = f32x16{};
+    }
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk) {
+      bf16x8 af[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) af[rb] = a_frag(As, LD, rb * 32, (sk * KB + kk) * 16, lane);
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          acc[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[rb], cur[j][kk], acc[rb][j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < NBW; ++j)
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk) cur[j][kk] = nxt[j][kk];
+    if (sk != NSK - 1) continue;
+
+    // ---- epilogue of column group gi: each 32-column block goes through the wave's LDS
+    // staging area and leaves as row-contiguous 16-byte vectors
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+      const int cb = wave + 4 * (gi * NBW + j);
+      if (cb >= ncb) continue;
+      const float bias = a.bias ? a.bias[cb * 32 + (lane & 31)] : 0.f;
+      float* st = &Cs[wave * TM * 33];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) st[(rb * 32 + acc_row(i, lane)) * 33 + (lane & 31)] = acc[rb][j][i] + bias;
+      __builtin_amdgcn_wave_barrier();
+      if constexpr (EPI == EPI_RESID) {
+        // fp32 out = residual + value: 8 lanes x float4 per 32-column row segment
+#pragma unroll
+        for (int it = 0; it < TM * 8 / 64; ++it) {
+          const int e = it * 64 + lane, rr = e >> 3, c4 = (e & 7) * 4;
           if (!s_valid[rr]) continue;
           const long long r = row0 + rr;
-          float v = acc[rb][j][i] + bias;
-          if (a.epi == EPI_RESID) {
-            const long long ro = r * a.ldr + n;
-            const float res = a.res_f32 ? static_cast<const float*>(a.res)[ro] : (float)static_cast<const bf16*>(a.res)[ro];
-            static_cast<float*>(a.C)[r * a.ldc + n] = res + v;
+          const int n = cb * 32 + c4;
+          float4 res;
+          if (a.res_f32) {
+            res = *reinterpret_cast<const float4*>(static_cast<const float*>(a.res) + r * a.ldr + n);
           } else {
-            if (a.epi == EPI_RELU) v = fmaxf(v, 0.f);
-            if (a.c_f32) static_cast<float*>(a.C)[cofs + r * a.ldc] = v;
-            else static_cast<bf16*>(a.C)[cofs + r * a.ldc] = (bf16)v;
+            const bf16x4 rb4 = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(a.res) + r * a.ldr + n);
+            res = make_float4((float)rb4[0], (float)rb4[1], (float)rb4[2], (float)rb4[3]);
           }
+          const float* sv = &st[rr * 33 + c4];
+          *reinterpret_cast<float4*>(static_cast<float*>(a.C) + r * a.ldc + n) =
+              make_float4(res.x + sv[0], res.y + sv[1], res.z + sv[2], res.w + sv[3]);
         }
+      } else {
+        // bf16 out: 4 lanes x 8 values per 32-column row segment
+#pragma unroll
+        for (int it = 0; it < TM * 4 / 64; ++it) {
+          const int e = it * 64 + lane, rr = e >> 2, c8 = (e & 3) * 8;
+          if (!s_valid[rr]) continue;
+          const int n = cb * 32 + c8;
+          const float* sv = &st[rr * 33 + c8];
+          bf16x8 o;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) o[q] = (bf16)(EPI == EPI_RELU ? fmaxf(sv[q], 0.f) : sv[q]);
+          const long long cofs = (long long)(n / a.col_block) * a.col_block_stride + (n % a.col_block);
+          *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.C) + cofs + (long long)(row0 + rr) * a.ldc) = o;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
     }
   }
 }
 
 // ------------------------------------------------------------------------------------------
 // X += W2 ReLU(LN(X) W1 + b1) + b2 over TM = 64 rows, hidden produced 128 columns at a time.
+//
+// Per 128-column hidden chunk: phase H (wave w: hidden columns 32w..32w+31 of the chunk for
+// all 64 rows, written to LDS after bias and ReLU) and phase O (wave w: its D/4 output columns
+// accumulated over the chunk).  Every phase's weight fragments are requested one phase ahead
+// (W2 of chunk c during phase H of c, W1 of chunk c+1 during phase O of c), each into the
+// register set the previous phase has just released.
 // ------------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(WG) void k_ffn(FfnArgs a) {
@@ -201,34 +260,52 @@ __global__ __launch_bounds__(WG) void k_ffn(FfnArgs a) {
   constexpr int OCB = D / 128;             // output column blocks per wave
   __shared__ __attribute__((aligned(16))) bf16 As[TM * LD];
   __shared__ __attribute__((aligned(16))) bf16 Hs[TM * HLD];
+  __shared__ __attribute__((aligned(16))) float s_g[D], s_b[D];
+  __shared__ __attribute__((aligned(16))) float Cs[4 * TM * 33];   // per-wave output staging
   __shared__ int s_valid[TM];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int row0 = blockIdx.x * TM;
-  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
-  stage_rows<TM, D>(a.X, true, D, row0, s_valid, a.ln_g, a.ln_b, As);
-  __syncthreads();
-
   const bf16* W1 = static_cast<const bf16*>(a.W1p);
   const bf16* W2 = static_cast<const bf16*>(a.W2p);
   const int KS2 = a.F / 16;
+  const int nchunks = a.F / HC;
+
+  bf16x8 w1[KS], w2[OCB][HC / 16];
+  auto load_w1 = [&](int c) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) w1[ks] = b_frag(W1, KS, c * 4 + wave, ks, lane);
+  };
+  auto load_w2 = [&](int c) {
+#pragma unroll
+    for (int j = 0; j < OCB; ++j)
+#pragma unroll
+      for (int ks = 0; ks < HC / 16; ++ks) w2[j][ks] = b_frag(W2, KS2, wave + 4 * j, c * (HC / 16) + ks, lane);
+  };
+  load_w1(0);
+
+  copy_ln_params<D>(a.ln_g, a.ln_b, s_g, s_b);
+  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
+  stage_rows<TM, D>(a.X, true, D, row0, s_valid, s_g, s_b, As);
+  load_w2(0);
+  __syncthreads();
+
   f32x16 acc_o[RB][OCB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int j = 0; j < OCB; ++j) acc_o[rb][j] = f32x16{};
 
-  for (int h0 = 0; h0 < a.F; h0 += HC) {
-    // hidden columns h0 + 32*wave .. +31 for all 64 rows
-    const int cbh = h0 / 32 + wave;
+  for (int c = 0; c < nchunks; ++c) {
+    const int cbh = c * 4 + wave;
+    const float bias1 = a.b1[cbh * 32 + (lane & 31)];
     f32x16 acc_h[RB] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 bfr = b_frag(W1, KS, cbh, ks, lane);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
-        acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_frag(As, LD, rb * 32, ks * 16, lane), bfr, acc_h[rb], 0, 0, 0);
+        acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_frag(As, LD, rb * 32, ks * 16, lane), w1[ks], acc_h[rb], 0, 0, 0);
     }
-    const float bias1 = a.b1[cbh * 32 + (lane & 31)];
+    if (c + 1 < nchunks) load_w1(c + 1);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -241,50 +318,69 @@ __global__ __launch_bounds__(WG) void k_ffn(FfnArgs a) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) af[rb] = a_frag(Hs, HLD, rb * 32, ks * 16, lane);
 #pragma unroll
-      for (int j = 0; j < OCB; ++j) {
-        const bf16x8 bfr = b_frag(W2, KS2, wave + 4 * j, h0 / 16 + ks, lane);
+      for (int j = 0; j < OCB; ++j)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) acc_o[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[rb], bfr, acc_o[rb][j], 0, 0, 0);
-      }
+        for (int rb = 0; rb < RB; ++rb) acc_o[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[rb], w2[j][ks], acc_o[rb][j], 0, 0, 0);
     }
+    if (c + 1 < nchunks) load_w2(c + 1);
     __syncthreads();
   }
   float* X = a.X;
+  float* st = &Cs[wave * TM * 33];
 #pragma unroll
   for (int j = 0; j < OCB; ++j) {
-    const int n = (wave + 4 * j) * 32 + (lane & 31);
-    const float bias2 = a.b2[n];
+    const int cb = wave + 4 * j;
+    const float bias2 = a.b2[cb * 32 + (lane & 31)];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int rr = rb * 32 + acc_row(i, lane);
-        if (!s_valid[rr]) continue;
-        float* p = X + (long long)(row0 + rr) * D + n;
-        *p = *p + acc_o[rb][j][i] + bias2;
-      }
+      for (int i = 0; i < 16; ++i) st[(rb * 32 + acc_row(i, lane)) * 33 + (lane & 31)] = acc_o[rb][j][i] + bias2;
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int it = 0; it < TM * 8 / 64; ++it) {
+      const int e = it * 64 + lane, rr = e >> 3, c4 = (e & 7) * 4;
+      if (!s_valid[rr]) continue;
+      float4* p = reinterpret_cast<float4*>(X + (long long)(row0 + rr) * D + cb * 32 + c4);
+      const float4 x = *p;
+      const float* sv = &st[rr * 33 + c4];
+      *p = make_float4(x.x + sv[0], x.y + sv[1], x.z + sv[2], x.w + sv[3]);
+    }
+    __builtin_amdgcn_wave_barrier();
   }
+}
+
+template <int TM, int D>
+hipError_t launch_proj_d(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((a.R + TM - 1) / TM);
+  switch (a.epi) {
+    case EPI_STORE: hipLaunchKernelGGL((k_proj<TM, D, EPI_STORE>), grid, dim3(WG), 0, s, a); break;
+    case EPI_RELU: hipLaunchKernelGGL((k_proj<TM, D, EPI_RELU>), grid, dim3(WG), 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((k_proj<TM, D, EPI_RESID>), grid, dim3(WG), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <int TM>
 hipError_t launch_proj_tm(const GemmArgs& a, hipStream_t s) {
-  dim3 grid((a.R + TM - 1) / TM);
+  if (a.c_f32 && a.epi != EPI_RESID) return hipErrorInvalidValue;   // fp32 output only through the residual
   switch (a.K) {
-    case 128: hipLaunchKernelGGL((k_proj<TM, 128>), grid, dim3(WG), 0, s, a); break;
-    case 256: hipLaunchKernelGGL((k_proj<TM, 256>), grid, dim3(WG), 0, s, a); break;
-    case 512: hipLaunchKernelGGL((k_proj<TM, 512>), grid, dim3(WG), 0, s, a); break;
+    case 128: return launch_proj_d<TM, 128>(a, s);
+    case 256: return launch_proj_d<TM, 256>(a, s);
+    case 512:
+      if constexpr (TM == 32) return launch_proj_d<TM, 512>(a, s);
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_proj(const GemmArgs& a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
-  // small row counts: 32-row tiles to put more workgroups on the 256 compute units
-  if ((a.R + 63) / 64 < 512) return launch_proj_tm<32>(a, s);
-  return launch_proj_tm<64>(a, s);
+  // 32-row tiles: two workgroups fit per compute unit (a 64-row tile needs all 512 registers
+  // of a lane and runs one wave per SIMD) and small batches still spread over 256 units
+  return launch_proj_tm<32>(a, s);
 }
 
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s) {

@@ -85,16 +85,19 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     // ---- stage A (LayerNorm applied, rounded to the operand type) in groups of 4 along k
     for (int gi = tid; gi < TM * KC / 4; gi += 256) {
       const int rr = gi / (KC / 4), kk = (gi % (KC / 4)) * 4;
-      float v[4] = {0.f, 0.f, 0.f, 0.f};
-      if (s_valid[rr]) {
-        load4(A + ((size_t)(row0 + rr) * a.lda + k0 + kk) * asz, a_f32, v);
-        if (ln) {
-          const float mu = s_mean[rr], rs = s_rstd[rr];
-          for (int j = 0; j < 4; ++j) v[j] = (v[j] - mu) * rs * a.ln_g[k0 + kk + j] + a.ln_b[k0 + kk + j];
-        }
+      // padding rows load row0 (inside the tile's allocation) and are stored as zeros
+      const bool ok = s_valid[rr];
+      float v[4];
+      load4(A + ((size_t)(ok ? row0 + rr : row0) * a.lda + k0 + kk) * asz, a_f32, v);
+      if (ln) {
+        const float4 gg = *reinterpret_cast<const float4*>(a.ln_g + k0 + kk);
+        const float4 bb = *reinterpret_cast<const float4*>(a.ln_b + k0 + kk);
+        const float mu = s_mean[rr], rs = s_rstd[rr];
+        v[0] = (v[0] - mu) * rs * gg.x + bb.x; v[1] = (v[1] - mu) * rs * gg.y + bb.y;
+        v[2] = (v[2] - mu) * rs * gg.z + bb.z; v[3] = (v[3] - mu) * rs * gg.w + bb.w;
       }
       T* dst = &As[rr * LDS_LD + kk];
-      for (int j = 0; j < 4; ++j) dst[j] = from_f32<T>(v[j]);
+      for (int j = 0; j < 4; ++j) dst[j] = from_f32<T>(ok ? v[j] : 0.f);
     }
     // ---- stage W^T rows col0..col0+TN, 16 bytes per load
     constexpr int VB = 16 / sizeof(T);
