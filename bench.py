@@ -52,6 +52,48 @@ def algorithmic_work(c, U):
     return {"gemm": proj, "ffn": ffn, "attention": attn}, asm_bytes
 
 
+def family_flops(c, U, fam_names):
+    """Split the algorithmic flops over the kernel families that ran.
+
+    Fused kernels take the work of the stages they contain: "layer" (whole blocks of short
+    groups: the sequence encoder and, when its groups are short, the cross-sequence module),
+    "post" (output projection and FFN / query projection of long-group blocks).
+    """
+    d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
+    tile = 32 if d >= 512 else 64
+    rows_item = sum(U)
+    out = {k: 0.0 for k in fam_names}
+
+    def add(fam, v):
+        out[fam] = out.get(fam, 0.0) + v
+
+    fused = "layer" in fam_names or "post" in fam_names
+    # context: QKV projection + attention + tail; key/value cache projection
+    for mod_rows, group, attn in ((B * T, T, 4.0 * n * B * T * T * d), (B * K * S, S, 4.0 * n * B * K * S * S * d),
+                                  (B * K, K, 4.0 * n * B * K * K * d)):
+        if fused and group <= tile:
+            add("layer", n * (8.0 * d * d + 4.0 * d * F) * mod_rows + attn)
+        elif fused:
+            add("gemm", n * 6.0 * d * d * mod_rows)
+            add("attention", attn)
+            add("post", n * (2.0 * d * d + 4.0 * d * F) * mod_rows)
+        else:
+            add("gemm", n * 8.0 * d * d * mod_rows)
+            add("attention", attn)
+            add("ffn" if "ffn" in fam_names else "gemm", n * 4.0 * d * F * mod_rows)
+    add("gemm", 4.0 * n * B * T * d * d)
+    # distinct items: QKV, self-attention, O + query projection, cross-attention, O2 + FFN
+    item_attn = sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U)
+    add("attention", item_attn)
+    if fused:
+        add("gemm", n * 6.0 * d * d * rows_item)
+        add("post", n * (6.0 * d * d + 4.0 * d * F) * rows_item)
+    else:
+        add("gemm", n * 12.0 * d * d * rows_item)
+        add("ffn" if "ffn" in fam_names else "gemm", n * 4.0 * d * F * rows_item)
+    return out
+
+
 def cpu_baseline(c, W, I, seconds: float):
     """The float64 oracle, in its candidate-factorised order, on this host for a bounded time.
 
@@ -190,10 +232,9 @@ def main() -> int:
             stages[name] = {"ms_per_step": round(ms / args.steps, 5), "launches_per_step": n // args.steps,
                             "avg_launch_us": round(ms * 1e3 / n, 3)}
         peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
-        if "ffn" not in stages:                       # fp32 models run the FFN as two projections
-            flops = dict(flops, gemm=flops["gemm"] + flops["ffn"], ffn=0.0)
-        for name in ("gemm", "ffn", "attention"):
-            if name in stages:
+        flops = family_flops(c, U, set(stages))
+        for name in ("gemm", "ffn", "attention", "layer", "post"):
+            if name in stages and flops.get(name, 0.0) > 0:
                 tf = flops[name] / (fam[name][0] / args.steps / 1e3) / 1e12
                 stages[name].update(tflops=round(tf, 2), mfma_frac=round(tf / peak, 4))
         if "assemble" in stages:
@@ -202,7 +243,7 @@ def main() -> int:
         dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
         dom_ms, dom_n = fam[dom]
         avg_s = dom_ms / dom_n / 1e3
-        if dom in flops and flops[dom] > 0:
+        if flops.get(dom, 0.0) > 0:
             per_launch = flops[dom] / (dom_n / args.steps)
             ach = per_launch / avg_s / 1e12
             out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1),
@@ -214,8 +255,9 @@ def main() -> int:
             out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
                                "avg_launch_us": round(avg_s * 1e6, 3), "launches_per_step": dom_n // args.steps}
-        mm_ms = sum(fam[k][0] for k in ("gemm", "ffn", "attention") if k in fam) / args.steps
-        mm_flops = flops["gemm"] + flops["ffn"] + flops["attention"]
+        mm_fams = [k for k in ("gemm", "ffn", "attention", "layer", "post") if k in stages]
+        mm_ms = sum(fam[k][0] for k in mm_fams) / args.steps
+        mm_flops = sum(flops.get(k, 0.0) for k in mm_fams)
         out["mfma_util_matrix_stages"] = round(mm_flops / (mm_ms / 1e3) / 1e12 / peak, 4)
         out["kernel_ms_per_step"] = round(sum(v[0] for v in fam.values()) / args.steps, 5)
         out["stages"] = stages

@@ -26,9 +26,9 @@ thread_local std::string g_err;
 // ------------------------------------------------------------------------------------------
 // Kernel timing (flasheval_trace.h): events recorded around each launch while enabled.
 // ------------------------------------------------------------------------------------------
-enum Fam { F_GEMM = 0, F_ATTN, F_LN, F_DEDUP, F_GATHER, F_ASSEMBLE, F_SCORE, F_FILL, F_FFN };
-const char* const kFamName[FE_TRACE_FAMILIES] = {"gemm", "attention", "layernorm", "dedup", "gather",
-                                                 "assemble", "score_select", "fill", "ffn"};
+enum Fam { F_GEMM = 0, F_ATTN, F_LN, F_DEDUP, F_GATHER, F_ASSEMBLE, F_SCORE, F_FILL, F_FFN, F_LAYER, F_POST };
+const char* const kFamName[FE_TRACE_FAMILIES] = {"gemm", "attention", "layernorm", "dedup", "gather", "assemble",
+                                                 "score_select", "fill", "ffn", "layer", "post"};
 struct TraceRec { int fam; hipEvent_t a, b; };
 std::mutex g_trace_mu;
 bool g_trace_on = false;
@@ -409,6 +409,14 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   const int d = m->cfg.d, F = m->cfg.ffn_dim, R = nb * per;
   const bool bf = m->bf16;
   const size_t e = bf ? 2 : 4;
+  const float scale = 1.0f / sqrtf((float)(d / m->cfg.n_heads));
+  if (bf && !nvalid && per <= layer_small_tile_rows(d)) {
+    // short groups: the whole block in one kernel
+    LayerArgs la{xin, xin_f32, b.X, nb, per, 0, d, m->cfg.n_heads, F, scale, w.ln1g, w.ln1b, w.wqkv, w.bqkv,
+                 w.wo, w.bo, w.ln2g, w.ln2b, w.w1, w.b1, w.w2, w.b2};
+    FE_LAUNCH(F_LAYER, s, launch_layer_small(la, s));
+    return FE_OK;
+  }
   GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
   g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
   fe_status st0 = run_proj(m, g, s);
@@ -420,8 +428,15 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   a.O = b.O; a.o_bs = (long long)per * d; a.o_rs = d;
   a.B = nb; a.nq = per; a.nk = per; a.n_heads = m->cfg.n_heads; a.dh = d / m->cfg.n_heads;
   a.q_valid = nvalid; a.k_valid = nvalid;
-  a.scale = 1.0f / sqrtf((float)a.dh);
+  a.scale = scale;
   FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+  if (bf) {
+    // output projection, residual, LN2 and FFN in one kernel
+    PostArgs p{b.O, xin, xin_f32, b.X, R, per, nvalid, d, F, 0, w.wo, w.bo, w.ln2g, w.ln2b,
+               w.w1, w.b1, w.w2, w.b2, nullptr, nullptr, nullptr};
+    FE_LAUNCH(F_POST, s, launch_post(p, s));
+    return FE_OK;
+  }
   g = gemm(b.O, d, false, R, d, d, w.wo, w.bo, b.X, d, true, EPI_RESID);
   g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = nvalid; g.rows_per_batch = per;
   fe_status st = run_proj(m, g, s);
@@ -668,15 +683,22 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     a.q_valid = n_uniq; a.k_valid = n_uniq;
     a.scale = 1.0f / sqrtf((float)dh);
     FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
-    g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
-    g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-    st = run_proj(m, g, s);
-    if (st != FE_OK) return st;
-    // cross-attention: the distinct elements are the queries, the context cache the keys/values
-    g = gemm(G, d, true, R, d, d, iw.wq, iw.bq, Qc, d, false, EPI_STORE);
-    g.ln_g = iw.ln2g; g.ln_b = iw.ln2b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-    st = run_proj(m, g, s);
-    if (st != FE_OK) return st;
+    if (bf) {
+      // x1 = x + O Wo + bo -> G, and the cross-attention queries q = LN2(x1) Wq + bq -> Qc
+      PostArgs p{O, xin, xin_f32, G, R, Ucap, n_uniq, d, F, 1, iw.wo, iw.bo, iw.ln2g, iw.ln2b,
+                 nullptr, nullptr, nullptr, nullptr, iw.wq, iw.bq, Qc};
+      FE_LAUNCH(F_POST, s, launch_post(p, s));
+    } else {
+      g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
+      g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+      st = run_proj(m, g, s);
+      if (st != FE_OK) return st;
+      // cross-attention: the distinct elements are the queries, the context cache the keys/values
+      g = gemm(G, d, true, R, d, d, iw.wq, iw.bq, Qc, d, false, EPI_STORE);
+      g.ln_g = iw.ln2g; g.ln_b = iw.ln2b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+      st = run_proj(m, g, s);
+      if (st != FE_OK) return st;
+    }
     AttnArgs c{};
     c.Q = Qc; c.q_bs = (long long)Ucap * d; c.q_rs = d;
     c.K = static_cast<const char*>(kv) + (size_t)(2 * l) * B * T * d * e; c.k_bs = (long long)T * d; c.k_rs = d;
@@ -686,6 +708,12 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     c.q_valid = n_uniq; c.k_valid = nullptr;
     c.scale = 1.0f / sqrtf((float)dh);
     FE_LAUNCH(F_ATTN, s, launch_attention(c, bf, s));
+    if (bf) {
+      PostArgs p{O, G, 1, G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
+                 iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr};
+      FE_LAUNCH(F_POST, s, launch_post(p, s));
+      continue;
+    }
     g = gemm(O, d, false, R, d, d, iw.wo2, iw.bo2, G, d, true, EPI_RESID);
     g.res = G; g.ldr = d; g.res_f32 = true; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
     st = run_proj(m, g, s);

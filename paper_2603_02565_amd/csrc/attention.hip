@@ -1,6 +1,7 @@
 // Multi-head scaled dot-product attention with a key padding mask and online softmax.
 //
-// One wave owns 16 queries of one (batch, head); a workgroup holds WAVES waves that share the
+// fp32 models (k_attention): one wave owns 16 queries of one (batch, head); a workgroup holds
+// WAVES waves that share the
 // (batch, head) and walk the keys in blocks of 32.  For each block the wave computes the
 // transposed score tile S^T = K Q^T with matrix-core instructions (keys are rows, so every lane
 // ends up holding scores of ONE query), updates that query's running max / sum in fp32, and
@@ -155,6 +156,169 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention(AttnArgs a) {
     for (int j = 0; j < 4; ++j) Ob[i * 16 + g * 4 + j] = from_f32<T>(o[i][j] * inv);
 }
 
+// ------------------------------------------------------------------------------------------
+// bf16 models: a workgroup owns one (batch, head) and up to WAVES*QT*16 queries.  Keys are
+// walked in chunks of KC that the whole workgroup stages once in LDS (K row-major, V
+// transposed) and every query tile of every wave consumes; the next chunk is fetched into
+// registers while the current one is in use.  Per 32-key block the wave runs the same
+// transposed score / probability / output scheme as above.
+// ------------------------------------------------------------------------------------------
+template <int DH, int WAVES, int QT, int KC>
+__global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
+  constexpr int NT = WAVES * 64;
+  constexpr int KLD = DH + 8, VLD = KC + 8, NB = DH / 16;
+  constexpr int PER_T = KC * DH / 8 / NT;         // 16-byte vectors per thread per tensor
+  static_assert(PER_T >= 1 && KC * DH / 8 % NT == 0, "chunk does not split over the workgroup");
+  __shared__ __attribute__((aligned(16))) bf16 Ks[KC * KLD];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VLD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, q_in = lane & 15;
+  const int per_group = WAVES * QT * 16;
+  const int groups = (a.nq + per_group - 1) / per_group;
+  const int qg = blockIdx.x % groups, bh = blockIdx.x / groups;
+  const int h = bh % a.n_heads, b = bh / a.n_heads;
+  int nq = a.nq, nk = a.nk;
+  if (a.q_valid) nq = min(nq, a.q_valid[b]);
+  if (a.k_valid) nk = min(nk, a.k_valid[b]);
+  if (qg * per_group >= nq || nk <= 0) return;     // uniform over the workgroup
+
+  const bf16* Qb = static_cast<const bf16*>(a.Q) + b * a.q_bs + h * DH;
+  const bf16* Kb = static_cast<const bf16*>(a.K) + b * a.k_bs + h * DH;
+  const bf16* Vb = static_cast<const bf16*>(a.V) + b * a.v_bs + h * DH;
+  const float sl2 = a.scale * kLog2e;
+
+  // query tile t of this wave: rows q0(t) .. q0(t)+15
+  auto q0_of = [&](int t) { return qg * per_group + (t * WAVES + wave) * 16; };
+  bf16x8 qf[QT][DH / 32];
+  float m_run[QT], l_run[QT];
+  f32x4 o[QT][NB];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int qrow = q0_of(t) + q_in;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+      qf[t][c] = qrow < nq ? *reinterpret_cast<const bf16x8*>(Qb + (long long)qrow * a.q_rs + c * 32 + g * 8) : bf16x8{};
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) o[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  uint4 kreg[PER_T], vreg[PER_T];
+  auto load_chunk = [&](int c0) {
+#pragma unroll
+    for (int p = 0; p < PER_T; ++p) {
+      const int e = p * NT + tid, key = e / (DH / 8), d0 = (e % (DH / 8)) * 8;
+      const bool ok = c0 + key < nk;
+      kreg[p] = ok ? *reinterpret_cast<const uint4*>(Kb + (long long)(c0 + key) * a.k_rs + d0) : make_uint4(0, 0, 0, 0);
+      vreg[p] = ok ? *reinterpret_cast<const uint4*>(Vb + (long long)(c0 + key) * a.v_rs + d0) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  load_chunk(0);
+
+  for (int c0 = 0; c0 < nk; c0 += KC) {
+    __syncthreads();                                  // the previous chunk is no longer read
+#pragma unroll
+    for (int p = 0; p < PER_T; ++p) {
+      const int e = p * NT + tid, key = e / (DH / 8), d0 = (e % (DH / 8)) * 8;
+      *reinterpret_cast<uint4*>(&Ks[key * KLD + d0]) = kreg[p];
+      const bf16* v = reinterpret_cast<const bf16*>(&vreg[p]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) Vt[(d0 + i) * VLD + key] = v[i];
+    }
+    __syncthreads();
+    if (c0 + KC < nk) load_chunk(c0 + KC);
+    const int nkeys = min(KC, nk - c0);
+
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      if (q0_of(t) >= nq) continue;
+      for (int kb = 0; kb < nkeys; kb += 32) {
+        const int r = lane & 15;
+        const int k0 = kb + (r >> 2) * 8 + (r & 3), k1 = k0 + 4;
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < DH / 32; ++c) {
+          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&Ks[k0 * KLD + c * 32 + g * 8]);
+          const bf16x8 kb8 = *reinterpret_cast<const bf16x8*>(&Ks[k1 * KLD + c * 32 + g * 8]);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[t][c], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qf[t][c], s1, 0, 0, 0);
+        }
+        float p[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          p[j] = (kb + g * 8 + j < nkeys) ? s0[j] * sl2 : -INFINITY;
+          p[4 + j] = (kb + g * 8 + 4 + j < nkeys) ? s1[j] * sl2 : -INFINITY;
+        }
+        float mx = p[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) mx = fmaxf(mx, p[j]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m_run[t], mx);
+        const float alpha = exp2f(m_run[t] - m_new);
+        float psum = 0.f;
+        bf16x8 pb;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float e = exp2f(p[j] - m_new);
+          psum += e;
+          pb[j] = (bf16)e;
+        }
+        l_run[t] = l_run[t] * alpha + psum;
+        m_run[t] = m_new;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          o[t][i] *= alpha;
+          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vt[(i * 16 + (lane & 15)) * VLD + kb + g * 8]);
+          o[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[t][i], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int qrow = q0_of(t) + q_in;
+    if (q0_of(t) >= nq) continue;
+    float l_tot = l_run[t] + __shfl_xor(l_run[t], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    if (qrow >= nq) continue;
+    const float inv = 1.f / l_tot;
+    bf16* Ob = static_cast<bf16*>(a.O) + b * a.o_bs + (long long)qrow * a.o_rs + h * DH;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      bf16x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = (bf16)(o[t][i][j] * inv);
+      *reinterpret_cast<bf16x4*>(Ob + i * 16 + g * 4) = w;
+    }
+  }
+}
+
+template <int DH, int WAVES, int QT, int KC>
+hipError_t launch_chunked(const AttnArgs& a, hipStream_t s) {
+  const long long groups = (a.nq + WAVES * QT * 16 - 1) / (WAVES * QT * 16);
+  const long long n = groups * a.n_heads * a.B;
+  hipLaunchKernelGGL((k_attention_chunked<DH, WAVES, QT, KC>), dim3((unsigned)n), dim3(WAVES * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int DH>
+hipError_t launch_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.nq <= 16) {
+    // tiny groups (sequence encoder): one wave per (group, head)
+    return a.nk <= 32 ? launch_chunked<DH, 1, 1, 32>(a, s) : launch_chunked<DH, 1, 1, 128>(a, s);
+  }
+  // as many queries per workgroup as keep >= 256 workgroups, so K/V chunks are reused widely
+  const long long bh = (long long)a.n_heads * a.B;
+  auto wgs = [&](int qt) { return (a.nq + 64 * qt - 1) / (64 * qt) * bh; };
+  if (wgs(4) >= 256) return launch_chunked<DH, 4, 4, 128>(a, s);
+  if (wgs(2) >= 256) return launch_chunked<DH, 4, 2, 128>(a, s);
+  return launch_chunked<DH, 4, 1, 128>(a, s);
+}
+
 template <typename T, int DH>
 hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
   const int qt = (a.nq + 15) / 16;
@@ -173,6 +337,6 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attention(const AttnArgs& a, bool bf16_model, hipStream_t s) {
   if (a.B <= 0 || a.nq <= 0) return hipSuccess;
-  if (bf16_model) return a.dh == 64 ? launch_t<bf16, 64>(a, s) : launch_t<bf16, 32>(a, s);
+  if (bf16_model) return a.dh == 64 ? launch_bf16<64>(a, s) : launch_bf16<32>(a, s);
   return a.dh == 64 ? launch_t<float, 64>(a, s) : launch_t<float, 32>(a, s);
 }

@@ -18,6 +18,23 @@ template <typename T> FE_DEV T from_f32(float v);
 template <> FE_DEV float from_f32<float>(float v) { return v; }
 template <> FE_DEV bf16 from_f32<bf16>(float v) { return (bf16)v; }  // round to nearest even
 
+// Butterflies across the four 16-lane rows of a wave on the gfx950 lane-swap instructions
+// (VALU, no LDS round trip).  v_permlane16_swap / v_permlane32_swap applied to (v, v) return,
+// in every lane l, the pair {v[l & ~16], v[l | 16]} resp. {v[l & ~32], v[l | 32]}; combining the
+// pair gives the xor-16 / xor-32 butterfly, with the same operand order in both partner lanes.
+FE_DEV float rows_max(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+FE_DEV float rows_sum(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 FE_DEV float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -79,6 +96,33 @@ struct FfnArgs {
   const int32_t* nvalid; int rows_per_batch;
 };
 
+// One whole pre-LN encoder block over groups of S consecutive rows (attention inside a group),
+// for S no longer than a tile (bf16 models).  Xout may equal Xin.
+struct LayerArgs {
+  const void* Xin; int xin_f32; float* Xout;
+  int n_groups, S, gpt;        // gpt: groups per tile (set by the launcher)
+  int D, H, F; float scale;
+  const float *ln1g, *ln1b; const void* wqkv; const float* bqkv;
+  const void* wo; const float* bo;
+  const float *ln2g, *ln2b; const void* w1; const float* b1; const void* w2; const float* b2;
+};
+
+// Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
+//   tail 0: Xout = x1 + FFN(LN2(x1));
+//   tail 1: Xout = x1 and Qout = LN2(x1) Wq + bq (bf16).
+// Rows with (r % rows_per_batch) >= nvalid[r / rows_per_batch] are padding.
+struct PostArgs {
+  const void* O; const void* Xin; int xin_f32; float* Xout;
+  int R, rows_per_batch; const int32_t* nvalid;
+  int D, F, tail;
+  const void* wo; const float* bo; const float *ln2g, *ln2b;
+  const void* w1; const float* b1; const void* w2; const float* b2;
+  const void* wq; const float* bq; void* Qout;
+};
+
+int layer_small_tile_rows(int d);
+hipError_t launch_layer_small(LayerArgs a, hipStream_t s);
+hipError_t launch_post(const PostArgs& a, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s);   // fp32 models
 hipError_t launch_proj(const GemmArgs& a, hipStream_t s);                    // bf16 models, K = d
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);                      // bf16 models

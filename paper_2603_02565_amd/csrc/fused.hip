@@ -11,118 +11,11 @@
 //  * The FFN hidden activations (TM x F) never leave the chip: they are produced 128 columns
 //    at a time into LDS and immediately contracted with the matching rows of W2.
 #include "fe_common.h"
+#include "fe_tile.h"
 
 namespace {
 
-constexpr int WG = 256;
-constexpr int APAD = 8;  // bf16 elements of padding per LDS row
-
-// Copy LayerNorm gains and offsets (D floats each) into LDS; visible after the next barrier.
-template <int D>
-FE_DEV void copy_ln_params(const float* g, const float* b, float* s_g, float* s_b) {
-  if (!g) return;
-  for (int i = threadIdx.x; i < D / 4; i += WG) {
-    reinterpret_cast<float4*>(s_g)[i] = reinterpret_cast<const float4*>(g)[i];
-    reinterpret_cast<float4*>(s_b)[i] = reinterpret_cast<const float4*>(b)[i];
-  }
-}
-
-// Stage rows row0..row0+TM-1 of A (fp32 or bf16, row stride lda) into LDS as bf16, as
-// LayerNorm(A) when g != nullptr (g, b point at the LDS copies of the gains and offsets).
-// Rows whose s_valid flag is 0 are written as zeros.  The global loads of a thread (its row
-// slice) are unconditional vector loads, so they are in flight together.
-template <int TM, int D, typename TA>
-FE_DEV void stage_rows_t(const TA* A, long long lda, int row0, const int* s_valid, const float* g, const float* b,
-                         bf16* As) {
-  constexpr int TPR = WG / TM;                   // threads per row
-  constexpr int VE = 16 / sizeof(TA);            // elements per 16-byte vector
-  constexpr int NV = D / (VE * TPR);             // vectors per thread
-  static_assert(NV >= 1, "row too short for this tile");
-  constexpr int LD = D + APAD;
-  const int tid = threadIdx.x;
-  const int rr = tid / TPR, part = tid % TPR;
-  const bool valid = s_valid[rr];
-  // padding rows read row0 (always a valid row of the tile) and are zeroed below
-  const long long r = valid ? row0 + rr : row0;
-  float v[NV * VE];
-  const uint4* src = reinterpret_cast<const uint4*>(A + r * lda);
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const uint4 t = src[i * TPR + part];
-    const TA* e = reinterpret_cast<const TA*>(&t);
-#pragma unroll
-    for (int j = 0; j < VE; ++j) v[i * VE + j] = (float)e[j];
-  }
-  if (g) {
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < NV * VE; ++i) s += v[i];
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
-    const float mean = s / (float)D;
-    float q = 0.f;
-#pragma unroll
-    for (int i = 0; i < NV * VE; ++i) { const float t = v[i] - mean; q += t * t; }
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) q += __shfl_xor(q, o, 64);
-    const float rstd = rsqrtf(q / (float)D + 1e-5f);
-    const float4* g4 = reinterpret_cast<const float4*>(g);   // LDS copies (copy_ln_params)
-    const float4* b4 = reinterpret_cast<const float4*>(b);
-#pragma unroll
-    for (int i = 0; i < NV; ++i)
-#pragma unroll
-      for (int h = 0; h < VE / 4; ++h) {
-        const int idx = (i * TPR + part) * (VE / 4) + h;
-        const float4 gg = g4[idx], bb = b4[idx];
-        float* x = &v[i * VE + 4 * h];
-        x[0] = (x[0] - mean) * rstd * gg.x + bb.x;
-        x[1] = (x[1] - mean) * rstd * gg.y + bb.y;
-        x[2] = (x[2] - mean) * rstd * gg.z + bb.z;
-        x[3] = (x[3] - mean) * rstd * gg.w + bb.w;
-      }
-  }
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int k = (i * TPR + part) * VE;
-#pragma unroll
-    for (int h = 0; h < VE / 4; ++h) {
-      bf16x4 o;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = valid ? (bf16)v[i * VE + 4 * h + j] : (bf16)0.f;
-      *reinterpret_cast<bf16x4*>(&As[rr * LD + k + 4 * h]) = o;
-    }
-  }
-}
-
-template <int TM, int D>
-FE_DEV void stage_rows(const void* A, bool a_f32, long long lda, int row0, const int* s_valid, const float* g,
-                       const float* b, bf16* As) {
-  if (a_f32) stage_rows_t<TM, D>(static_cast<const float*>(A), lda, row0, s_valid, g, b, As);
-  else stage_rows_t<TM, D>(static_cast<const bf16*>(A), lda, row0, s_valid, g, b, As);
-}
-
-FE_DEV bf16x8 a_frag(const bf16* As, int ld, int row_base, int k0, int lane) {
-  return *reinterpret_cast<const bf16x8*>(&As[(row_base + (lane & 31)) * ld + k0 + (lane >> 5) * 8]);
-}
-
-FE_DEV bf16x8 b_frag(const bf16* Wp, int ksteps, int cb, int ks, int lane) {
-  return reinterpret_cast<const bf16x8*>(Wp)[((long long)cb * ksteps + ks) * 64 + lane];
-}
-
-// row (within the 32-row block) of accumulator element i for this lane
-FE_DEV int acc_row(int i, int lane) { return (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3); }
-
-template <int TM>
-FE_DEV bool mark_rows(int row0, int R, const int32_t* nvalid, int rpb, int* s_valid) {
-  int v = 0;
-  if ((int)threadIdx.x < TM) {
-    const int r = row0 + threadIdx.x;
-    v = r < R;
-    if (v && nvalid) v = (r % rpb) < nvalid[r / rpb];
-    s_valid[threadIdx.x] = v;
-  }
-  return __syncthreads_or(v);
-}
+using namespace fe_tile;
 
 // ------------------------------------------------------------------------------------------
 // C = epi(LN(A) W + bias) for K = D, any N that is a multiple of 32.

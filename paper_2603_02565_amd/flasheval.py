@@ -23,7 +23,7 @@ FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
             "fe_score_select", "fe_trace_enable", "fe_trace_read", "fe_trace_family")
-FE_TRACE_FAMILIES = 9
+FE_TRACE_FAMILIES = 11
 
 
 class FeError(RuntimeError):

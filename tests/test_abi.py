@@ -83,5 +83,6 @@ def test_trace_toggle_without_launches():
     fe.fe_trace_enable(True)
     out = fe.fe_trace_read()
     fe.fe_trace_enable(False)
-    assert set(out) == {"gemm", "attention", "layernorm", "dedup", "gather", "assemble", "score_select", "fill", "ffn"}
+    assert set(out) == {"gemm", "attention", "layernorm", "dedup", "gather", "assemble", "score_select", "fill", "ffn",
+                        "layer", "post"}
     assert all(v == (0.0, 0) for v in out.values())
