@@ -80,18 +80,6 @@ fe_status fail(fe_status st, const char* fmt, ...) {
     if (e_ != hipSuccess) return fail(FE_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
   } while (0)
 
-struct EncW {
-  const float *ln1g, *ln1b;
-  const void* wqkv;
-  const float* bqkv;
-  const void* wo;
-  const float* bo;
-  const float *ln2g, *ln2b;
-  const void* w1;
-  const float* b1;
-  const void* w2;
-  const float* b2;
-};
 
 struct ItemW {
   const float *ln1g, *ln1b;
@@ -410,13 +398,6 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   const bool bf = m->bf16;
   const size_t e = bf ? 2 : 4;
   const float scale = 1.0f / sqrtf((float)(d / m->cfg.n_heads));
-  if (bf && !nvalid && per <= layer_small_tile_rows(d)) {
-    // short groups: the whole block in one kernel
-    LayerArgs la{xin, xin_f32, b.X, nb, per, 0, d, m->cfg.n_heads, F, scale, w.ln1g, w.ln1b, w.wqkv, w.bqkv,
-                 w.wo, w.bo, w.ln2g, w.ln2b, w.w1, w.b1, w.w2, w.b2};
-    FE_LAUNCH(F_LAYER, s, launch_layer_small(la, s));
-    return FE_OK;
-  }
   GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
   g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
   fe_status st0 = run_proj(m, g, s);
@@ -442,6 +423,25 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   fe_status st = run_proj(m, g, s);
   if (st != FE_OK) return st;
   return run_ffn(m, b.X, R, w.ln2g, w.ln2b, w.w1, w.b1, w.w2, w.b2, b.Hf, nvalid, per, s);
+}
+
+// Whole modules of short groups run as one kernel on bf16 models.
+bool module_fits(const fe_model* m, int per) { return m->bf16 && per <= module_small_tile_rows(m->cfg.d); }
+
+// n encoder blocks `ws` over ngroups groups of `per` rows, then the final LayerNorm (lnf_g,
+// lnf_b) into fp32 Y: every row, or the first row of each group.
+fe_status run_module(const fe_model* m, const std::vector<EncW>& ws, int ngroups, int per, const void* xin, bool xin_f32,
+                     const float* lnf_g, const float* lnf_b, float* Y, bool first_row_only, hipStream_t s) {
+  ModuleArgs a{};
+  a.Xin = xin; a.xin_f32 = xin_f32;
+  a.Y = Y; a.first_row_only = first_row_only;
+  a.n_groups = ngroups; a.S = per;
+  a.D = m->cfg.d; a.H = m->cfg.n_heads; a.F = m->cfg.ffn_dim; a.n_layers = m->cfg.n_layers;
+  a.scale = 1.0f / sqrtf((float)(m->cfg.d / m->cfg.n_heads));
+  a.lnfg = lnf_g; a.lnfb = lnf_b;
+  for (int l = 0; l < m->cfg.n_layers; ++l) a.layer[l] = ws[l];
+  FE_LAUNCH(F_LAYER, s, launch_module_small(a, s));
+  return FE_OK;
 }
 
 fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s) {
@@ -624,13 +624,23 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
     src = at<char>(ws, w.c_xin);
   }
   Bufs b{at<float>(ws, w.c_x), at<char>(ws, w.c_qkv), at<char>(ws, w.c_o), at<char>(ws, w.c_h)};
-  for (int l = 0; l < m->cfg.n_layers; ++l) {
-    st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s);
+  const bool whole = module_fits(m, T);
+  if (whole) {
+    st = run_module(m, m->ctx, B, T, src, false, m->ctx_lnf_g, m->ctx_lnf_b, b.X, false, s);
     if (st != FE_OK) return st;
+  } else {
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s);
+      if (st != FE_OK) return st;
+    }
   }
-  // final LayerNorm of the context module fused into the key/value projections of all item layers
+  // key/value projections of all item layers, with the context module's final LayerNorm fused
+  // into their prologue unless the module kernel already applied it
   GemmArgs g = gemm(b.X, d, true, R, d, 2 * m->cfg.n_layers * d, m->wkv, m->bkv, kv, d, false, EPI_STORE);
-  g.ln_g = m->ctx_lnf_g; g.ln_b = m->ctx_lnf_b;
+  if (!whole) {
+    g.ln_g = m->ctx_lnf_g;
+    g.ln_b = m->ctx_lnf_b;
+  }
   g.col_block = d; g.col_block_stride = (long long)R * d;
   return run_proj(m, g, s);
 }
@@ -748,13 +758,19 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   const bool bf = m->bf16;
   const int d = m->cfg.d, S = L + 1;
   Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h)};
-  for (int l = 0; l < m->cfg.n_layers; ++l) {
-    st = enc_block(m, m->seq[l], B * K, S, l == 0 ? seq : b.X, l > 0, b, nullptr, s);
-    if (st != FE_OK) return st;
-  }
   // c_k = final LayerNorm of each list's [CLS] row (row 0 of every S-row group)
   float* c = at<float>(ws, w.s_c);
-  FE_LAUNCH(F_LN, s, launch_layernorm(b.X, 1, (long long)S * d, B * K, d, m->seq_lnf_g, m->seq_lnf_b, c, 1, d, bf, s));
+  if (module_fits(m, S)) {
+    st = run_module(m, m->seq, B * K, S, seq, false, m->seq_lnf_g, m->seq_lnf_b, c, true, s);
+    if (st != FE_OK) return st;
+  } else {
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      st = enc_block(m, m->seq[l], B * K, S, l == 0 ? seq : b.X, l > 0, b, nullptr, s);
+      if (st != FE_OK) return st;
+    }
+    FE_LAUNCH(F_LN, s, launch_layernorm(b.X, 1, (long long)S * d, B * K, d, m->seq_lnf_g, m->seq_lnf_b, c, 1, d, bf, s));
+  }
+  if (module_fits(m, K)) return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
   Bufs bc{c, b.qkv, b.O, b.Hf};
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s);

@@ -96,17 +96,6 @@ struct FfnArgs {
   const int32_t* nvalid; int rows_per_batch;
 };
 
-// One whole pre-LN encoder block over groups of S consecutive rows (attention inside a group),
-// for S no longer than a tile (bf16 models).  Xout may equal Xin.
-struct LayerArgs {
-  const void* Xin; int xin_f32; float* Xout;
-  int n_groups, S, gpt;        // gpt: groups per tile (set by the launcher)
-  int D, H, F; float scale;
-  const float *ln1g, *ln1b; const void* wqkv; const float* bqkv;
-  const void* wo; const float* bo;
-  const float *ln2g, *ln2b; const void* w1; const float* b1; const void* w2; const float* b2;
-};
-
 // Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
 //   tail 0: Xout = x1 + FFN(LN2(x1));
 //   tail 1: Xout = x1 and Qout = LN2(x1) Wq + bq (bf16).
@@ -120,8 +109,29 @@ struct PostArgs {
   const void* wq; const float* bq; void* Qout;
 };
 
-int layer_small_tile_rows(int d);
-hipError_t launch_layer_small(LayerArgs a, hipStream_t s);
+// Device pointers of one pre-LN encoder block (matrices of bf16 models in packed fragment order).
+struct EncW {
+  const float *ln1g, *ln1b; const void* wqkv; const float* bqkv;
+  const void* wo; const float* bo;
+  const float *ln2g, *ln2b; const void* w1; const float* b1; const void* w2; const float* b2;
+};
+constexpr int FE_MAX_LAYERS = 8;
+
+// A whole encoder module over short groups (bf16 models): n_layers pre-LN blocks over groups of
+// S consecutive rows (attention inside a group), then the module's final LayerNorm.  Y receives
+// in fp32 the final LayerNorm of every row (first_row_only = 0, Y [n_groups*S][D]) or of the
+// first row of each group (first_row_only = 1, Y [n_groups][D]).
+struct ModuleArgs {
+  const void* Xin; int xin_f32;
+  float* Y; int first_row_only;
+  int n_groups, S, gpt;        // gpt: groups per tile (set by the launcher)
+  int D, H, F, n_layers; float scale;
+  const float *lnfg, *lnfb;
+  EncW layer[FE_MAX_LAYERS];
+};
+
+int module_small_tile_rows(int d);
+hipError_t launch_module_small(ModuleArgs a, hipStream_t s);
 hipError_t launch_post(const PostArgs& a, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s);   // fp32 models
 hipError_t launch_proj(const GemmArgs& a, hipStream_t s);                    // bf16 models, K = d

@@ -1,18 +1,18 @@
 // Fused pre-LN transformer layers for bf16 models.
 //
-// k_layer_small: a whole encoder block in one kernel for modules whose attention groups are
-//   short (the intra-sequence encoder over [CLS; items] of each list, and the cross-sequence
-//   module when K <= 64).  A workgroup owns a tile of whole groups (at most TM rows); every
-//   intermediate stays on chip:
+// k_module_small: a whole encoder module -- every block and the final LayerNorm -- in one
+//   kernel for modules whose attention groups are short (the intra-sequence encoder over
+//   [CLS; items] of each list, the cross-sequence module when K <= 64, the context module when
+//   T <= 64).  A workgroup owns a tile of whole groups (at most TM rows); the fp32 residual
+//   stream stays in registers for all blocks and every intermediate stays on chip.  Per block:
 //     A  LN1(x) -> LDS; q|k|v = LN1(x) Wqkv + b -> LDS
-//     B  attention inside each group, per (group, head, 16-query tile) on one wave, keys in
-//        blocks of 16 (S^T = K Q^T on 16x16x32 MFMA, P V on 16x16x16 MFMA, online softmax)
-//     C  x1 = x + O Wo + bo -> LDS (fp32); LN2(x1) -> LDS; FFN in 128-wide hidden chunks;
-//        x2 = x1 + FFN -> global fp32.
-// k_post: the same tail (C) for modules with long groups (context, distinct items, wide
+//     B  attention inside each group, per (group, head, 16-query tile) on one wave
+//        (S^T = K Q^T on 16x16x32 MFMA, one softmax over the group, P V on 16x16x16 MFMA)
+//     C  x += O Wo + bo; LN2(x) -> LDS; x += FFN in 128-wide hidden chunks.
+// k_post: the tail (C) for modules with long groups (context, distinct items, wide
 //   cross-sequence sets) whose attention ran in the chunked attention kernel; it reads the
-//   attention output O from global memory.  Its PROJ variant replaces the FFN by the item
-//   layers' cross-attention query projection q = LN2(x1) Wq + bq.
+//   attention output O and the residual stream from global memory.  Its second variant replaces
+//   the FFN by the item layers' cross-attention query projection q = LN2(x1) Wq + bq.
 #include "fe_common.h"
 #include "fe_tile.h"
 
@@ -29,7 +29,8 @@ constexpr int HLD = HC + APAD;
 // streamed through registers one 8-fragment stage ahead (all shapes compile-time, so the
 // stage loop unrolls completely and fragment addresses are immediate offsets).  start() issues the first
 // stage (so its latency can hide behind other work); run() calls epi(cb, rb, acc) for every
-// finished 32x32 block (row block rb).
+// finished 32x32 block: epi(jj, cb, rb, acc) with jj the wave-local block index (compile-time
+// after unrolling), cb = wave + 4*jj the column block and rb the row block.
 //
 // The product is formed transposed, C^T = W^T A^T: the packed weight fragments are the A
 // operand and the activation fragments the B operand.  Each lane then holds one output ROW
@@ -96,7 +97,7 @@ struct ColGemm {
       for (int j = 0; j < NBW; ++j) {
         if (j >= blocks_in(g)) continue;
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) epi(wave + 4 * (g * NBW + j), rb, acc[rb][j]);
+        for (int rb = 0; rb < RB; ++rb) epi(g * NBW + j, wave + 4 * (g * NBW + j), rb, acc[rb][j]);
       }
     }
   }
@@ -385,59 +386,6 @@ FE_DEV void ffn_tail(Ffn<TM, D>& ffn, float* Xs, int ldx, bf16* As, bf16* Hs, co
   store_rows<TM, D>(Xs, ldx, Xout, row0, s_valid);
 }
 
-template <int TM, int D>
-struct SmallSmem {
-  static constexpr int LDA = D + APAD, LDQ = 3 * D + APAD, LDX = D + 4;
-  static constexpr int QKV_BYTES = TM * LDQ * 2;
-  static constexpr int TAIL_BYTES = TM * LDX * 4 + TM * HLD * 2;
-  static constexpr int BIG = QKV_BYTES > TAIL_BYTES ? QKV_BYTES : TAIL_BYTES;
-};
-
-template <int TM, int D, int DH, int NKB>
-__global__ __launch_bounds__(WG, 2) void k_layer_small(LayerArgs a) {
-  using L = SmallSmem<TM, D>;
-  __shared__ __attribute__((aligned(16))) bf16 As[TM * L::LDA];
-  __shared__ __attribute__((aligned(16))) char big[L::BIG];
-  __shared__ __attribute__((aligned(16))) float s_g1[D], s_b1[D], s_g2[D], s_b2[D];
-  __shared__ int s_valid[TM];
-  bf16* QKVs = reinterpret_cast<bf16*>(big);
-  float* Xs = reinterpret_cast<float*>(big);
-  bf16* Hs = reinterpret_cast<bf16*>(big + TM * L::LDX * 4);
-  const int lane = threadIdx.x & 63;
-
-  const int g0 = blockIdx.x * a.gpt;
-  const int ng = min(a.gpt, a.n_groups - g0);
-  const long long row0 = (long long)g0 * a.S;
-  const int nrows = ng * a.S;
-
-  ColGemm<TM, D, 3 * D / 32> gq;
-  gq.start(a.wqkv);
-  copy_ln_params<D>(a.ln1g, a.ln1b, s_g1, s_b1);
-  copy_ln_params<D>(a.ln2g, a.ln2b, s_g2, s_b2);
-  if (!mark_rows<TM>(0, nrows, nullptr, 1, s_valid)) return;
-  stage_rows<TM, D>(a.Xin, a.xin_f32, D, (int)row0, s_valid, s_g1, s_b1, As);
-  __syncthreads();
-
-  // A: q|k|v of the tile into LDS
-  gq.run(As, L::LDA, [&](int cb, int rb, const f32x16& acc) { block_to_lds_bf16(acc, cb, rb, a.bqkv, QKVs, L::LDQ); });
-  ColGemm<TM, D, D / 32> go;
-  go.start(a.wo);
-  __syncthreads();
-
-  // B: attention inside each group -> As (the LN1 tile is no longer needed)
-  group_attention<D, DH, NKB>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
-  Ffn<TM, D> ffn;
-  ffn.preload(a.w1, a.w2, a.F);
-  __syncthreads();
-
-  // C: x1 = x + O Wo + bo -> Xs (fp32); then LN2, FFN, x2 = x1 + FFN
-  go.run(As, L::LDA, [&](int cb, int rb, const f32x16& acc) { block_to_lds_f32(acc, cb, rb, a.bo, Xs, L::LDX); });
-  __syncthreads();
-  add_rows<TM, D>(Xs, L::LDX, a.Xin, a.xin_f32, row0, s_valid);
-  __syncthreads();
-  ffn_tail<TM, D>(ffn, Xs, L::LDX, As, Hs, s_g2, s_b2, a.b1, a.b2, a.Xout, row0, s_valid);
-}
-
 template <int TM, int D, int TAIL>
 __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   constexpr int LDA = D + APAD, LDX = D + 4;
@@ -459,7 +407,7 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   if constexpr (TAIL == 0) ffn.preload(a.w1, a.w2, a.F);
   __syncthreads();
 
-  go.run(As, LDA, [&](int cb, int rb, const f32x16& acc) { block_to_lds_f32(acc, cb, rb, a.bo, Xs, LDX); });
+  go.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) { block_to_lds_f32(acc, cb, rb, a.bo, Xs, LDX); });
   if constexpr (TAIL == 1) gq.start(a.wq);
   __syncthreads();
   add_rows<TM, D>(Xs, LDX, a.Xin, a.xin_f32, row0, s_valid);
@@ -473,7 +421,7 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
     __syncthreads();
     bf16* Qs = reinterpret_cast<bf16*>(Xs);   // Xs is dead now: per-wave 32 x 32 bf16 staging
     const int wave = threadIdx.x >> 6;
-    gq.run(As, LDA, [&](int cb, int rb, const f32x16& acc) {
+    gq.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) {
       bf16* st = Qs + wave * 32 * 40;
       // the block's rows land in the wave's 32 x 32 staging area (columns relative to cb*32)
       block_to_lds_bf16(acc, 0, 0, a.bq + cb * 32, st, 40);
@@ -492,14 +440,347 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// Whole modules over short groups, residual stream in registers.
+//
+// Wave w keeps the fp32 residual rows of its output column blocks cb = w + 4j (j < D/128) --
+// the blocks its column-split products (Wo, the FFN down-projection) produce -- in the
+// transposed accumulator layout: x.v[j][rb][4q + e] is row rb*32 + lane%32, column
+// cb*32 + 8q + 4*(lane/32) + e.  Output-projection and FFN epilogues add into it directly;
+// only the LayerNorm statistics cross waves (through a small LDS array).
+// ------------------------------------------------------------------------------------------
+template <int TM, int D>
+struct Resid {
+  static constexpr int RB = TM / 32, BPW = D / 128;
+  f32x16 v[BPW][RB];
+};
+
+FE_DEV int resid_col(int j, int q) {
+  return (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) + 4 * j) * 32 + 8 * q + 4 * ((threadIdx.x & 63) >> 5);
+}
+
+// x = rows row0.. of X (fp32 or bf16, row stride D); rows whose s_valid flag is 0 are zero.
+// All loads of a lane are unconditional and independent, so they are in flight together.
+template <int TM, int D, typename TX>
+FE_DEV void resid_load_t(Resid<TM, D>& x, const TX* X, long long row0, const int* s_valid) {
+  const int lane = threadIdx.x & 63;
+  typedef TX vec4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int rb = 0; rb < TM / 32; ++rb) {
+    const int r = rb * 32 + (lane & 31);
+    const bool ok = s_valid[r];
+    const TX* src = X + (ok ? row0 + r : row0) * D;
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const vec4 t = *reinterpret_cast<const vec4*>(src + resid_col(j, q));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x.v[j][rb][4 * q + e] = ok ? (float)t[e] : 0.f;
+      }
+  }
+}
+
+template <int TM, int D>
+FE_DEV void resid_load(Resid<TM, D>& x, const void* X, bool x_f32, long long row0, const int* s_valid) {
+  if (x_f32) resid_load_t<TM, D>(x, static_cast<const float*>(X), row0, s_valid);
+  else resid_load_t<TM, D>(x, static_cast<const bf16*>(X), row0, s_valid);
+}
+
+// x[block jj, row block rb] += acc + bias (acc in the same transposed layout; bias [D]).
+template <int TM, int D>
+FE_DEV void resid_add(Resid<TM, D>& x, int jj, int rb, const f32x16& acc, const float* bias) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 bb = *reinterpret_cast<const float4*>(&bias[resid_col(jj, q)]);
+    x.v[jj][rb][4 * q] += acc[4 * q] + bb.x;
+    x.v[jj][rb][4 * q + 1] += acc[4 * q + 1] + bb.y;
+    x.v[jj][rb][4 * q + 2] += acc[4 * q + 2] + bb.z;
+    x.v[jj][rb][4 * q + 3] += acc[4 * q + 3] + bb.w;
+  }
+}
+
+// Mean and 1/sqrt(var + eps) of every row of x (this lane's rows rb*32 + lane%32).  Each lane
+// reduces its 16*D/128 values to a mean and a sum of squared deviations; partial results are
+// merged pairwise with the update of Chan, Golub and LeVeque (equal counts: mean of the means,
+// M2 = M2a + M2b + (ma - mb)^2 n/2), first across the two lanes that share a row
+// (v_permlane32_swap), then across the four waves through s_stat [4][TM].  Contains one barrier;
+// s_stat must not be read by an earlier call any more when a wave arrives here.
+template <int TM, int D>
+FE_DEV void resid_stats(const Resid<TM, D>& x, float2* s_stat, float (&mean)[TM / 32], float (&rstd)[TM / 32]) {
+  constexpr int RB = TM / 32, BPW = D / 128, NL = 16 * BPW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < BPW; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sum += x.v[j][rb][i];
+    const float m = sum * (1.f / NL);
+    float m2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < BPW; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float t = x.v[j][rb][i] - m;
+        m2 += t * t;
+      }
+    const auto pm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    const auto pq = __builtin_amdgcn_permlane32_swap(__float_as_uint(m2), __float_as_uint(m2), false, false);
+    const float ma = __uint_as_float(pm[0]), mb = __uint_as_float(pm[1]);
+    const float dm = mb - ma;
+    const float mw = 0.5f * (ma + mb);
+    const float qw = __uint_as_float(pq[0]) + __uint_as_float(pq[1]) + dm * dm * (0.5f * NL);
+    if (lane < 32) s_stat[wave * TM + rb * 32 + lane] = make_float2(mw, qw);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = rb * 32 + (lane & 31);
+    const float2 p0 = s_stat[r], p1 = s_stat[TM + r], p2 = s_stat[2 * TM + r], p3 = s_stat[3 * TM + r];
+    const float mu = 0.25f * ((p0.x + p1.x) + (p2.x + p3.x));
+    const float d0 = p0.x - mu, d1 = p1.x - mu, d2 = p2.x - mu, d3 = p3.x - mu;
+    const float m2 = (p0.y + p1.y) + (p2.y + p3.y) + (d0 * d0 + d1 * d1 + d2 * d2 + d3 * d3) * (float)(2 * NL);
+    mean[rb] = mu;
+    rstd[rb] = rsqrtf(m2 * (1.f / D) + 1e-5f);
+  }
+}
+
+// As (bf16, row stride D + APAD) = LayerNorm(x) with gains g and offsets b (global, [D]).
+template <int TM, int D>
+FE_DEV void resid_ln_to_lds(const Resid<TM, D>& x, const float* g, const float* b, float2* s_stat, bf16* As) {
+  constexpr int RB = TM / 32, LDA = D + APAD;
+  const int lane = threadIdx.x & 63;
+  float4 gg[D / 128][4], bb[D / 128][4];
+#pragma unroll
+  for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      gg[j][q] = *reinterpret_cast<const float4*>(&g[resid_col(j, q)]);
+      bb[j][q] = *reinterpret_cast<const float4*>(&b[resid_col(j, q)]);
+    }
+  float mean[RB], rstd[RB];
+  resid_stats<TM, D>(x, s_stat, mean, rstd);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = rb * 32 + (lane & 31);
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& v = x.v[j][rb];
+        bf16x4 o;
+        o[0] = (bf16)((v[4 * q] - mean[rb]) * rstd[rb] * gg[j][q].x + bb[j][q].x);
+        o[1] = (bf16)((v[4 * q + 1] - mean[rb]) * rstd[rb] * gg[j][q].y + bb[j][q].y);
+        o[2] = (bf16)((v[4 * q + 2] - mean[rb]) * rstd[rb] * gg[j][q].z + bb[j][q].z);
+        o[3] = (bf16)((v[4 * q + 3] - mean[rb]) * rstd[rb] * gg[j][q].w + bb[j][q].w);
+        *reinterpret_cast<bf16x4*>(&As[r * LDA + resid_col(j, q)]) = o;
+      }
+  }
+}
+
+// x += W2 ReLU(As W1 + b1) + b2 for the tile in As (LN2 output), hidden width F in chunks of
+// HC = 128, accumulating straight into the register-resident residual (its blocks are the
+// down-projection's output blocks).  Wave w computes hidden columns 32w..32w+31 of a chunk and
+// output blocks w + 4j.  The weight fragments of a chunk form one stream -- the KS k-steps of
+// W1 column block 4c + w, then for every output block j the 8 k-steps 8c.. of W2 column block
+// w + 4j -- consumed in stages of 8 fragments through a two-stage register buffer, each stage
+// requested one stage ahead (2*KS/8 stages per chunk, an even count, so buffer parities are
+// compile-time).  Hidden chunks alternate between two LDS buffers in Hs (2 x TM x HLD): chunk
+// c is written to buffer c&1 and one barrier per chunk separates its writers from its readers;
+// buffer c&1 is rewritten (chunk c+2) only after every wave passed the barrier of chunk c+1,
+// i.e. finished reading chunk c.  The caller orders the first writes to Hs after its earlier
+// readers and the next writes to As or Hs after this call.
+template <int TM, int D>
+struct FfnStream {
+  static constexpr int RB = TM / 32, KS = D / 16, OCB = D / 128;
+  static constexpr int S1 = KS / 8, NS = S1 + OCB;         // W1 stages, stages per chunk
+  static_assert(KS % 8 == 0 && NS % 2 == 0, "unsupported width");
+  bf16x8 buf[2][8];
+  const bf16x8 *W1l, *W2l;
+  int F;
+  FE_DEV void load(int c, int t) {      // stage t (compile-time) of chunk c into buf[t & 1]
+    if (t < S1) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) buf[t & 1][k] = W1l[((long long)c * 4 * KS + t * 8 + k) * 64];
+    } else {
+      const int j = t - S1;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) buf[t & 1][k] = W2l[((long long)4 * j * (F / 16) + c * 8 + k) * 64];
+    }
+  }
+  FE_DEV void start(const void* w1p, const void* w2p, int f) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    F = f;
+    W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
+    W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (f / 16) * 64 + lane;
+    load(0, 0);
+  }
+  template <class Acc>
+  FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x) {
+    constexpr int LD = D + APAD;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nchunks = F / HC;
+    for (int c = 0; c < nchunks; ++c) {
+      bf16* Hc = Hs + (c & 1) * TM * HLD;
+      float4 bias1[4];
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+        bias1[qq] = *reinterpret_cast<const float4*>(&b1[(c * 4 + wave) * 32 + qq * 8 + (lane >> 5) * 4]);
+      f32x16 acc_h[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc_h[rb] = f32x16{};
+#pragma unroll
+      for (int t = 0; t < S1; ++t) {
+        load(c, t + 1);                  // t + 1 <= S1 < NS: still this chunk
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          bf16x8 af[4][RB];
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(As, LD, rb * 32, (t * 8 + h * 4 + k) * 16, lane);
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+              acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][h * 4 + k], af[k][rb], acc_h[rb], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const float* bb = reinterpret_cast<const float*>(&bias1[qq]);
+          bf16x4 hv;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) hv[e] = (bf16)fmaxf(acc_h[rb][4 * qq + e] + bb[e], 0.f);
+          *reinterpret_cast<bf16x4*>(&Hc[(rb * 32 + (lane & 31)) * HLD + wave * 32 + qq * 8 + (lane >> 5) * 4]) = hv;
+        }
+      __syncthreads();
+      bf16x8 af[8][RB];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(Hc, HLD, rb * 32, k * 16, lane);
+#pragma unroll
+      for (int j = 0; j < OCB; ++j) {
+        const int t = S1 + j;
+        if (t + 1 < NS) load(c, t + 1);
+        else if (c + 1 < nchunks) load(c + 1, 0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            x.v[j][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][k], af[k][rb], x.v[j][rb], 0, 0, 0);
+      }
+    }
+  }
+};
+
+template <int TM, int D>
+struct ModuleSmem {
+  static constexpr int LDA = D + APAD, LDQ = 3 * D + APAD;
+  static constexpr int QKV_BYTES = TM * LDQ * 2, HS_BYTES = 2 * TM * HLD * 2;
+  static constexpr int BIG = QKV_BYTES > HS_BYTES ? QKV_BYTES : HS_BYTES;
+};
+
+// n_layers encoder blocks and the final LayerNorm over a tile of whole groups; one launch per
+// module.  Per block: LN1 -> As; q|k|v -> LDS; attention per (group, head) -> As; x += O Wo + bo;
+// LN2 -> As; x += FFN.  The fp32 residual x never leaves registers; the result leaves as fp32.
+template <int TM, int D, int DH, int NKB>
+__global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
+  using L = ModuleSmem<TM, D>;
+  constexpr int RB = TM / 32, OCB = D / 128;
+  __shared__ __attribute__((aligned(16))) bf16 As[TM * L::LDA];
+  __shared__ __attribute__((aligned(16))) char big[L::BIG];
+  __shared__ __attribute__((aligned(16))) float2 s_stat[4 * TM];
+  __shared__ int s_valid[TM];
+  bf16* QKVs = reinterpret_cast<bf16*>(big);
+  bf16* Hs = reinterpret_cast<bf16*>(big);
+  const int lane = threadIdx.x & 63;
+
+  const int g0 = blockIdx.x * a.gpt;
+  const int ng = min(a.gpt, a.n_groups - g0);
+  const long long row0 = (long long)g0 * a.S;
+  const int nrows = ng * a.S;
+
+  ColGemm<TM, D, 3 * D / 32> gq;
+  gq.start(a.layer[0].wqkv);
+  if (!mark_rows<TM>(0, nrows, nullptr, 1, s_valid)) return;
+  Resid<TM, D> x;
+  resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
+
+  for (int l = 0; l < a.n_layers; ++l) {
+    const EncW& w = a.layer[l];
+    if (l > 0) gq.start(w.wqkv);
+    // LN1 -> As (the barrier inside the statistics also retires every earlier reader of As)
+    resid_ln_to_lds<TM, D>(x, w.ln1g, w.ln1b, s_stat, As);
+    __syncthreads();
+    gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) { block_to_lds_bf16(acc, cb, rb, w.bqkv, QKVs, L::LDQ); });
+    ColGemm<TM, D, D / 32> go;
+    go.start(w.wo);
+    __syncthreads();
+    group_attention<D, DH, NKB>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
+    FfnStream<TM, D> ffn;
+    ffn.start(w.w1, w.w2, a.F);
+    __syncthreads();
+    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, w.bo); });
+    resid_ln_to_lds<TM, D>(x, w.ln2g, w.ln2b, s_stat, As);
+    __syncthreads();
+    ffn.run(As, Hs, w.b1, x);
+#pragma unroll
+    for (int j = 0; j < OCB; ++j)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, w.b2);
+  }
+
+  // final LayerNorm, fp32 out: every valid row, or the first row of each group
+  float4 gg[D / 128][4], bb[D / 128][4];
+#pragma unroll
+  for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      gg[j][q] = *reinterpret_cast<const float4*>(&a.lnfg[resid_col(j, q)]);
+      bb[j][q] = *reinterpret_cast<const float4*>(&a.lnfb[resid_col(j, q)]);
+    }
+  float mean[RB], rstd[RB];
+  resid_stats<TM, D>(x, s_stat, mean, rstd);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = rb * 32 + (lane & 31);
+    if (!s_valid[r]) continue;
+    long long out;
+    if (a.first_row_only) {
+      if (r % a.S) continue;
+      out = g0 + r / a.S;
+    } else {
+      out = row0 + r;
+    }
+    float* y = a.Y + out * D;
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& v = x.v[j][rb];
+        *reinterpret_cast<float4*>(&y[resid_col(j, q)]) =
+            make_float4((v[4 * q] - mean[rb]) * rstd[rb] * gg[j][q].x + bb[j][q].x,
+                        (v[4 * q + 1] - mean[rb]) * rstd[rb] * gg[j][q].y + bb[j][q].y,
+                        (v[4 * q + 2] - mean[rb]) * rstd[rb] * gg[j][q].z + bb[j][q].z,
+                        (v[4 * q + 3] - mean[rb]) * rstd[rb] * gg[j][q].w + bb[j][q].w);
+      }
+  }
+}
+
 template <int TM, int D, int DH>
-hipError_t launch_small_t(const LayerArgs& a, hipStream_t s) {
+hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
   const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
   switch ((a.S + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_layer_small<TM, D, DH, 1>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_layer_small<TM, D, DH, 2>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_layer_small<TM, D, DH, 3>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_layer_small<TM, D, DH, 4>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4>), dim3(tiles), dim3(WG), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -516,18 +797,18 @@ hipError_t launch_post_t(const PostArgs& a, hipStream_t s) {
 }  // namespace
 
 // groups of up to 64 rows (the score blocks of a group are held in registers at once)
-int layer_small_tile_rows(int d) { return d >= 512 ? 32 : 64; }
+int module_small_tile_rows(int d) { return d >= 512 ? 32 : 64; }
 
-hipError_t launch_layer_small(LayerArgs a, hipStream_t s) {
+hipError_t launch_module_small(ModuleArgs a, hipStream_t s) {
   if (a.n_groups <= 0) return hipSuccess;
-  const int tm = layer_small_tile_rows(a.D);
-  if (a.S > tm) return hipErrorInvalidValue;
+  const int tm = module_small_tile_rows(a.D);
+  if (a.S < 1 || a.S > tm || a.n_layers < 1 || a.n_layers > FE_MAX_LAYERS || a.F % HC) return hipErrorInvalidValue;
   a.gpt = tm / a.S;
   const int dh = a.D / a.H;
   switch (a.D) {
-    case 128: return dh == 64 ? launch_small_t<64, 128, 64>(a, s) : launch_small_t<64, 128, 32>(a, s);
-    case 256: return dh == 64 ? launch_small_t<64, 256, 64>(a, s) : launch_small_t<64, 256, 32>(a, s);
-    case 512: return dh == 64 ? launch_small_t<32, 512, 64>(a, s) : launch_small_t<32, 512, 32>(a, s);
+    case 128: return dh == 64 ? launch_module_t<64, 128, 64>(a, s) : launch_module_t<64, 128, 32>(a, s);
+    case 256: return dh == 64 ? launch_module_t<64, 256, 64>(a, s) : launch_module_t<64, 256, 32>(a, s);
+    case 512: return dh == 64 ? launch_module_t<32, 512, 64>(a, s) : launch_module_t<32, 512, 32>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
