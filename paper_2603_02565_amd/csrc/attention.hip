@@ -248,21 +248,27 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
         float p[8];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          p[j] = (kb + g * 8 + j < nkeys) ? s0[j] * sl2 : -INFINITY;
-          p[4 + j] = (kb + g * 8 + 4 + j < nkeys) ? s1[j] * sl2 : -INFINITY;
+          p[j] = s0[j] * sl2;
+          p[4 + j] = s1[j] * sl2;
+        }
+        if (kb + 32 > nkeys) {                      // ragged last block (uniform branch)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (kb + g * 8 + j >= nkeys) p[j] = -INFINITY;
+            if (kb + g * 8 + 4 + j >= nkeys) p[4 + j] = -INFINITY;
+          }
         }
         float mx = p[0];
 #pragma unroll
         for (int j = 1; j < 8; ++j) mx = fmaxf(mx, p[j]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run[t], mx);
-        const float alpha = exp2f(m_run[t] - m_new);
+        mx = rows_max(mx);
+        const float m_new = fmaxf(m_run[t], mx);   // finite: every key block holds a valid key
+        const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);   // v_exp_f32; exp2(-inf) = 0
         float psum = 0.f;
         bf16x8 pb;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float e = exp2f(p[j] - m_new);
+          const float e = __builtin_amdgcn_exp2f(p[j] - m_new);
           psum += e;
           pb[j] = (bf16)e;
         }
@@ -282,8 +288,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
   for (int t = 0; t < QT; ++t) {
     const int qrow = q0_of(t) + q_in;
     if (q0_of(t) >= nq) continue;
-    float l_tot = l_run[t] + __shfl_xor(l_run[t], 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float l_tot = rows_sum(l_run[t]);
     if (qrow >= nq) continue;
     const float inv = 1.f / l_tot;
     bf16* Ob = static_cast<bf16*>(a.O) + b * a.o_bs + (long long)qrow * a.o_rs + h * DH;
@@ -297,6 +302,140 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// bf16 models, at most 32*NB32 keys per (batch, head): every key is resident in LDS at once, so
+// each 16-query tile takes one softmax over its whole score row (scores of all key blocks held
+// in registers) instead of a running rescale.  One workgroup of WAVES waves owns a (batch, head)
+// and all its queries (at most 16*WAVES; query tile t on wave t), so its keys are read from
+// memory once; they
+// are staged behind a single barrier (K row-major, V transposed, rows past nk zero-filled up to
+// the next multiple of 32).  Score and output blocks use the same transposed 16x16x32 layout as
+// the chunked kernel; the softmax scale is folded into the exponent (exp2(s*c - max(s)*c) with
+// c = scale*log2(e) > 0, one FMA per score).
+// ------------------------------------------------------------------------------------------
+template <int DH, int WAVES, int NB32>
+__global__ __launch_bounds__(WAVES * 64) void k_attention_rows(AttnArgs a) {
+  constexpr int NT = WAVES * 64, NK = NB32 * 32;
+  constexpr int KLD = DH + 8, VLD = NK + 8, NB = DH / 16;
+  constexpr int NV = NK * DH / 8;                  // 16-byte vectors per tensor
+  constexpr int PER_T = (NV + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) bf16 Ks[NK * KLD];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VLD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r = lane & 15;
+  const int h = blockIdx.x % a.n_heads, b = blockIdx.x / a.n_heads;
+  int nq = a.nq, nk = a.nk;
+  if (a.q_valid) nq = min(nq, a.q_valid[b]);
+  if (a.k_valid) nk = min(nk, a.k_valid[b]);
+  if (nq <= 0 || nk <= 0) return;                  // uniform over the workgroup
+  const int nb32 = (nk + 31) / 32;
+
+  const bf16* Qb = static_cast<const bf16*>(a.Q) + b * a.q_bs + h * DH;
+  const bf16* Kb = static_cast<const bf16*>(a.K) + b * a.k_bs + h * DH;
+  const bf16* Vb = static_cast<const bf16*>(a.V) + b * a.v_bs + h * DH;
+  const float c2 = a.scale * kLog2e;
+
+  {
+    uint4 kr[PER_T], vr[PER_T];
+#pragma unroll
+    for (int p = 0; p < PER_T; ++p) {
+      const int e = p * NT + tid, key = e / (DH / 8), d0 = (e % (DH / 8)) * 8;
+      const bool ok = e < NV && key < nk;
+      kr[p] = ok ? *reinterpret_cast<const uint4*>(Kb + (long long)key * a.k_rs + d0) : make_uint4(0, 0, 0, 0);
+      vr[p] = ok ? *reinterpret_cast<const uint4*>(Vb + (long long)key * a.v_rs + d0) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int p = 0; p < PER_T; ++p) {
+      const int e = p * NT + tid, key = e / (DH / 8), d0 = (e % (DH / 8)) * 8;
+      if (e >= NV || key >= nb32 * 32) continue;     // never read
+      *reinterpret_cast<uint4*>(&Ks[key * KLD + d0]) = kr[p];
+      const bf16* v = reinterpret_cast<const bf16*>(&vr[p]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) Vt[(d0 + i) * VLD + key] = v[i];
+    }
+  }
+  __syncthreads();
+
+  {
+    const int q0 = wave * 16, qrow = q0 + r;
+    if (q0 >= nq) return;                            // uniform over the wave; no barrier follows
+    bf16x8 qf[DH / 32];
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+      qf[c] = *reinterpret_cast<const bf16x8*>(Qb + (long long)(qrow < nq ? qrow : q0) * a.q_rs + c * 32 + g * 8);
+    // raw scores: lane holds, for query r, keys 32*kb + 8*g + j (j < 8)
+    float p[NB32][8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NB32; ++kb) {
+      if (kb >= nb32) continue;                      // uniform
+      const int k0 = kb * 32 + (r >> 2) * 8 + (r & 3), k1 = k0 + 4;
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&Ks[k0 * KLD + c * 32 + g * 8]);
+        const bf16x8 kc = *reinterpret_cast<const bf16x8*>(&Ks[k1 * KLD + c * 32 + g * 8]);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[c], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc, qf[c], s1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        p[kb][j] = s0[j];
+        p[kb][4 + j] = s1[j];
+      }
+      if (kb * 32 + 32 > nk) {                       // ragged last block (uniform)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (kb * 32 + g * 8 + j >= nk) p[kb][j] = -INFINITY;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) mx = fmaxf(mx, p[kb][j]);
+    }
+    const float mc = rows_max(mx) * c2;              // finite: key 0 is always valid
+    float l = 0.f;
+    bf16x8 pb[NB32];
+#pragma unroll
+    for (int kb = 0; kb < NB32; ++kb) {
+      if (kb >= nb32) continue;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(p[kb][j], c2, -mc));   // v_exp_f32; exp2(-inf) = 0
+        l += e;
+        pb[kb][j] = (bf16)e;
+      }
+    }
+    const float inv = 1.f / rows_sum(l);
+    f32x4 o[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < NB32; ++kb) {
+      if (kb >= nb32) continue;
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vt[(i * 16 + r) * VLD + kb * 32 + g * 8]);
+        o[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[kb], o[i], 0, 0, 0);
+      }
+    }
+    if (qrow >= nq) return;
+    bf16* Ob = static_cast<bf16*>(a.O) + b * a.o_bs + (long long)qrow * a.o_rs + h * DH;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      bf16x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = (bf16)(o[i][j] * inv);
+      *reinterpret_cast<bf16x4*>(Ob + i * 16 + g * 4) = w;
+    }
+  }
+}
+
+template <int DH, int WAVES>
+hipError_t launch_rows(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((k_attention_rows<DH, WAVES, 8>), dim3((unsigned)(a.n_heads * a.B)), dim3(WAVES * 64), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int DH, int WAVES, int QT, int KC>
 hipError_t launch_chunked(const AttnArgs& a, hipStream_t s) {
   const long long groups = (a.nq + WAVES * QT * 16 - 1) / (WAVES * QT * 16);
@@ -307,15 +446,22 @@ hipError_t launch_chunked(const AttnArgs& a, hipStream_t s) {
 
 template <int DH>
 hipError_t launch_bf16(const AttnArgs& a, hipStream_t s) {
+  // all keys in LDS, one workgroup per (batch, head), one query tile per wave (up to 16 waves)
+  if (a.nk <= 256 && a.nq > 16 && a.nq <= 256) {
+    if (a.nq > 128) return launch_rows<DH, 16>(a, s);
+    if (a.nq > 64) return launch_rows<DH, 8>(a, s);
+    return launch_rows<DH, 4>(a, s);
+  }
   if (a.nq <= 16) {
     // tiny groups (sequence encoder): one wave per (group, head)
     return a.nk <= 32 ? launch_chunked<DH, 1, 1, 32>(a, s) : launch_chunked<DH, 1, 1, 128>(a, s);
   }
-  // as many queries per workgroup as keep >= 256 workgroups, so K/V chunks are reused widely
+  // as many queries per workgroup as keep >= 1024 workgroups (four per compute unit, so each
+  // SIMD has several waves to switch between), so K/V chunks are still shared widely
   const long long bh = (long long)a.n_heads * a.B;
   auto wgs = [&](int qt) { return (a.nq + 64 * qt - 1) / (64 * qt) * bh; };
-  if (wgs(4) >= 256) return launch_chunked<DH, 4, 4, 128>(a, s);
-  if (wgs(2) >= 256) return launch_chunked<DH, 4, 2, 128>(a, s);
+  if (wgs(4) >= 1024) return launch_chunked<DH, 4, 4, 128>(a, s);
+  if (wgs(2) >= 1024) return launch_chunked<DH, 4, 2, 128>(a, s);
   return launch_chunked<DH, 4, 1, 128>(a, s);
 }
 
