@@ -324,7 +324,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_rows(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r = lane & 15;
-  const int h = blockIdx.x % a.n_heads, b = blockIdx.x / a.n_heads;
+  const int bh = xcd_tile(blockIdx.x, gridDim.x), h = bh % a.n_heads, b = bh / a.n_heads;
   int nq = a.nq, nk = a.nk;
   if (a.q_valid) nq = min(nq, a.q_valid[b]);
   if (a.k_valid) nk = min(nk, a.k_valid[b]);

@@ -35,6 +35,16 @@ FE_DEV float rows_sum(float v) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Tile handled by this workgroup when the tile range is split into eight contiguous parts, one
+// per XCD: workgroups are dispatched round-robin over the XCDs (workgroup i to XCD i % 8), so
+// XCD x takes tiles x*q + min(x, r) ... of n = 8q + r tiles.  Kernels that walk the same
+// batch-major row order then read, on each XCD, rows that the previous kernel wrote through
+// that XCD's own L2.  A bijection on [0, n) for every n.
+FE_DEV int xcd_tile(int i, int n) {
+  const int q = n >> 3, r = n & 7, x = i & 7, y = i >> 3;
+  return x * q + min(x, r) + y;
+}
+
 FE_DEV float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -36,7 +36,7 @@ __global__ __launch_bounds__(WG) void k_proj(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float Cs[4 * TM * 33];   // per-wave output staging
   __shared__ int s_valid[TM];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int row0 = blockIdx.x * TM;
+  const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
   const bf16* Wp = static_cast<const bf16*>(a.Wt);
   const int ncb = a.N / 32;
   const int ngroups = wave < ncb ? (ncb - wave + 4 * NBW - 1) / (4 * NBW) : 0;
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(WG) void k_ffn(FfnArgs a) {
   __shared__ __attribute__((aligned(16))) float Cs[4 * TM * 33];   // per-wave output staging
   __shared__ int s_valid[TM];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int row0 = blockIdx.x * TM;
+  const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
   const bf16* W1 = static_cast<const bf16*>(a.W1p);
   const bf16* W2 = static_cast<const bf16*>(a.W2p);
   const int KS2 = a.F / 16;

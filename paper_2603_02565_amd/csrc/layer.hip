@@ -395,7 +395,7 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   __shared__ __attribute__((aligned(16))) float s_g2[D], s_b2[D];
   __shared__ int s_valid[TM];
   const int lane = threadIdx.x & 63;
-  const int row0 = blockIdx.x * TM;
+  const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
 
   ColGemm<TM, D, D / 32> go;
   go.start(a.wo);
@@ -701,7 +701,7 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
   bf16* Hs = reinterpret_cast<bf16*>(big);
   const int lane = threadIdx.x & 63;
 
-  const int g0 = blockIdx.x * a.gpt;
+  const int g0 = xcd_tile(blockIdx.x, gridDim.x) * a.gpt;
   const int ng = min(a.gpt, a.n_groups - g0);
   const long long row0 = (long long)g0 * a.S;
   const int nrows = ng * a.S;
