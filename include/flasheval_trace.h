@@ -22,9 +22,10 @@ extern "C" {
 #define FE_TRACE_FAMILIES 11
 /* 0 "gemm" (projections and the key/value cache; on fp32 models also the FFN), 1 "attention",
  * 2 "layernorm", 3 "dedup", 4 "gather", 5 "assemble", 6 "score_select", 7 "fill",
- * 8 "ffn" (a standalone fused feed-forward sub-block), 9 "layer" (a whole encoder block in one
- * kernel, for short attention groups), 10 "post" (output projection, residual, LayerNorm and
- * FFN or query projection after a separate attention kernel) */
+ * 8 "ffn" (kept for index stability; no kernel of this family is launched), 9 "layer" (a whole
+ * encoder module -- every block and the final LayerNorm -- in one kernel, for short attention
+ * groups), 10 "post" (output projection, residual, LayerNorm and FFN or query projection after
+ * a separate attention kernel) */
 
 /* Turn tracing on (1) or off (0).  Turning it on discards earlier records. */
 fe_status fe_trace_enable(int on);

@@ -378,7 +378,7 @@ GemmArgs gemm(const void* A, int lda, bool a_f32, int R, int K, int N, const voi
 
 // One projection launch: packed-weight bf16 kernel or generic fp32 kernel.
 fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s);
-// X += FFN(LN(X)): fused on bf16 models, two generic launches through Hf on fp32 models.
+// X += FFN(LN(X)) on fp32 models: two generic launches through Hf.
 fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const float* lnb, const void* w1,
                   const float* b1, const void* w2, const float* b2, void* Hf, const int32_t* nvalid, int rpb,
                   hipStream_t s);
@@ -454,11 +454,6 @@ fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const fl
                   const float* b1, const void* w2, const float* b2, void* Hf, const int32_t* nvalid, int rpb,
                   hipStream_t s) {
   const int d = m->cfg.d, F = m->cfg.ffn_dim;
-  if (m->bf16) {
-    FfnArgs f{X, R, d, F, lng, lnb, w1, b1, w2, b2, nvalid, rpb};
-    FE_LAUNCH(F_FFN, s, launch_ffn(f, s));
-    return FE_OK;
-  }
   GemmArgs g = gemm(X, d, true, R, d, F, w1, b1, Hf, F, false, EPI_RELU);
   g.ln_g = lng; g.ln_b = lnb; g.nvalid = nvalid; g.rows_per_batch = rpb;
   FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));

@@ -96,16 +96,6 @@ struct AttnArgs {
   float scale;
 };
 
-// X += W2 ReLU(LN(X) W1 + b1) + b2 over R rows of fp32 X [R][D] (bf16 models; weights packed
-// in MFMA B-operand order).  Padding rows (per nvalid) are neither read nor written.
-struct FfnArgs {
-  float* X; int R, D, F;
-  const float* ln_g; const float* ln_b;
-  const void* W1p; const float* b1;
-  const void* W2p; const float* b2;
-  const int32_t* nvalid; int rows_per_batch;
-};
-
 // Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
 //   tail 0: Xout = x1 + FFN(LN2(x1));
 //   tail 1: Xout = x1 and Qout = LN2(x1) Wq + bq (bf16).
@@ -145,7 +135,6 @@ hipError_t launch_module_small(ModuleArgs a, hipStream_t s);
 hipError_t launch_post(const PostArgs& a, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s);   // fp32 models
 hipError_t launch_proj(const GemmArgs& a, hipStream_t s);                    // bf16 models, K = d
-hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);                      // bf16 models
 hipError_t launch_attention(const AttnArgs& a, bool bf16_model, hipStream_t s);
 hipError_t launch_layernorm(const void* X, int x_f32, long long x_rs, int R, int d, const float* g,
                             const float* b, void* Y, int y_f32, long long y_rs, bool bf16_model,

@@ -159,4 +159,127 @@ FE_DEV void stage_rows_lds(const float* X, int ldx, const int* s_valid, const fl
   }
 }
 
+// Column-split product over an LDS tile: wave w computes the 32-column output blocks
+// w + 4j (j < NCB/4) of As[TM][K] x W, NBW blocks at a time, with the weight fragments
+// streamed through registers one 8-fragment stage ahead (all shapes compile-time, so the
+// stage loop unrolls completely and fragment addresses are immediate offsets).  start() issues the first
+// stage (so its latency can hide behind other work); run() calls epi(cb, rb, acc) for every
+// finished 32x32 block: epi(jj, cb, rb, acc) with jj the wave-local block index (compile-time
+// after unrolling), cb = wave + 4*jj the column block and rb the row block.
+//
+// The product is formed transposed, C^T = W^T A^T: the packed weight fragments are the A
+// operand and the activation fragments the B operand.  Each lane then holds one output ROW
+// (rb*32 + lane%32) and, in acc[4q..4q+3], the four consecutive output columns
+// 8q + 4*(lane/32) .. +3 of the block (q = 0..3), so epilogues write 8- or 16-byte vectors.
+template <int TM, int K, int NCB>
+struct ColGemm {
+  static constexpr int RB = TM / 32, KS = K / 16, NBW = 4 / RB;
+  static constexpr int BPW = NCB / 4;                            // column blocks per wave
+  static constexpr int KB = (8 / NBW < KS) ? 8 / NBW : KS;      // k-steps per stage (8 fragments)
+  static constexpr int NSK = KS / KB;                            // stages per column group
+  static constexpr int NG = (BPW + NBW - 1) / NBW;               // column groups per wave
+  static constexpr int NST = NG * NSK;                           // stages per wave
+  static_assert(NCB % 4 == 0 && KS % KB == 0, "unsupported shape");
+  bf16x8 buf[2][NBW][KB];
+  const bf16x8* Wl;   // this wave's first column block, this lane's fragment slot
+
+  static constexpr int blocks_in(int g) { return (g + 1) * NBW <= BPW ? NBW : BPW - g * NBW; }
+  FE_DEV void load(int t) {
+    const int g = t / NSK, sk = t % NSK;
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+      if (j >= blocks_in(g)) continue;
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk) buf[t & 1][j][kk] = Wl[((4 * (g * NBW + j)) * KS + sk * KB + kk) * 64];
+    }
+  }
+  FE_DEV void start(const void* W) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    Wl = reinterpret_cast<const bf16x8*>(W) + (long long)wave * KS * 64 + (threadIdx.x & 63);
+    load(0);
+  }
+  template <class Epi>
+  FE_DEV void run(const bf16* As, int lda, Epi&& epi) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    f32x16 acc[RB][NBW];
+#pragma unroll
+    for (int t = 0; t < NST; ++t) {
+      const int g = t / NSK, sk = t % NSK;
+      if (t + 1 < NST) load(t + 1);
+      if (sk == 0) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int j = 0; j < NBW; ++j) acc[rb][j] = f32x16{};
+      }
+      bf16x8 af[KB][RB];
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) af[kk][rb] = a_frag(As, lda, rb * 32, (sk * KB + kk) * 16, lane);
+#pragma unroll
+      for (int kk = 0; kk < KB; ++kk)
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) {
+          if (j >= blocks_in(g)) continue;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            acc[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][j][kk], af[kk][rb], acc[rb][j], 0, 0, 0);
+        }
+      if (sk != NSK - 1) continue;
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+        if (j >= blocks_in(g)) continue;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) epi(g * NBW + j, wave + 4 * (g * NBW + j), rb, acc[rb][j]);
+      }
+    }
+  }
+};
+
+// Epilogues of a transposed 32x32 block (see ColGemm): row rb*32 + lane%32, columns
+// cb*32 + 8q + 4*(lane/32) + e hold acc[4q + e].
+FE_DEV void block_to_lds_bf16(const f32x16& acc, int cb, int rb, const float* bias, bf16* dst, int ld) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int qq = 0; qq < 4; ++qq) {
+    const int n = cb * 32 + qq * 8 + (lane >> 5) * 4;
+    const float4 bb = *reinterpret_cast<const float4*>(&bias[n]);
+    bf16x4 o;
+    o[0] = (bf16)(acc[4 * qq] + bb.x);
+    o[1] = (bf16)(acc[4 * qq + 1] + bb.y);
+    o[2] = (bf16)(acc[4 * qq + 2] + bb.z);
+    o[3] = (bf16)(acc[4 * qq + 3] + bb.w);
+    *reinterpret_cast<bf16x4*>(&dst[(rb * 32 + (lane & 31)) * ld + n]) = o;
+  }
+}
+FE_DEV void block_to_lds_f32(const f32x16& acc, int cb, int rb, const float* bias, float* dst, int ld) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int qq = 0; qq < 4; ++qq) {
+    const int n = cb * 32 + qq * 8 + (lane >> 5) * 4;
+    const float4 bb = *reinterpret_cast<const float4*>(&bias[n]);
+    *reinterpret_cast<float4*>(&dst[(rb * 32 + (lane & 31)) * ld + n]) =
+        make_float4(acc[4 * qq] + bb.x, acc[4 * qq + 1] + bb.y, acc[4 * qq + 2] + bb.z, acc[4 * qq + 3] + bb.w);
+  }
+}
+
+// Write a transposed 32x32 block plus bias as bf16 through the wave's LDS staging area st
+// (32 x 40 bf16): the block's rows leave as 16-byte row segments.  out points at the block's
+// first column in row 0 of the tile (row stride ld); rows rb*32 + r with s_valid set are written.
+FE_DEV void store_block_bf16(const f32x16& acc, const float* bias, bf16* st, bf16* out, long long ld, int rb,
+                             const int* s_valid) {
+  const int lane = threadIdx.x & 63;
+  block_to_lds_bf16(acc, 0, 0, bias, st, 40);
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int e = it * 64 + lane, r = e >> 2, c8 = (e & 3) * 8;
+    const int rr = rb * 32 + r;
+    if (s_valid[rr]) *reinterpret_cast<bf16x8*>(out + (long long)rr * ld + c8) = *reinterpret_cast<const bf16x8*>(&st[r * 40 + c8]);
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
 }  // namespace fe_tile
