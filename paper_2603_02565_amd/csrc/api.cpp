@@ -611,7 +611,10 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
   const bool bf = m->bf16;
   const int d = m->cfg.d, R = B * T;
   int32_t* status_ctx = at<int32_t>(ws, w.status) + B;
-  FE_LAUNCH(F_FILL, s, launch_fill_i32(status_ctx, B, 0, s));
+  // the context status words start at zero: cleared before the embedding gather sets bits in
+  // them, else by the key/value projection at the end of this call (nothing else writes them)
+  const bool clear_late = bf && !ctx_ids;
+  if (!clear_late) FE_LAUNCH(F_FILL, s, launch_fill_i32(status_ctx, B, 0, s));
   const void* src = x;
   if (ctx_ids) {
     FE_LAUNCH(F_GATHER, s, launch_gather_rows(m->emb, 0, m->cfg.vocab, ctx_ids, T, nullptr, B, T, d, at<char>(ws, w.c_xin), status_ctx,
@@ -637,6 +640,10 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
     g.ln_b = m->ctx_lnf_b;
   }
   g.col_block = d; g.col_block_stride = (long long)R * d;
+  if (clear_late) {
+    g.zero = status_ctx;
+    g.zero_n = B;
+  }
   return run_proj(m, g, s);
 }
 
@@ -714,8 +721,11 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     c.scale = 1.0f / sqrtf((float)dh);
     FE_LAUNCH(F_ATTN, s, launch_attention(c, bf, s));
     if (bf) {
-      PostArgs p{O, G, 1, G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
-                 iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr};
+      // the last layer also applies the module's final LayerNorm and writes H directly
+      const bool last = l + 1 == m->cfg.n_layers;
+      PostArgs p{O, G, 1, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
+                 iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr,
+                 last ? m->item_lnf_g : nullptr, last ? m->item_lnf_b : nullptr, last ? H : nullptr};
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }
@@ -726,7 +736,8 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     st = run_ffn(m, G, R, iw.ln3g, iw.ln3b, iw.w1, iw.b1, iw.w2, iw.b2, Hf, n_uniq, Ucap, s);
     if (st != FE_OK) return st;
   }
-  FE_LAUNCH(F_LN, s, launch_layernorm_masked(G, 1, d, R, d, m->item_lnf_g, m->item_lnf_b, H, 0, d, n_uniq, Ucap, bf, s));
+  if (!bf)
+    FE_LAUNCH(F_LN, s, launch_layernorm_masked(G, 1, d, R, d, m->item_lnf_g, m->item_lnf_b, H, 0, d, n_uniq, Ucap, bf, s));
   return FE_OK;
 }
 

@@ -80,6 +80,7 @@ struct GemmArgs {
   int epi;
   const void* res; int ldr; int res_f32;
   const int32_t* nvalid; int rows_per_batch;
+  int32_t* zero; int zero_n;           // bf16 projection: zero[0 .. zero_n) is cleared (or nullptr)
 };
 
 // O = softmax(Q K^T * scale) V per (batch, head).  Q rows of batch b start at
@@ -97,7 +98,9 @@ struct AttnArgs {
 };
 
 // Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
-//   tail 0: Xout = x1 + FFN(LN2(x1));
+//   tail 0: Xout = x1 + FFN(LN2(x1)); with Hout != nullptr also Hout = LayerNorm(x1 + FFN)
+//           with gains lnfg, offsets lnfb (bf16), padding rows of Hout below R set to zero
+//           (Xout may then be nullptr);
 //   tail 1: Xout = x1 and Qout = LN2(x1) Wq + bq (bf16).
 // Rows with (r % rows_per_batch) >= nvalid[r / rows_per_batch] are padding.
 struct PostArgs {
@@ -107,6 +110,7 @@ struct PostArgs {
   const void* wo; const float* bo; const float *ln2g, *ln2b;
   const void* w1; const float* b1; const void* w2; const float* b2;
   const void* wq; const float* bq; void* Qout;
+  const float *lnfg, *lnfb; void* Hout;
 };
 
 // Device pointers of one pre-LN encoder block (matrices of bf16 models in packed fragment order).

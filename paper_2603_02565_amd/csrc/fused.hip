@@ -28,6 +28,8 @@ __global__ __launch_bounds__(WG, 2) void k_proj(GemmArgs a) {
   const int wave = threadIdx.x >> 6;
   const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
   const int cb0 = blockIdx.y * NCB;                 // first column block of the slab
+  if (a.zero && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < a.zero_n; i += WG) a.zero[i] = 0;
 
   ColGemm<TM, D, NCB> gq;
   gq.start(static_cast<const bf16x8*>(a.Wt) + (long long)cb0 * KS * 64);

@@ -133,25 +133,47 @@ __global__ __launch_bounds__(256) void k_assemble(const int32_t* __restrict__ sl
 }
 
 // ------------------------------------------------------------------------------------------
-// Score head and selection: one workgroup per request.  Each wave forms whole dot products
-// (fixed reduction order, so identical rows give identical scores wherever they sit), then a
-// block reduction keeps the largest non-NaN score with the smallest index.
+// Score head and selection: one workgroup per request (XCD-contiguous, like the cross-sequence
+// module that wrote Cp).  A group of LPR = min(16, D/4) lanes forms one dot product (lane l sums
+// columns 4(l + LPR*i) .. +3 in a fixed order, then a fixed butterfly over the group), so
+// identical rows give identical scores wherever they sit; each thread keeps RPT rows in flight.  A
+// block reduction then keeps the largest non-NaN score with the smallest index.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_score_select(const float* __restrict__ Cp, int K, int d,
-                                                      const float* __restrict__ w, const float* __restrict__ bias,
-                                                      float* __restrict__ scores, int32_t* __restrict__ best) {
+template <int D>
+__global__ __launch_bounds__(256) void k_score_select(const float* __restrict__ Cp, int K, const float* __restrict__ w,
+                                                      const float* __restrict__ bias, float* __restrict__ scores,
+                                                      int32_t* __restrict__ best) {
+  constexpr int LPR = D / 4 < 16 ? D / 4 : 16, NV = D / (4 * LPR), NG = 256 / LPR, RPT = 4;
   __shared__ float s_val[256];
   __shared__ int s_idx[256];
   __shared__ float s_score[4096];
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const float* cb = Cp + (long long)b * K * d;
-  for (int k = wave; k < K; k += 4) {
-    float acc = 0.f;
-    for (int i = lane; i < d; i += 64) acc += cb[(long long)k * d + i] * w[i];
-    acc = wave_sum(acc) + bias[0];
-    if (lane == 0) {
-      scores[(long long)b * K + k] = acc;
-      s_score[k] = acc;
+  const int b = xcd_tile(blockIdx.x, gridDim.x), tid = threadIdx.x, l16 = tid % LPR, grp = tid / LPR;
+  const float* cb = Cp + (long long)b * K * D;
+  float4 wv[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) wv[i] = *reinterpret_cast<const float4*>(&w[4 * (l16 + LPR * i)]);
+  const float b0 = bias[0];
+  for (int k0 = grp; k0 < K; k0 += NG * RPT) {
+    float4 xv[RPT][NV];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      const int k = min(k0 + NG * r, K - 1);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) xv[r][i] = *reinterpret_cast<const float4*>(&cb[(long long)k * D + 4 * (l16 + LPR * i)]);
+    }
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < NV; ++i)
+        acc += xv[r][i].x * wv[i].x + xv[r][i].y * wv[i].y + xv[r][i].z * wv[i].z + xv[r][i].w * wv[i].w;
+#pragma unroll
+      for (int o = 1; o < LPR; o <<= 1) acc += __shfl_xor(acc, o, LPR);
+      const int k = k0 + NG * r;
+      if (l16 == 0 && k < K) {
+        scores[(long long)b * K + k] = acc + b0;
+        s_score[k] = acc + b0;
+      }
     }
   }
   __syncthreads();
@@ -234,6 +256,13 @@ hipError_t launch_assemble(const int32_t* slot, const void* H, int B, int K, int
 
 hipError_t launch_score_select(const float* Cp, int B, int K, int d, const float* w, const float* bias, float* scores,
                                int32_t* best, hipStream_t s) {
-  hipLaunchKernelGGL(k_score_select, dim3(B), dim3(256), 0, s, Cp, K, d, w, bias, scores, best);
+  switch (d) {
+    case 32: hipLaunchKernelGGL(k_score_select<32>, dim3(B), dim3(256), 0, s, Cp, K, w, bias, scores, best); break;
+    case 64: hipLaunchKernelGGL(k_score_select<64>, dim3(B), dim3(256), 0, s, Cp, K, w, bias, scores, best); break;
+    case 128: hipLaunchKernelGGL(k_score_select<128>, dim3(B), dim3(256), 0, s, Cp, K, w, bias, scores, best); break;
+    case 256: hipLaunchKernelGGL(k_score_select<256>, dim3(B), dim3(256), 0, s, Cp, K, w, bias, scores, best); break;
+    case 512: hipLaunchKernelGGL(k_score_select<512>, dim3(B), dim3(256), 0, s, Cp, K, w, bias, scores, best); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }

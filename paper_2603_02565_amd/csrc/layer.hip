@@ -280,60 +280,6 @@ FE_DEV void ffn_tail(Ffn<TM, D>& ffn, float* Xs, int ldx, bf16* As, bf16* Hs, co
   store_rows<TM, D>(Xs, ldx, Xout, row0, s_valid);
 }
 
-template <int TM, int D, int TAIL>
-__global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
-  constexpr int LDA = D + APAD, LDX = D + 4;
-  __shared__ __attribute__((aligned(16))) bf16 As[TM * LDA];
-  __shared__ __attribute__((aligned(16))) float Xs[TM * LDX];
-  __shared__ __attribute__((aligned(16))) bf16 Hs[TM * HLD];
-  __shared__ __attribute__((aligned(16))) float s_g2[D], s_b2[D];
-  __shared__ int s_valid[TM];
-  const int lane = threadIdx.x & 63;
-  const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
-
-  ColGemm<TM, D, D / 32> go;
-  go.start(a.wo);
-  copy_ln_params<D>(a.ln2g, a.ln2b, s_g2, s_b2);
-  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
-  stage_rows<TM, D>(a.O, false, D, row0, s_valid, nullptr, nullptr, As);
-  Ffn<TM, D> ffn;
-  ColGemm<TM, D, D / 32> gq;
-  if constexpr (TAIL == 0) ffn.preload(a.w1, a.w2, a.F);
-  __syncthreads();
-
-  go.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) { block_to_lds_f32(acc, cb, rb, a.bo, Xs, LDX); });
-  if constexpr (TAIL == 1) gq.start(a.wq);
-  __syncthreads();
-  add_rows<TM, D>(Xs, LDX, a.Xin, a.xin_f32, row0, s_valid);
-  __syncthreads();
-  if constexpr (TAIL == 0) {
-    ffn_tail<TM, D>(ffn, Xs, LDX, As, Hs, s_g2, s_b2, a.b1, a.b2, a.Xout, row0, s_valid);
-  } else {
-    // x1 leaves as the new residual stream; q = LN2(x1) Wq + bq for the cross-attention
-    store_rows<TM, D>(Xs, LDX, a.Xout, row0, s_valid);
-    stage_rows_lds<TM, D>(Xs, LDX, s_valid, s_g2, s_b2, As);
-    __syncthreads();
-    bf16* Qs = reinterpret_cast<bf16*>(Xs);   // Xs is dead now: per-wave 32 x 32 bf16 staging
-    const int wave = threadIdx.x >> 6;
-    gq.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) {
-      bf16* st = Qs + wave * 32 * 40;
-      // the block's rows land in the wave's 32 x 32 staging area (columns relative to cb*32)
-      block_to_lds_bf16(acc, 0, 0, a.bq + cb * 32, st, 40);
-      __builtin_amdgcn_wave_barrier();
-      // 32 rows x 64 bytes: 4 lanes per row, 16 bytes each, two passes
-#pragma unroll
-      for (int it = 0; it < 2; ++it) {
-        const int e = it * 64 + lane, r = e >> 2, c8 = (e & 3) * 8;
-        const int rr = rb * 32 + r;
-        if (s_valid[rr])
-          *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.Qout) + (long long)(row0 + rr) * D + cb * 32 + c8) =
-              *reinterpret_cast<const bf16x8*>(&st[r * 40 + c8]);
-      }
-      __builtin_amdgcn_wave_barrier();
-    });
-  }
-}
-
 // ------------------------------------------------------------------------------------------
 // Whole modules over short groups, residual stream in registers.
 //
@@ -664,6 +610,114 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
                         (v[4 * q + 2] - mean[rb]) * rstd[rb] * gg[j][q].z + bb[j][q].z,
                         (v[4 * q + 3] - mean[rb]) * rstd[rb] * gg[j][q].w + bb[j][q].w);
       }
+  }
+}
+
+// Residual rows of x to Xout (fp32, row stride D) for valid tile rows.
+template <int TM, int D>
+FE_DEV void resid_store(const Resid<TM, D>& x, float* Xout, long long row0, const int* s_valid) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int rb = 0; rb < TM / 32; ++rb) {
+    const int r = rb * 32 + (lane & 31);
+    if (!s_valid[r]) continue;
+    float* y = Xout + (row0 + r) * D;
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& v = x.v[j][rb];
+        *reinterpret_cast<float4*>(&y[resid_col(j, q)]) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+      }
+  }
+}
+
+// Rows [row0, row0 + TM) of the bf16 output Y that lie below R get zeros (padding rows).
+template <int TM, int D>
+FE_DEV void zero_rows_bf16(bf16* Y, long long row0, long long R, const int* s_valid) {
+  for (int e = threadIdx.x; e < TM * D / 8; e += WG) {
+    const int rr = e / (D / 8), c = (e % (D / 8)) * 8;
+    if (row0 + rr >= R || (s_valid && s_valid[rr])) continue;
+    *reinterpret_cast<bf16x8*>(Y + (row0 + rr) * D + c) = bf16x8{};
+  }
+}
+
+// The tail of a block whose attention ran in a separate kernel (long groups), bf16 models:
+//   x1 = Xin + O Wo + bo (residual in registers), then
+//   TAIL 0: x2 = x1 + FFN(LN2(x1)) -> Xout (fp32); when Hout is set (last item layer) also
+//           Hout = LNf(x2) in bf16, with zero rows for padding rows;
+//   TAIL 1: Xout = x1, and the item layers' cross-attention queries Qout = LN2(x1) Wq + bq (bf16).
+template <int TM, int D, int TAIL>
+__global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
+  constexpr int LDA = D + APAD;
+  constexpr int HS_BYTES = 2 * TM * HLD * 2, QS_BYTES = 4 * 32 * 40 * 2;
+  constexpr int BIG = HS_BYTES > QS_BYTES ? HS_BYTES : QS_BYTES;
+  __shared__ __attribute__((aligned(16))) bf16 As[TM * LDA];
+  __shared__ __attribute__((aligned(16))) char big[BIG];
+  __shared__ __attribute__((aligned(16))) float2 s_stat[4 * TM];
+  __shared__ int s_valid[TM];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
+
+  ColGemm<TM, D, D / 32> go;
+  go.start(a.wo);
+  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) {
+    if (TAIL == 0 && a.Hout) zero_rows_bf16<TM, D>(static_cast<bf16*>(a.Hout), row0, a.R, nullptr);
+    return;
+  }
+  stage_rows<TM, D>(a.O, false, D, row0, s_valid, nullptr, nullptr, As);
+  Resid<TM, D> x;
+  resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
+  FfnStream<TM, D> ffn;
+  if constexpr (TAIL == 0) ffn.start(a.w1, a.w2, a.F);
+  __syncthreads();
+  go.run(As, LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, a.bo); });
+  ColGemm<TM, D, D / 32> gq;
+  if constexpr (TAIL == 1) gq.start(a.wq);
+  // LN2 -> As (the barrier inside the statistics retires every read of As by the Wo product)
+  resid_ln_to_lds<TM, D>(x, a.ln2g, a.ln2b, s_stat, As);
+  __syncthreads();
+  if constexpr (TAIL == 0) {
+    ffn.run(As, reinterpret_cast<bf16*>(big), a.b1, x);
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int rb = 0; rb < TM / 32; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, a.b2);
+    if (a.Xout) resid_store<TM, D>(x, a.Xout, row0, s_valid);
+    if (a.Hout) {
+      // final LayerNorm of the module into bf16 H; padding rows of the tile become zeros
+      float mean[TM / 32], rstd[TM / 32];
+      resid_stats<TM, D>(x, s_stat, mean, rstd);
+      bf16* H = static_cast<bf16*>(a.Hout);
+#pragma unroll
+      for (int rb = 0; rb < TM / 32; ++rb) {
+        const int r = rb * 32 + (lane & 31);
+        if (!s_valid[r]) continue;
+#pragma unroll
+        for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int c = resid_col(j, q);
+            const float4 gg = *reinterpret_cast<const float4*>(&a.lnfg[c]);
+            const float4 bb = *reinterpret_cast<const float4*>(&a.lnfb[c]);
+            const f32x16& v = x.v[j][rb];
+            bf16x4 o;
+            o[0] = (bf16)((v[4 * q] - mean[rb]) * rstd[rb] * gg.x + bb.x);
+            o[1] = (bf16)((v[4 * q + 1] - mean[rb]) * rstd[rb] * gg.y + bb.y);
+            o[2] = (bf16)((v[4 * q + 2] - mean[rb]) * rstd[rb] * gg.z + bb.z);
+            o[3] = (bf16)((v[4 * q + 3] - mean[rb]) * rstd[rb] * gg.w + bb.w);
+            *reinterpret_cast<bf16x4*>(H + ((long long)row0 + r) * D + c) = o;
+          }
+      }
+      zero_rows_bf16<TM, D>(H, row0, a.R, s_valid);
+    }
+  } else {
+    resid_store<TM, D>(x, a.Xout, row0, s_valid);
+    bf16* st = reinterpret_cast<bf16*>(big) + wave * 32 * 40;
+    bf16* Q = static_cast<bf16*>(a.Qout) + (long long)row0 * D;
+    gq.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) {
+      store_block_bf16(acc, a.bq + cb * 32, st, Q + cb * 32, D, rb, s_valid);
+    });
   }
 }
 
