@@ -290,7 +290,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
     if (q0_of(t) >= nq) continue;
     const float l_tot = rows_sum(l_run[t]);
     if (qrow >= nq) continue;
-    const float inv = 1.f / l_tot;
+    const float inv = __builtin_amdgcn_rcpf(l_tot);   // v_rcp_f32
     bf16* Ob = static_cast<bf16*>(a.O) + b * a.o_bs + (long long)qrow * a.o_rs + h * DH;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
@@ -405,7 +405,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_rows(AttnArgs a) {
         pb[kb][j] = (bf16)e;
       }
     }
-    const float inv = 1.f / rows_sum(l);
+    const float inv = __builtin_amdgcn_rcpf(rows_sum(l));   // v_rcp_f32
     f32x4 o[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};

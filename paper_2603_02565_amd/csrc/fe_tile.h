@@ -56,7 +56,7 @@ FE_DEV void stage_rows_t(const TA* A, long long lda, int row0, const int* s_vali
     for (int i = 0; i < NV * VE; ++i) { const float t = v[i] - mean; q += t * t; }
 #pragma unroll
     for (int o = 1; o < TPR; o <<= 1) q += __shfl_xor(q, o, 64);
-    const float rstd = rsqrtf(q / (float)D + 1e-5f);
+    const float rstd = rsqrtf(q / (float)D + 1e-5f), nm = -mean * rstd;
     const float4* g4 = reinterpret_cast<const float4*>(g);   // LDS copies (copy_ln_params)
     const float4* b4 = reinterpret_cast<const float4*>(b);
 #pragma unroll
@@ -66,10 +66,10 @@ FE_DEV void stage_rows_t(const TA* A, long long lda, int row0, const int* s_vali
         const int idx = (i * TPR + part) * (VE / 4) + h;
         const float4 gg = g4[idx], bb = b4[idx];
         float* x = &v[i * VE + 4 * h];
-        x[0] = (x[0] - mean) * rstd * gg.x + bb.x;
-        x[1] = (x[1] - mean) * rstd * gg.y + bb.y;
-        x[2] = (x[2] - mean) * rstd * gg.z + bb.z;
-        x[3] = (x[3] - mean) * rstd * gg.w + bb.w;
+        x[0] = fmaf(fmaf(x[0], rstd, nm), gg.x, bb.x);
+        x[1] = fmaf(fmaf(x[1], rstd, nm), gg.y, bb.y);
+        x[2] = fmaf(fmaf(x[2], rstd, nm), gg.z, bb.z);
+        x[3] = fmaf(fmaf(x[3], rstd, nm), gg.w, bb.w);
       }
   }
 #pragma unroll
@@ -96,13 +96,6 @@ FE_DEV bf16x8 a_frag(const bf16* As, int ld, int row_base, int k0, int lane) {
   return *reinterpret_cast<const bf16x8*>(&As[(row_base + (lane & 31)) * ld + k0 + (lane >> 5) * 8]);
 }
 
-FE_DEV bf16x8 b_frag(const bf16* Wp, int ksteps, int cb, int ks, int lane) {
-  return reinterpret_cast<const bf16x8*>(Wp)[((long long)cb * ksteps + ks) * 64 + lane];
-}
-
-// row (within the 32-row block) of accumulator element i for this lane
-FE_DEV int acc_row(int i, int lane) { return (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3); }
-
 template <int TM>
 FE_DEV bool mark_rows(int row0, int R, const int32_t* nvalid, int rpb, int* s_valid) {
   int v = 0;
@@ -115,49 +108,6 @@ FE_DEV bool mark_rows(int row0, int R, const int32_t* nvalid, int rpb, int* s_va
   return __syncthreads_or(v);
 }
 
-
-// Stage rows of an fp32 LDS tile X (row stride ldx) into LDS as bf16 LayerNorm(X), same thread
-// mapping as stage_rows_t.  Rows whose s_valid flag is 0 are written as zeros.
-template <int TM, int D>
-FE_DEV void stage_rows_lds(const float* X, int ldx, const int* s_valid, const float* g, const float* b, bf16* As) {
-  constexpr int TPR = WG / TM;
-  constexpr int NV = D / (4 * TPR);
-  constexpr int LD = D + APAD;
-  const int tid = threadIdx.x;
-  const int rr = tid / TPR, part = tid % TPR;
-  const bool valid = s_valid[rr];
-  float v[NV * 4];
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const float4 t = *reinterpret_cast<const float4*>(&X[rr * ldx + (i * TPR + part) * 4]);
-    v[4 * i] = t.x; v[4 * i + 1] = t.y; v[4 * i + 2] = t.z; v[4 * i + 3] = t.w;
-  }
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < NV * 4; ++i) s += v[i];
-#pragma unroll
-  for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
-  const float mean = s / (float)D;
-  float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < NV * 4; ++i) { const float t = v[i] - mean; q += t * t; }
-#pragma unroll
-  for (int o = 1; o < TPR; o <<= 1) q += __shfl_xor(q, o, 64);
-  const float rstd = rsqrtf(q / (float)D + 1e-5f);
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int k = (i * TPR + part) * 4;
-    const float4 gg = *reinterpret_cast<const float4*>(&g[k]);
-    const float4 bb = *reinterpret_cast<const float4*>(&b[k]);
-    bf16x4 o;
-    o[0] = (bf16)((v[4 * i] - mean) * rstd * gg.x + bb.x);
-    o[1] = (bf16)((v[4 * i + 1] - mean) * rstd * gg.y + bb.y);
-    o[2] = (bf16)((v[4 * i + 2] - mean) * rstd * gg.z + bb.z);
-    o[3] = (bf16)((v[4 * i + 3] - mean) * rstd * gg.w + bb.w);
-    if (!valid) o = bf16x4{};
-    *reinterpret_cast<bf16x4*>(&As[rr * LD + k]) = o;
-  }
-}
 
 // Column-split product over an LDS tile: wave w computes the 32-column output blocks
 // w + 4j (j < NCB/4) of As[TM][K] x W, NBW blocks at a time, with the weight fragments
@@ -252,16 +202,6 @@ FE_DEV void block_to_lds_bf16(const f32x16& acc, int cb, int rb, const float* bi
     o[2] = (bf16)(acc[4 * qq + 2] + bb.z);
     o[3] = (bf16)(acc[4 * qq + 3] + bb.w);
     *reinterpret_cast<bf16x4*>(&dst[(rb * 32 + (lane & 31)) * ld + n]) = o;
-  }
-}
-FE_DEV void block_to_lds_f32(const f32x16& acc, int cb, int rb, const float* bias, float* dst, int ld) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int qq = 0; qq < 4; ++qq) {
-    const int n = cb * 32 + qq * 8 + (lane >> 5) * 4;
-    const float4 bb = *reinterpret_cast<const float4*>(&bias[n]);
-    *reinterpret_cast<float4*>(&dst[(rb * 32 + (lane & 31)) * ld + n]) =
-        make_float4(acc[4 * qq] + bb.x, acc[4 * qq + 1] + bb.y, acc[4 * qq + 2] + bb.z, acc[4 * qq + 3] + bb.w);
   }
 }
 

@@ -24,107 +24,15 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr int HC = 128;              // FFN hidden chunk
 constexpr int HLD = HC + APAD;
 
-// FFN of a TM-row tile: acc_o += ReLU(As W1 + b1) W2 over 128-wide hidden chunks through Hs.
-// Wave w produces hidden columns 32w..32w+31 of each chunk and accumulates output column
-// blocks w + 4j.  Each phase's weight fragments are requested one phase ahead; the caller
-// issues ffn_preload() for chunk 0 earlier.
-template <int TM, int D>
-struct Ffn {
-  static constexpr int RB = TM / 32, KS = D / 16, OCB = D / 128;
-  bf16x8 w1[KS], w2[OCB][HC / 16];
-  const bf16x8 *W1l, *W2l;   // this wave's first column block, this lane's fragment slot
-  int F;
-  FE_DEV void load_w1(int c) {
-    // W1 [D][F]: column block 4c + wave, k-steps 0..KS-1
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) w1[ks] = W1l[((long long)c * 4 * KS + ks) * 64];
-  }
-  FE_DEV void load_w2(int c) {
-    // W2 [F][D]: column blocks wave + 4j, k-steps 8c..8c+7 of F/16
-    const int ks2 = F / 16;
-#pragma unroll
-    for (int j = 0; j < OCB; ++j)
-#pragma unroll
-      for (int ks = 0; ks < HC / 16; ++ks) w2[j][ks] = W2l[((long long)4 * j * ks2 + c * (HC / 16) + ks) * 64];
-  }
-  FE_DEV void preload(const void* w1p, const void* w2p, int f) {
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-    F = f;
-    W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
-    W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (f / 16) * 64 + lane;
-    load_w1(0);
-    load_w2(0);
-  }
-  FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, f32x16 (&acc_o)[RB][OCB]) {
-    constexpr int LD = D + APAD;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int j = 0; j < OCB; ++j) acc_o[rb][j] = f32x16{};
-    const int nchunks = F / HC;
-    for (int c = 0; c < nchunks; ++c) {
-      // this lane's hidden columns of the chunk: 32*wave + 8q + 4*(lane/32) + e
-      float4 bias1[4];
-#pragma unroll
-      for (int qq = 0; qq < 4; ++qq)
-        bias1[qq] = *reinterpret_cast<const float4*>(&b1[(c * 4 + wave) * 32 + qq * 8 + (lane >> 5) * 4]);
-      f32x16 acc_h[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) acc_h[rb] = f32x16{};
-      {
-        // all A fragments of the phase first, so the matrix instructions run back to back
-        bf16x8 af[KS][RB];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) af[ks][rb] = a_frag(As, LD, rb * 32, ks * 16, lane);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-            acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1[ks], af[ks][rb], acc_h[rb], 0, 0, 0);
-      }
-      if (c + 1 < nchunks) load_w1(c + 1);
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const float* bb = reinterpret_cast<const float*>(&bias1[qq]);
-          bf16x4 h;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) h[e] = (bf16)fmaxf(acc_h[rb][4 * qq + e] + bb[e], 0.f);
-          *reinterpret_cast<bf16x4*>(&Hs[(rb * 32 + (lane & 31)) * HLD + wave * 32 + qq * 8 + (lane >> 5) * 4]) = h;
-        }
-      __syncthreads();
-      {
-        bf16x8 af[HC / 16][RB];
-#pragma unroll
-        for (int ks = 0; ks < HC / 16; ++ks)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) af[ks][rb] = a_frag(Hs, HLD, rb * 32, ks * 16, lane);
-#pragma unroll
-        for (int ks = 0; ks < HC / 16; ++ks)
-#pragma unroll
-          for (int j = 0; j < OCB; ++j)
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-              acc_o[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w2[j][ks], af[ks][rb], acc_o[rb][j], 0, 0, 0);
-      }
-      if (c + 1 < nchunks) load_w2(c + 1);
-      __syncthreads();
-    }
-  }
-};
-
 // Attention inside groups of S consecutive tile rows (S <= 16*NKB), reading q|k|v from the
 // LDS tile QKVs (row stride ldq; query columns 0..D-1, keys D..2D-1, values 2D..3D-1) and
-// writing the per-head outputs into Os (row stride lds).  One wave per (group, head, 16-query
+// writing the per-head outputs into Os (row stride lds); with FIRST_TILE only the first 16
+// queries of each group are computed.  One wave per (group, head, 16-query
 // tile), two such units in flight per wave: the NKB score blocks are formed first as
 // independent MFMA chains, then one softmax over the whole group, then P V.
-template <int D, int DH, int NKB>
+template <int D, int DH, int NKB, bool FIRST_TILE = false>
 FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng, int S, float sl2) {
-  constexpr int H = D / DH, NU = 2, UPG = H * NKB;   // units per group: heads x query tiles
+  constexpr int H = D / DH, NU = 2, QT = FIRST_TILE ? 1 : NKB, UPG = H * QT;   // units per group
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g4 = lane >> 4, c16 = lane & 15;
   const int units = ng * UPG;
@@ -138,9 +46,9 @@ FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng
       const int u = min(u0 + x, units - 1);
       live[x] = u0 + x < units;
       const int grp = u / UPG, rem = u % UPG;
-      hcol[x] = (rem / NKB) * DH;
+      hcol[x] = (rem / QT) * DH;
       base[x] = grp * S;
-      q[x] = (rem % NKB) * 16 + c16;
+      q[x] = (rem % QT) * 16 + c16;
       const int qrow = base[x] + (q[x] < S ? q[x] : 0);
 #pragma unroll
       for (int c = 0; c < DH / 32; ++c)
@@ -182,7 +90,7 @@ FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng
           l += e;
           pb[x][kb][j] = (bf16)e;
         }
-      inv[x] = 1.f / rows_sum(l);
+      inv[x] = __builtin_amdgcn_rcpf(rows_sum(l));   // v_rcp_f32
     }
     // LDS element offsets of the value rows this lane feeds into P V (keys past S: row 0, weight 0)
     int vrow[NU][NKB][4];
@@ -219,65 +127,6 @@ FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng
       }
     }
   }
-}
-
-// Xs[r][:] += x_in[row0 + r][:] for valid tile rows (fp32 or bf16 input, 16-byte vectors).
-template <int TM, int D>
-FE_DEV void add_rows(float* Xs, int ldx, const void* Xin, bool xin_f32, long long row0, const int* s_valid) {
-  for (int e = threadIdx.x; e < TM * D / 4; e += WG) {
-    const int rr = e / (D / 4), c = (e % (D / 4)) * 4;
-    if (!s_valid[rr]) continue;
-    float4 x;
-    if (xin_f32) {
-      x = *reinterpret_cast<const float4*>(static_cast<const float*>(Xin) + (row0 + rr) * D + c);
-    } else {
-      const bf16x4 t = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(Xin) + (row0 + rr) * D + c);
-      x = make_float4((float)t[0], (float)t[1], (float)t[2], (float)t[3]);
-    }
-    float* d = &Xs[rr * ldx + c];
-    d[0] += x.x; d[1] += x.y; d[2] += x.z; d[3] += x.w;
-  }
-}
-
-// Xout[row0 + r][:] = Xs[r][:] for valid rows.
-template <int TM, int D>
-FE_DEV void store_rows(const float* Xs, int ldx, float* Xout, long long row0, const int* s_valid) {
-  for (int e = threadIdx.x; e < TM * D / 4; e += WG) {
-    const int rr = e / (D / 4), c = (e % (D / 4)) * 4;
-    if (!s_valid[rr]) continue;
-    *reinterpret_cast<float4*>(Xout + (row0 + rr) * D + c) = *reinterpret_cast<const float4*>(&Xs[rr * ldx + c]);
-  }
-}
-
-// tail shared by both kernels: x1 = Xs (already holds O Wo + bo + x), LN2 -> As, FFN, store
-template <int TM, int D>
-FE_DEV void ffn_tail(Ffn<TM, D>& ffn, float* Xs, int ldx, bf16* As, bf16* Hs, const float* s_g2, const float* s_b2,
-                     const float* b1, const float* b2, float* Xout, long long row0, const int* s_valid) {
-  constexpr int RB = TM / 32, OCB = D / 128;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  stage_rows_lds<TM, D>(Xs, ldx, s_valid, s_g2, s_b2, As);
-  __syncthreads();
-  f32x16 acc_o[RB][OCB];
-  ffn.run(As, Hs, b1, acc_o);
-#pragma unroll
-  for (int j = 0; j < OCB; ++j)
-#pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
-      const int n = (wave + 4 * j) * 32 + qq * 8 + (lane >> 5) * 4;
-      const float4 bb = *reinterpret_cast<const float4*>(&b2[n]);
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        float4* x = reinterpret_cast<float4*>(&Xs[(rb * 32 + (lane & 31)) * ldx + n]);
-        float4 v = *x;
-        v.x += acc_o[rb][j][4 * qq] + bb.x;
-        v.y += acc_o[rb][j][4 * qq + 1] + bb.y;
-        v.z += acc_o[rb][j][4 * qq + 2] + bb.z;
-        v.w += acc_o[rb][j][4 * qq + 3] + bb.w;
-        *x = v;
-      }
-    }
-  __syncthreads();
-  store_rows<TM, D>(Xs, ldx, Xout, row0, s_valid);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -340,14 +189,15 @@ FE_DEV void resid_add(Resid<TM, D>& x, int jj, int rb, const f32x16& acc, const 
   }
 }
 
-// Mean and 1/sqrt(var + eps) of every row of x (this lane's rows rb*32 + lane%32).  Each lane
+// Per row of x (this lane's rows rb*32 + lane%32): rstd = 1/sqrt(var + eps) and nm = -mean*rstd,
+// so the normalised value is x*rstd + nm.  Each lane
 // reduces its 16*D/128 values to a mean and a sum of squared deviations; partial results are
 // merged pairwise with the update of Chan, Golub and LeVeque (equal counts: mean of the means,
 // M2 = M2a + M2b + (ma - mb)^2 n/2), first across the two lanes that share a row
 // (v_permlane32_swap), then across the four waves through s_stat [4][TM].  Contains one barrier;
 // s_stat must not be read by an earlier call any more when a wave arrives here.
 template <int TM, int D>
-FE_DEV void resid_stats(const Resid<TM, D>& x, float2* s_stat, float (&mean)[TM / 32], float (&rstd)[TM / 32]) {
+FE_DEV void resid_stats(const Resid<TM, D>& x, float2* s_stat, float (&nm)[TM / 32], float (&rstd)[TM / 32]) {
   constexpr int RB = TM / 32, BPW = D / 128, NL = 16 * BPW;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -382,26 +232,17 @@ FE_DEV void resid_stats(const Resid<TM, D>& x, float2* s_stat, float (&mean)[TM 
     const float mu = 0.25f * ((p0.x + p1.x) + (p2.x + p3.x));
     const float d0 = p0.x - mu, d1 = p1.x - mu, d2 = p2.x - mu, d3 = p3.x - mu;
     const float m2 = (p0.y + p1.y) + (p2.y + p3.y) + (d0 * d0 + d1 * d1 + d2 * d2 + d3 * d3) * (float)(2 * NL);
-    mean[rb] = mu;
     rstd[rb] = rsqrtf(m2 * (1.f / D) + 1e-5f);
+    nm[rb] = -mu * rstd[rb];
   }
 }
 
-// As (bf16, row stride D + APAD) = LayerNorm(x) with gains g and offsets b (global, [D]).
+// As (bf16, row stride D + APAD) = (x*rstd + nm) * g + b per row (g, b: [D], LDS or global).
 template <int TM, int D>
-FE_DEV void resid_ln_to_lds(const Resid<TM, D>& x, const float* g, const float* b, float2* s_stat, bf16* As) {
+FE_DEV void resid_norm_to_lds(const Resid<TM, D>& x, const float (&nm)[TM / 32], const float (&rstd)[TM / 32],
+                              const float* g, const float* b, bf16* As) {
   constexpr int RB = TM / 32, LDA = D + APAD;
   const int lane = threadIdx.x & 63;
-  float4 gg[D / 128][4], bb[D / 128][4];
-#pragma unroll
-  for (int j = 0; j < D / 128; ++j)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      gg[j][q] = *reinterpret_cast<const float4*>(&g[resid_col(j, q)]);
-      bb[j][q] = *reinterpret_cast<const float4*>(&b[resid_col(j, q)]);
-    }
-  float mean[RB], rstd[RB];
-  resid_stats<TM, D>(x, s_stat, mean, rstd);
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int r = rb * 32 + (lane & 31);
@@ -409,15 +250,67 @@ FE_DEV void resid_ln_to_lds(const Resid<TM, D>& x, const float* g, const float* 
     for (int j = 0; j < D / 128; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
+        const int c = resid_col(j, q);
+        const float4 gg = *reinterpret_cast<const float4*>(&g[c]);
+        const float4 bb = *reinterpret_cast<const float4*>(&b[c]);
         const f32x16& v = x.v[j][rb];
         bf16x4 o;
-        o[0] = (bf16)((v[4 * q] - mean[rb]) * rstd[rb] * gg[j][q].x + bb[j][q].x);
-        o[1] = (bf16)((v[4 * q + 1] - mean[rb]) * rstd[rb] * gg[j][q].y + bb[j][q].y);
-        o[2] = (bf16)((v[4 * q + 2] - mean[rb]) * rstd[rb] * gg[j][q].z + bb[j][q].z);
-        o[3] = (bf16)((v[4 * q + 3] - mean[rb]) * rstd[rb] * gg[j][q].w + bb[j][q].w);
-        *reinterpret_cast<bf16x4*>(&As[r * LDA + resid_col(j, q)]) = o;
+        o[0] = (bf16)(fmaf(fmaf(v[4 * q], rstd[rb], nm[rb]), gg.x, bb.x));
+        o[1] = (bf16)(fmaf(fmaf(v[4 * q + 1], rstd[rb], nm[rb]), gg.y, bb.y));
+        o[2] = (bf16)(fmaf(fmaf(v[4 * q + 2], rstd[rb], nm[rb]), gg.z, bb.z));
+        o[3] = (bf16)(fmaf(fmaf(v[4 * q + 3], rstd[rb], nm[rb]), gg.w, bb.w));
+        *reinterpret_cast<bf16x4*>(&As[r * LDA + c]) = o;
       }
   }
+}
+
+// As = LayerNorm(x) with gains g and offsets b; contains the statistics barrier.
+template <int TM, int D>
+FE_DEV void resid_ln_to_lds(const Resid<TM, D>& x, const float* g, const float* b, float2* s_stat, bf16* As) {
+  float nm[TM / 32], rstd[TM / 32];
+  resid_stats<TM, D>(x, s_stat, nm, rstd);
+  resid_norm_to_lds<TM, D>(x, nm, rstd, g, b, As);
+}
+
+// Per-layer vectors staged in LDS by the module kernel, [ln2g D | ln2b D | bqkv 3D | bo D | b2 D]
+// (fp32), so no epilogue or LayerNorm of the layer waits on a global load.  load() issues this
+// thread's share into registers; store() writes it to LDS once the previous layer no longer
+// reads the block.
+template <int D>
+struct LayerVecs {
+  static constexpr int N4 = 7 * D / 4, PER = (N4 + WG - 1) / WG;
+  static constexpr int G2 = 0, B2N = D, BQKV = 2 * D, BO = 5 * D, BF2 = 6 * D, SIZE = 7 * D;
+  float4 v[PER];
+  FE_DEV void load(const EncW& w) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = i * WG + threadIdx.x, o = 4 * e;
+      if (e >= N4) continue;
+      const float* src = o < D ? w.ln2g + o
+                       : o < 2 * D ? w.ln2b + (o - D)
+                       : o < 5 * D ? w.bqkv + (o - 2 * D)
+                       : o < 6 * D ? w.bo + (o - 5 * D)
+                                   : w.b2 + (o - 6 * D);
+      v[i] = *reinterpret_cast<const float4*>(src);
+    }
+  }
+  FE_DEV void store(float* s) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = i * WG + threadIdx.x;
+      if (e < N4) reinterpret_cast<float4*>(s)[e] = v[i];
+    }
+  }
+};
+
+// LN1 gains and offsets of one layer, [g D | b D], one float4 on each of the first D/2 threads.
+FE_DEV float4 ln1_load(const EncW& w, int D) {
+  const int o = 4 * threadIdx.x;
+  if (o >= 2 * D) return make_float4(0.f, 0.f, 0.f, 0.f);
+  return *reinterpret_cast<const float4*>(o < D ? w.ln1g + o : w.ln1b + (o - D));
+}
+FE_DEV void ln1_store(float* s, float4 v, int D) {
+  if (4 * (int)threadIdx.x < 2 * D) reinterpret_cast<float4*>(s)[threadIdx.x] = v;
 }
 
 // x += W2 ReLU(As W1 + b1) + b2 for the tile in As (LN2 output), hidden width F in chunks of
@@ -529,13 +422,15 @@ struct ModuleSmem {
 // n_layers encoder blocks and the final LayerNorm over a tile of whole groups; one launch per
 // module.  Per block: LN1 -> As; q|k|v -> LDS; attention per (group, head) -> As; x += O Wo + bo;
 // LN2 -> As; x += FFN.  The fp32 residual x never leaves registers; the result leaves as fp32.
-template <int TM, int D, int DH, int NKB>
+template <int TM, int D, int DH, int NKB, bool CLS>
 __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
   using L = ModuleSmem<TM, D>;
   constexpr int RB = TM / 32, OCB = D / 128;
   __shared__ __attribute__((aligned(16))) bf16 As[TM * L::LDA];
   __shared__ __attribute__((aligned(16))) char big[L::BIG];
   __shared__ __attribute__((aligned(16))) float2 s_stat[4 * TM];
+  __shared__ __attribute__((aligned(16))) float s_vec[LayerVecs<D>::SIZE];
+  __shared__ __attribute__((aligned(16))) float s_ln1[2][2 * D];
   __shared__ int s_valid[TM];
   bf16* QKVs = reinterpret_cast<bf16*>(big);
   bf16* Hs = reinterpret_cast<bf16*>(big);
@@ -546,19 +441,36 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
   const long long row0 = (long long)g0 * a.S;
   const int nrows = ng * a.S;
 
+  LayerVecs<D> vecs;
+  vecs.load(a.layer[0]);
+  float4 ln1v = ln1_load(a.layer[0], D);
   ColGemm<TM, D, 3 * D / 32> gq;
   gq.start(a.layer[0].wqkv);
   if (!mark_rows<TM>(0, nrows, nullptr, 1, s_valid)) return;
   Resid<TM, D> x;
   resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
+  vecs.store(s_vec);
+  ln1_store(s_ln1[0], ln1v, D);
 
-  for (int l = 0; l < a.n_layers; ++l) {
+  using V = LayerVecs<D>;
+  const int nfull = CLS ? a.n_layers - 1 : a.n_layers;
+  for (int l = 0; l < nfull; ++l) {
     const EncW& w = a.layer[l];
     if (l > 0) gq.start(w.wqkv);
-    // LN1 -> As (the barrier inside the statistics also retires every earlier reader of As)
-    resid_ln_to_lds<TM, D>(x, w.ln1g, w.ln1b, s_stat, As);
+    if (l + 1 < a.n_layers) ln1v = ln1_load(a.layer[l + 1], D);
+    // LN1 -> As.  The statistics barrier retires every reader of As and of the vector block
+    // from the previous layer, so this layer's vectors (loaded at its end) are stored now.
+    {
+      float nm[RB], rstd[RB];
+      resid_stats<TM, D>(x, s_stat, nm, rstd);
+      if (l > 0) vecs.store(s_vec);
+      const float* g1 = s_ln1[l & 1];
+      resid_norm_to_lds<TM, D>(x, nm, rstd, g1, g1 + D, As);
+    }
     __syncthreads();
-    gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) { block_to_lds_bf16(acc, cb, rb, w.bqkv, QKVs, L::LDQ); });
+    gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) {
+      block_to_lds_bf16(acc, cb, rb, s_vec + V::BQKV, QKVs, L::LDQ);
+    });
     ColGemm<TM, D, D / 32> go;
     go.start(w.wo);
     __syncthreads();
@@ -566,14 +478,118 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
     FfnStream<TM, D> ffn;
     ffn.start(w.w1, w.w2, a.F);
     __syncthreads();
-    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, w.bo); });
-    resid_ln_to_lds<TM, D>(x, w.ln2g, w.ln2b, s_stat, As);
+    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, s_vec + V::BO); });
+    resid_ln_to_lds<TM, D>(x, s_vec + V::G2, s_vec + V::B2N, s_stat, As);
     __syncthreads();
     ffn.run(As, Hs, w.b1, x);
 #pragma unroll
     for (int j = 0; j < OCB; ++j)
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, w.b2);
+      for (int rb = 0; rb < RB; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, s_vec + V::BF2);
+    if (l + 1 < a.n_layers) {
+      ln1_store(s_ln1[(l + 1) & 1], ln1v, D);   // that buffer was last read by LN1 of layer l - 1
+      vecs.load(a.layer[l + 1]);
+    }
+  }
+
+  if constexpr (CLS) {
+    // Last block when only each group's first row is wanted (the [CLS] rows of the sequence
+    // encoder): keys and values still come from every row, but the attention runs for the first
+    // query tile of each group only, and the output projection, LN2, FFN and the final LayerNorm
+    // run on the first rows alone, compacted into one 32-row block.
+    constexpr int LDC = D + 4;
+    const int last = a.n_layers - 1;
+    const EncW& w = a.layer[last];
+    if (last > 0) gq.start(w.wqkv);
+    {
+      float nm[RB], rstd[RB];
+      resid_stats<TM, D>(x, s_stat, nm, rstd);
+      if (last > 0) vecs.store(s_vec);
+      const float* g1 = s_ln1[last & 1];
+      resid_norm_to_lds<TM, D>(x, nm, rstd, g1, g1 + D, As);
+    }
+    __syncthreads();
+    gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) {
+      block_to_lds_bf16(acc, cb, rb, s_vec + V::BQKV, QKVs, L::LDQ);
+    });
+    ColGemm<32, D, D / 32> go;
+    go.start(w.wo);
+    __syncthreads();
+    group_attention<D, DH, NKB, true>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
+    __syncthreads();
+    // compaction: attention rows g*S of As -> Ac row g (bf16), residual rows g*S -> Xc row g
+    bf16* Ac = reinterpret_cast<bf16*>(big);
+    float* Xc = reinterpret_cast<float*>(big + 32 * L::LDA * 2);
+    for (int e = threadIdx.x; e < 32 * D / 8; e += WG) {
+      const int r = e / (D / 8), c = (e % (D / 8)) * 8;
+      const bf16x8 v = r < ng ? *reinterpret_cast<const bf16x8*>(&As[r * a.S * L::LDA + c]) : bf16x8{};
+      *reinterpret_cast<bf16x8*>(&Ac[r * L::LDA + c]) = v;
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int r = rb * 32 + (lane & 31);
+      if (!s_valid[r] || r % a.S) continue;
+      float* dst = Xc + (r / a.S) * LDC;
+#pragma unroll
+      for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x16& v = x.v[j][rb];
+          *reinterpret_cast<float4*>(&dst[resid_col(j, q)]) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+        }
+    }
+    __syncthreads();
+    Resid<32, D> xc;
+    {
+      const int r = lane & 31;
+#pragma unroll
+      for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 t = r < ng ? *reinterpret_cast<const float4*>(&Xc[r * LDC + resid_col(j, q)]) : make_float4(0.f, 0.f, 0.f, 0.f);
+          xc.v[j][0][4 * q] = t.x;
+          xc.v[j][0][4 * q + 1] = t.y;
+          xc.v[j][0][4 * q + 2] = t.z;
+          xc.v[j][0][4 * q + 3] = t.w;
+        }
+    }
+    FfnStream<32, D> ffn;
+    ffn.start(w.w1, w.w2, a.F);
+    go.run(Ac, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<32, D>(xc, jj, rb, acc, s_vec + V::BO); });
+    // LN2 of the compact rows -> As rows 0..31; its statistics barrier retires the reads of Ac,
+    // so the FFN's hidden buffers may reuse the compaction area
+    resid_ln_to_lds<32, D>(xc, s_vec + V::G2, s_vec + V::B2N, s_stat, As);
+    __syncthreads();
+    ffn.run(As, Hs, w.b1, xc);
+#pragma unroll
+    for (int j = 0; j < OCB; ++j) resid_add<32, D>(xc, j, 0, f32x16{}, s_vec + V::BF2);
+    float4 gg[D / 128][4], bb[D / 128][4];
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        gg[j][q] = *reinterpret_cast<const float4*>(&a.lnfg[resid_col(j, q)]);
+        bb[j][q] = *reinterpret_cast<const float4*>(&a.lnfb[resid_col(j, q)]);
+      }
+    float nm[1], rstd[1];
+    resid_stats<32, D>(xc, s_stat, nm, rstd);
+    const int r = lane & 31;
+    if (r < ng) {
+      float* y = a.Y + (long long)(g0 + r) * D;
+#pragma unroll
+      for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x16& v = xc.v[j][0];
+          const int rb = 0;
+          *reinterpret_cast<float4*>(&y[resid_col(j, q)]) =
+              make_float4(fmaf(fmaf(v[4 * q], rstd[rb], nm[rb]), gg[j][q].x, bb[j][q].x),
+                          fmaf(fmaf(v[4 * q + 1], rstd[rb], nm[rb]), gg[j][q].y, bb[j][q].y),
+                          fmaf(fmaf(v[4 * q + 2], rstd[rb], nm[rb]), gg[j][q].z, bb[j][q].z),
+                          fmaf(fmaf(v[4 * q + 3], rstd[rb], nm[rb]), gg[j][q].w, bb[j][q].w));
+        }
+    }
+    return;
   }
 
   // final LayerNorm, fp32 out: every valid row, or the first row of each group
@@ -585,8 +601,8 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
       gg[j][q] = *reinterpret_cast<const float4*>(&a.lnfg[resid_col(j, q)]);
       bb[j][q] = *reinterpret_cast<const float4*>(&a.lnfb[resid_col(j, q)]);
     }
-  float mean[RB], rstd[RB];
-  resid_stats<TM, D>(x, s_stat, mean, rstd);
+  float nm[RB], rstd[RB];
+  resid_stats<TM, D>(x, s_stat, nm, rstd);
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int r = rb * 32 + (lane & 31);
@@ -605,10 +621,10 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
       for (int q = 0; q < 4; ++q) {
         const f32x16& v = x.v[j][rb];
         *reinterpret_cast<float4*>(&y[resid_col(j, q)]) =
-            make_float4((v[4 * q] - mean[rb]) * rstd[rb] * gg[j][q].x + bb[j][q].x,
-                        (v[4 * q + 1] - mean[rb]) * rstd[rb] * gg[j][q].y + bb[j][q].y,
-                        (v[4 * q + 2] - mean[rb]) * rstd[rb] * gg[j][q].z + bb[j][q].z,
-                        (v[4 * q + 3] - mean[rb]) * rstd[rb] * gg[j][q].w + bb[j][q].w);
+            make_float4(fmaf(fmaf(v[4 * q], rstd[rb], nm[rb]), gg[j][q].x, bb[j][q].x),
+                        fmaf(fmaf(v[4 * q + 1], rstd[rb], nm[rb]), gg[j][q].y, bb[j][q].y),
+                        fmaf(fmaf(v[4 * q + 2], rstd[rb], nm[rb]), gg[j][q].z, bb[j][q].z),
+                        fmaf(fmaf(v[4 * q + 3], rstd[rb], nm[rb]), gg[j][q].w, bb[j][q].w));
       }
   }
 }
@@ -686,8 +702,8 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
     if (a.Xout) resid_store<TM, D>(x, a.Xout, row0, s_valid);
     if (a.Hout) {
       // final LayerNorm of the module into bf16 H; padding rows of the tile become zeros
-      float mean[TM / 32], rstd[TM / 32];
-      resid_stats<TM, D>(x, s_stat, mean, rstd);
+      float nm[TM / 32], rstd[TM / 32];
+      resid_stats<TM, D>(x, s_stat, nm, rstd);
       bf16* H = static_cast<bf16*>(a.Hout);
 #pragma unroll
       for (int rb = 0; rb < TM / 32; ++rb) {
@@ -702,10 +718,10 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
             const float4 bb = *reinterpret_cast<const float4*>(&a.lnfb[c]);
             const f32x16& v = x.v[j][rb];
             bf16x4 o;
-            o[0] = (bf16)((v[4 * q] - mean[rb]) * rstd[rb] * gg.x + bb.x);
-            o[1] = (bf16)((v[4 * q + 1] - mean[rb]) * rstd[rb] * gg.y + bb.y);
-            o[2] = (bf16)((v[4 * q + 2] - mean[rb]) * rstd[rb] * gg.z + bb.z);
-            o[3] = (bf16)((v[4 * q + 3] - mean[rb]) * rstd[rb] * gg.w + bb.w);
+            o[0] = (bf16)(fmaf(fmaf(v[4 * q], rstd[rb], nm[rb]), gg.x, bb.x));
+            o[1] = (bf16)(fmaf(fmaf(v[4 * q + 1], rstd[rb], nm[rb]), gg.y, bb.y));
+            o[2] = (bf16)(fmaf(fmaf(v[4 * q + 2], rstd[rb], nm[rb]), gg.z, bb.z));
+            o[3] = (bf16)(fmaf(fmaf(v[4 * q + 3], rstd[rb], nm[rb]), gg.w, bb.w));
             *reinterpret_cast<bf16x4*>(H + ((long long)row0 + r) * D + c) = o;
           }
       }
@@ -721,17 +737,27 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   }
 }
 
-template <int TM, int D, int DH>
-hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
+template <int TM, int D, int DH, bool CLS>
+hipError_t launch_module_c(const ModuleArgs& a, hipStream_t s) {
   const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
   switch ((a.S + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// first-row-only modules on 64-row tiles take the compacted last block (a 32-row tile would
+// gain nothing from compaction)
+template <int TM, int D, int DH>
+hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
+  if constexpr (TM == 64) {
+    if (a.first_row_only) return launch_module_c<TM, D, DH, true>(a, s);
+  }
+  return launch_module_c<TM, D, DH, false>(a, s);
 }
 
 template <int TM, int D>
