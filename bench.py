@@ -30,37 +30,43 @@ PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 
 
-def algorithmic_work(c, U):
-    """Per-step algorithmic flops per kernel family and bytes of the assembly, from the shapes.
-
-    U is the list of distinct-item counts of the B requests.  Projection flops ("gemm"): an
-    encoder block over R rows costs 8 R d^2 (q|k|v 6, output 2), an item block 12 U d^2 (plus
-    the cross-attention query and output projections), the key/value cache 4 n T d^2.  FFN
-    flops ("ffn"): 4 R d F per block.  Attention flops: 4 nq nk d per block (QK^T and PV).
-    """
-    d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
-    rows_enc = B * T + B * K * S + B * K            # context, sequence and cross blocks
-    rows_item = sum(U)
-    proj = n * 8.0 * d * d * rows_enc + n * 12.0 * d * d * rows_item + 4.0 * n * B * T * d * d
-    ffn = n * 4.0 * d * F * (rows_enc + rows_item)
-    attn = 4.0 * n * B * T * T * d
-    attn += sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U)
-    attn += 4.0 * n * B * K * S * S * d
-    attn += 4.0 * n * B * K * K * d
+def assemble_bytes(c, U):
+    """Algorithmic HBM bytes of the assembly: write every [CLS; items] row once, read each
+    distinct encoding once, read the slot indices."""
+    d, B, K, S = c.d, c.B, c.K, c.L + 1
     esz = 2 if c.dtype == "bf16" else 4
-    asm_bytes = B * K * S * d * esz + sum(U) * d * esz + B * K * c.L * 4
-    return {"gemm": proj, "ffn": ffn, "attention": attn}, asm_bytes
+    return B * K * S * d * esz + sum(U) * d * esz + B * K * c.L * 4
+
+
+def module_parts(d, F, n, rows, groups, S, first_row_only=False):
+    """Algorithmic flops of an encoder module of n pre-LN blocks over `groups` groups of S rows,
+    split into (q|k|v projections, attention, output projection + FFN).
+
+    Per row and block: q|k|v 6 d^2, output projection 2 d^2, FFN 4 d F; per group and block:
+    attention 4 S^2 d (Q K^T and P V).  When only the first row of each group leaves the module
+    (the [CLS] rows of the sequence encoder), the last block needs keys and values of every row
+    but the query, the attention, the output projection and the FFN of the first rows alone.
+    """
+    proj = n * 6.0 * d * d * rows
+    attn = n * 4.0 * S * S * d * groups
+    tail = n * (2.0 * d * d + 4.0 * d * F) * rows
+    if first_row_only:
+        proj -= 2.0 * d * d * (rows - groups)
+        attn -= 4.0 * S * d * (S - 1) * groups
+        tail -= (2.0 * d * d + 4.0 * d * F) * (rows - groups)
+    return proj, attn, tail
 
 
 def family_flops(c, U, fam_names):
-    """Split the algorithmic flops over the kernel families that ran.
+    """Split the algorithmic flops of one pass over the kernel families that ran.
 
-    Fused kernels take the work of the stages they contain: "layer" (whole blocks of short
-    groups: the sequence encoder and, when its groups are short, the cross-sequence module),
-    "post" (output projection and FFN / query projection of long-group blocks).
+    Fused kernels take the work of the stages they contain: "layer" (a whole module of short
+    groups in one kernel: the sequence encoder, and the cross-sequence and context modules when
+    their groups are short), "post" (output projection and FFN, or query projection, after a
+    separate attention kernel), "gemm" (q|k|v projections and the key/value cache).
     """
     d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
-    tile = 32 if d >= 512 else 64
+    tile = 0 if d >= 512 else 64          # module kernel: groups of up to 64 rows, d <= 256
     rows_item = sum(U)
     out = {k: 0.0 for k in fam_names}
 
@@ -68,29 +74,22 @@ def family_flops(c, U, fam_names):
         out[fam] = out.get(fam, 0.0) + v
 
     fused = "layer" in fam_names or "post" in fam_names
-    # context: QKV projection + attention + tail; key/value cache projection
-    for mod_rows, group, attn in ((B * T, T, 4.0 * n * B * T * T * d), (B * K * S, S, 4.0 * n * B * K * S * S * d),
-                                  (B * K, K, 4.0 * n * B * K * K * d)):
-        if fused and group <= tile:
-            add("layer", n * (8.0 * d * d + 4.0 * d * F) * mod_rows + attn)
+    for rows, groups, size, first in ((B * T, B, T, False), (B * K * S, B * K, S, True), (B * K, B, K, False)):
+        proj, attn, tail = module_parts(d, F, n, rows, groups, size, first)
+        if fused and size <= tile:
+            add("layer", proj + attn + tail)
         elif fused:
-            add("gemm", n * 6.0 * d * d * mod_rows)
+            add("gemm", proj)
             add("attention", attn)
-            add("post", n * (2.0 * d * d + 4.0 * d * F) * mod_rows)
+            add("post", tail)
         else:
-            add("gemm", n * 8.0 * d * d * mod_rows)
+            add("gemm", proj + tail)
             add("attention", attn)
-            add("ffn" if "ffn" in fam_names else "gemm", n * 4.0 * d * F * mod_rows)
-    add("gemm", 4.0 * n * B * T * d * d)
-    # distinct items: QKV, self-attention, O + query projection, cross-attention, O2 + FFN
-    item_attn = sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U)
-    add("attention", item_attn)
-    if fused:
-        add("gemm", n * 6.0 * d * d * rows_item)
-        add("post", n * (6.0 * d * d + 4.0 * d * F) * rows_item)
-    else:
-        add("gemm", n * 12.0 * d * d * rows_item)
-        add("ffn" if "ffn" in fam_names else "gemm", n * 4.0 * d * F * rows_item)
+    add("gemm", 4.0 * n * B * T * d * d)                      # key/value cache of the item layers
+    # distinct items: q|k|v, self-attention, output + query projections, cross-attention, FFN
+    add("attention", sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U))
+    add("gemm", n * 6.0 * d * d * rows_item)
+    add("post" if fused else "gemm", n * (6.0 * d * d + 4.0 * d * F) * rows_item)
     return out
 
 
@@ -252,7 +251,7 @@ def main() -> int:
     lists_per_s = c.B * c.K / (ms_per_step / 1e3)
 
     U = bufs["n_uniq"].cpu().numpy().tolist()
-    flops, asm_bytes = algorithmic_work(c, U)
+    asm_bytes = assemble_bytes(c, U)
 
     # ---- kernel-timing region: the same steps with HIP events around every launch
     fam = {}

@@ -45,6 +45,13 @@ FE_DEV int xcd_tile(int i, int n) {
   return x * q + min(x, r) + y;
 }
 
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations, then s_barrier.
+// Unlike __syncthreads() it does not wait for outstanding vector-memory operations, so a load
+// (or an LDS DMA) issued earlier stays in flight across it; data an LDS DMA writes becomes
+// visible to other waves only after the issuing wave's vmem_wait() and a following barrier.
+FE_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+FE_DEV void vmem_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 FE_DEV float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

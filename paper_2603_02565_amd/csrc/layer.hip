@@ -224,7 +224,7 @@ FE_DEV void resid_stats(const Resid<TM, D>& x, float2* s_stat, float (&nm)[TM / 
     const float qw = __uint_as_float(pq[0]) + __uint_as_float(pq[1]) + dm * dm * (0.5f * NL);
     if (lane < 32) s_stat[wave * TM + rb * 32 + lane] = make_float2(mw, qw);
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int r = rb * 32 + (lane & 31);
@@ -272,45 +272,34 @@ FE_DEV void resid_ln_to_lds(const Resid<TM, D>& x, const float* g, const float* 
   resid_norm_to_lds<TM, D>(x, nm, rstd, g, b, As);
 }
 
-// Per-layer vectors staged in LDS by the module kernel, [ln2g D | ln2b D | bqkv 3D | bo D | b2 D]
-// (fp32), so no epilogue or LayerNorm of the layer waits on a global load.  load() issues this
-// thread's share into registers; store() writes it to LDS once the previous layer no longer
-// reads the block.
+// The vectors of one encoder block as the module kernel keeps them in LDS (fp32):
+// [ln1g | ln1b | ln2g | ln2b | bqkv (3D) | bo | b2], 9D floats.
 template <int D>
-struct LayerVecs {
-  static constexpr int N4 = 7 * D / 4, PER = (N4 + WG - 1) / WG;
-  static constexpr int G2 = 0, B2N = D, BQKV = 2 * D, BO = 5 * D, BF2 = 6 * D, SIZE = 7 * D;
-  float4 v[PER];
-  FE_DEV void load(const EncW& w) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int e = i * WG + threadIdx.x, o = 4 * e;
-      if (e >= N4) continue;
-      const float* src = o < D ? w.ln2g + o
-                       : o < 2 * D ? w.ln2b + (o - D)
-                       : o < 5 * D ? w.bqkv + (o - 2 * D)
-                       : o < 6 * D ? w.bo + (o - 5 * D)
-                                   : w.b2 + (o - 6 * D);
-      v[i] = *reinterpret_cast<const float4*>(src);
-    }
-  }
-  FE_DEV void store(float* s) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int e = i * WG + threadIdx.x;
-      if (e < N4) reinterpret_cast<float4*>(s)[e] = v[i];
-    }
-  }
+struct Vecs {
+  static constexpr int G1 = 0, B1 = D, G2 = 2 * D, B2 = 3 * D, QKV = 4 * D, O = 7 * D, F2 = 8 * D, SIZE = 9 * D;
 };
 
-// LN1 gains and offsets of one layer, [g D | b D], one float4 on each of the first D/2 threads.
-FE_DEV float4 ln1_load(const EncW& w, int D) {
-  const int o = 4 * threadIdx.x;
-  if (o >= 2 * D) return make_float4(0.f, 0.f, 0.f, 0.f);
-  return *reinterpret_cast<const float4*>(o < D ? w.ln1g + o : w.ln1b + (o - D));
-}
-FE_DEV void ln1_store(float* s, float4 v, int D) {
-  if (4 * (int)threadIdx.x < 2 * D) reinterpret_cast<float4*>(s)[threadIdx.x] = v;
+// Copy one block's vectors from global memory straight into the LDS block dst with
+// global_load_lds (16 bytes per lane, no registers): wave w moves the 1 KiB chunks w, w + 4, ....
+// The data is visible to other waves once each issuing wave has passed vmem_wait() and then a
+// barrier; until then dst must not be read, and it must not be written while still being read.
+template <int D>
+FE_DEV void vecs_dma(const EncW& w, float* dst) {
+  using V = Vecs<D>;
+  constexpr int NCHK = (V::SIZE * 4 + 1023) / 1024;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int ch = wave; ch < NCHK; ch += 4) {
+    const int o = ch * 256 + lane * 4;              // this lane's first float
+    if (o >= V::SIZE) continue;
+    const float* src = o < V::B1    ? w.ln1g + o
+                     : o < V::G2    ? w.ln1b + (o - V::B1)
+                     : o < V::B2    ? w.ln2g + (o - V::G2)
+                     : o < V::QKV   ? w.ln2b + (o - V::B2)
+                     : o < V::O     ? w.bqkv + (o - V::QKV)
+                     : o < V::F2    ? w.bo + (o - V::O)
+                                    : w.b2 + (o - V::F2);
+    __builtin_amdgcn_global_load_lds(src, dst + ch * 256, 16, 0, 0);
+  }
 }
 
 // x += W2 ReLU(As W1 + b1) + b2 for the tile in As (LN2 output), hidden width F in chunks of
@@ -318,29 +307,43 @@ FE_DEV void ln1_store(float* s, float4 v, int D) {
 // down-projection's output blocks).  Wave w computes hidden columns 32w..32w+31 of a chunk and
 // output blocks w + 4j.  The weight fragments of a chunk form one stream -- the KS k-steps of
 // W1 column block 4c + w, then for every output block j the 8 k-steps 8c.. of W2 column block
-// w + 4j -- consumed in stages of 8 fragments through a two-stage register buffer, each stage
-// requested one stage ahead (2*KS/8 stages per chunk, an even count, so buffer parities are
-// compile-time).  Hidden chunks alternate between two LDS buffers in Hs (2 x TM x HLD): chunk
-// c is written to buffer c&1 and one barrier per chunk separates its writers from its readers;
-// buffer c&1 is rewritten (chunk c+2) only after every wave passed the barrier of chunk c+1,
-// i.e. finished reading chunk c.  The caller orders the first writes to Hs after its earlier
-// readers and the next writes to As or Hs after this call.
-template <int TM, int D>
+// w + 4j -- consumed in stages of 8 fragments (NS = 2*KS/8 per chunk, an even count) through a
+// ring of DEPTH register stages, each stage requested DEPTH - 1 stages ahead.  With NCH = 0 the
+// chunk count F/HC is a runtime value and DEPTH is 2 (ring slot = stage parity); with NCH > 0
+// the F = 128*NCH chunks are unrolled, so every ring slot is a compile-time index for any DEPTH.
+// Hidden chunks alternate between two LDS buffers in Hs (2 x TM x HLD): chunk c is written to
+// buffer c&1 and one barrier per chunk separates its writers from its readers; buffer c&1 is
+// rewritten (chunk c+2) only after every wave passed the barrier of chunk c+1, i.e. finished
+// reading chunk c.  The caller orders the first writes to Hs after its earlier readers and the
+// next writes to As or Hs after this call.
+template <int TM, int D, int NCH = 0, int DEPTH = 2>
 struct FfnStream {
   static constexpr int RB = TM / 32, KS = D / 16, OCB = D / 128;
   static constexpr int S1 = KS / 8, NS = S1 + OCB;         // W1 stages, stages per chunk
   static_assert(KS % 8 == 0 && NS % 2 == 0, "unsupported width");
-  bf16x8 buf[2][8];
+  static_assert(NCH > 0 || DEPTH == 2, "a runtime chunk count needs the two-stage ring");
+  bf16x8 buf[DEPTH][8];
   const bf16x8 *W1l, *W2l;
   int F;
-  FE_DEV void load(int c, int t) {      // stage t (compile-time) of chunk c into buf[t & 1]
+  static constexpr int slot(int c, int t) { return NCH ? (c * NS + t) % DEPTH : t % 2; }
+  FE_DEV void load(int c, int t) {      // stage t of chunk c into its ring slot (compile-time t, slot)
     if (t < S1) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) buf[t & 1][k] = W1l[((long long)c * 4 * KS + t * 8 + k) * 64];
+      for (int k = 0; k < 8; ++k) buf[slot(c, t)][k] = W1l[((long long)c * 4 * KS + t * 8 + k) * 64];
     } else {
       const int j = t - S1;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) buf[t & 1][k] = W2l[((long long)4 * j * (F / 16) + c * 8 + k) * 64];
+      for (int k = 0; k < 8; ++k) buf[slot(c, t)][k] = W2l[((long long)4 * j * (F / 16) + c * 8 + k) * 64];
+    }
+  }
+  // request the stage DEPTH - 1 positions after stage t of chunk c, if there is one
+  FE_DEV void prefetch(int c, int t, int nchunks) {
+    if constexpr (NCH == 0) {
+      if (t + 1 < NS) load(c, t + 1);
+      else if (c + 1 < nchunks) load(c + 1, 0);
+    } else {
+      const int g = c * NS + t + DEPTH - 1;
+      if (g < NCH * NS) load(g / NS, g % NS);
     }
   }
   FE_DEV void start(const void* w1p, const void* w2p, int f) {
@@ -348,65 +351,75 @@ struct FfnStream {
     F = f;
     W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
     W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (f / 16) * 64 + lane;
-    load(0, 0);
+#pragma unroll
+    for (int g = 0; g < DEPTH - 1; ++g) load(g / NS, g % NS);
   }
   template <class Acc>
   FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x) {
-    constexpr int LD = D + APAD;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nchunks = F / HC;
-    for (int c = 0; c < nchunks; ++c) {
-      bf16* Hc = Hs + (c & 1) * TM * HLD;
-      float4 bias1[4];
+    if constexpr (NCH > 0) {
 #pragma unroll
-      for (int qq = 0; qq < 4; ++qq)
-        bias1[qq] = *reinterpret_cast<const float4*>(&b1[(c * 4 + wave) * 32 + qq * 8 + (lane >> 5) * 4]);
-      f32x16 acc_h[RB];
+      for (int c = 0; c < NCH; ++c) chunk(c, NCH, As, Hs, b1, x, lane, wave);
+    } else {
+      const int nchunks = F / HC;
+      for (int c = 0; c < nchunks; ++c) chunk(c, nchunks, As, Hs, b1, x, lane, wave);
+    }
+  }
+  template <class Acc>
+  FE_DEV void chunk(int c, int nchunks, const bf16* As, bf16* Hs, const float* b1, Acc& x, int lane, int wave) {
+    constexpr int LD = D + APAD;
+    bf16* Hc = Hs + (c & 1) * TM * HLD;
+    float4 bias1[4];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) acc_h[rb] = f32x16{};
+    for (int qq = 0; qq < 4; ++qq)
+      bias1[qq] = *reinterpret_cast<const float4*>(&b1[(c * 4 + wave) * 32 + qq * 8 + (lane >> 5) * 4]);
+    f32x16 acc_h[RB];
 #pragma unroll
-      for (int t = 0; t < S1; ++t) {
-        load(c, t + 1);                  // t + 1 <= S1 < NS: still this chunk
+    for (int rb = 0; rb < RB; ++rb) acc_h[rb] = f32x16{};
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          bf16x8 af[4][RB];
+    for (int t = 0; t < S1; ++t) {
+      prefetch(c, t, nchunks);
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
+      for (int h = 0; h < 2; ++h) {
+        bf16x8 af[4][RB];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(As, LD, rb * 32, (t * 8 + h * 4 + k) * 16, lane);
+        for (int k = 0; k < 4; ++k)
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
+          for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(As, LD, rb * 32, (t * 8 + h * 4 + k) * 16, lane);
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-              acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][h * 4 + k], af[k][rb], acc_h[rb], 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const float* bb = reinterpret_cast<const float*>(&bias1[qq]);
-          bf16x4 hv;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) hv[e] = (bf16)fmaxf(acc_h[rb][4 * qq + e] + bb[e], 0.f);
-          *reinterpret_cast<bf16x4*>(&Hc[(rb * 32 + (lane & 31)) * HLD + wave * 32 + qq * 8 + (lane >> 5) * 4]) = hv;
-        }
-      __syncthreads();
-      bf16x8 af[8][RB];
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(Hc, HLD, rb * 32, k * 16, lane);
-#pragma unroll
-      for (int j = 0; j < OCB; ++j) {
-        const int t = S1 + j;
-        if (t + 1 < NS) load(c, t + 1);
-        else if (c + 1 < nchunks) load(c + 1, 0);
-#pragma unroll
-        for (int k = 0; k < 8; ++k)
+        for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            x.v[j][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][k], af[k][rb], x.v[j][rb], 0, 0, 0);
+            acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot(c, t)][h * 4 + k], af[k][rb], acc_h[rb], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        const float* bb = reinterpret_cast<const float*>(&bias1[qq]);
+        bf16x4 hv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) hv[e] = (bf16)fmaxf(acc_h[rb][4 * qq + e] + bb[e], 0.f);
+        *reinterpret_cast<bf16x4*>(&Hc[(rb * 32 + (lane & 31)) * HLD + wave * 32 + qq * 8 + (lane >> 5) * 4]) = hv;
+      }
+    lds_barrier();
+#pragma unroll
+    for (int j = 0; j < OCB; ++j) {
+      const int t = S1 + j;
+      prefetch(c, t, nchunks);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        bf16x8 af[4][RB];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(Hc, HLD, rb * 32, (h * 4 + k) * 16, lane);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            x.v[j][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot(c, t)][h * 4 + k], af[k][rb], x.v[j][rb], 0, 0, 0);
       }
     }
   }
@@ -429,8 +442,7 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 As[TM * L::LDA];
   __shared__ __attribute__((aligned(16))) char big[L::BIG];
   __shared__ __attribute__((aligned(16))) float2 s_stat[4 * TM];
-  __shared__ __attribute__((aligned(16))) float s_vec[LayerVecs<D>::SIZE];
-  __shared__ __attribute__((aligned(16))) float s_ln1[2][2 * D];
+  __shared__ __attribute__((aligned(16))) float s_vec[2][Vecs<D>::SIZE];   // by layer parity
   __shared__ int s_valid[TM];
   bf16* QKVs = reinterpret_cast<bf16*>(big);
   bf16* Hs = reinterpret_cast<bf16*>(big);
@@ -441,55 +453,49 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
   const long long row0 = (long long)g0 * a.S;
   const int nrows = ng * a.S;
 
-  LayerVecs<D> vecs;
-  vecs.load(a.layer[0]);
-  float4 ln1v = ln1_load(a.layer[0], D);
+  // layer 0's vectors: DMA into LDS, published by the statistics barrier of the first LN1
+  vecs_dma<D>(a.layer[0], s_vec[0]);
   ColGemm<TM, D, 3 * D / 32> gq;
   gq.start(a.layer[0].wqkv);
   if (!mark_rows<TM>(0, nrows, nullptr, 1, s_valid)) return;
   Resid<TM, D> x;
   resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
-  vecs.store(s_vec);
-  ln1_store(s_ln1[0], ln1v, D);
+  vmem_wait();
 
-  using V = LayerVecs<D>;
+  using V = Vecs<D>;
   const int nfull = CLS ? a.n_layers - 1 : a.n_layers;
   for (int l = 0; l < nfull; ++l) {
     const EncW& w = a.layer[l];
+    const float* vec = s_vec[l & 1];
     if (l > 0) gq.start(w.wqkv);
-    if (l + 1 < a.n_layers) ln1v = ln1_load(a.layer[l + 1], D);
-    // LN1 -> As.  The statistics barrier retires every reader of As and of the vector block
-    // from the previous layer, so this layer's vectors (loaded at its end) are stored now.
+    // LN1 -> As.  Past the statistics barrier every wave has left layer l - 1, so the other
+    // vector buffer is free for layer l + 1 (waited for at the end of this layer).
     {
       float nm[RB], rstd[RB];
       resid_stats<TM, D>(x, s_stat, nm, rstd);
-      if (l > 0) vecs.store(s_vec);
-      const float* g1 = s_ln1[l & 1];
-      resid_norm_to_lds<TM, D>(x, nm, rstd, g1, g1 + D, As);
+      if (l + 1 < a.n_layers) vecs_dma<D>(a.layer[l + 1], s_vec[(l + 1) & 1]);
+      resid_norm_to_lds<TM, D>(x, nm, rstd, vec + V::G1, vec + V::B1, As);
     }
-    __syncthreads();
+    lds_barrier();
     gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) {
-      block_to_lds_bf16(acc, cb, rb, s_vec + V::BQKV, QKVs, L::LDQ);
+      block_to_lds_bf16(acc, cb, rb, vec + V::QKV, QKVs, L::LDQ);
     });
     ColGemm<TM, D, D / 32> go;
     go.start(w.wo);
-    __syncthreads();
+    lds_barrier();
     group_attention<D, DH, NKB>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
     FfnStream<TM, D> ffn;
     ffn.start(w.w1, w.w2, a.F);
-    __syncthreads();
-    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, s_vec + V::BO); });
-    resid_ln_to_lds<TM, D>(x, s_vec + V::G2, s_vec + V::B2N, s_stat, As);
-    __syncthreads();
+    lds_barrier();
+    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, vec + V::O); });
+    resid_ln_to_lds<TM, D>(x, vec + V::G2, vec + V::B2, s_stat, As);
+    lds_barrier();
     ffn.run(As, Hs, w.b1, x);
 #pragma unroll
     for (int j = 0; j < OCB; ++j)
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, s_vec + V::BF2);
-    if (l + 1 < a.n_layers) {
-      ln1_store(s_ln1[(l + 1) & 1], ln1v, D);   // that buffer was last read by LN1 of layer l - 1
-      vecs.load(a.layer[l + 1]);
-    }
+      for (int rb = 0; rb < RB; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, vec + V::F2);
+    vmem_wait();   // this wave's share of the next layer's vectors has landed before the next barrier
   }
 
   if constexpr (CLS) {
@@ -500,23 +506,22 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
     constexpr int LDC = D + 4;
     const int last = a.n_layers - 1;
     const EncW& w = a.layer[last];
+    const float* vec = s_vec[last & 1];
     if (last > 0) gq.start(w.wqkv);
     {
       float nm[RB], rstd[RB];
       resid_stats<TM, D>(x, s_stat, nm, rstd);
-      if (last > 0) vecs.store(s_vec);
-      const float* g1 = s_ln1[last & 1];
-      resid_norm_to_lds<TM, D>(x, nm, rstd, g1, g1 + D, As);
+      resid_norm_to_lds<TM, D>(x, nm, rstd, vec + V::G1, vec + V::B1, As);
     }
-    __syncthreads();
+    lds_barrier();
     gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) {
-      block_to_lds_bf16(acc, cb, rb, s_vec + V::BQKV, QKVs, L::LDQ);
+      block_to_lds_bf16(acc, cb, rb, vec + V::QKV, QKVs, L::LDQ);
     });
     ColGemm<32, D, D / 32> go;
     go.start(w.wo);
-    __syncthreads();
+    lds_barrier();
     group_attention<D, DH, NKB, true>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
-    __syncthreads();
+    lds_barrier();
     // compaction: attention rows g*S of As -> Ac row g (bf16), residual rows g*S -> Xc row g
     bf16* Ac = reinterpret_cast<bf16*>(big);
     float* Xc = reinterpret_cast<float*>(big + 32 * L::LDA * 2);
@@ -538,7 +543,7 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
           *reinterpret_cast<float4*>(&dst[resid_col(j, q)]) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
         }
     }
-    __syncthreads();
+    lds_barrier();
     Resid<32, D> xc;
     {
       const int r = lane & 31;
@@ -555,14 +560,14 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
     }
     FfnStream<32, D> ffn;
     ffn.start(w.w1, w.w2, a.F);
-    go.run(Ac, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<32, D>(xc, jj, rb, acc, s_vec + V::BO); });
+    go.run(Ac, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<32, D>(xc, jj, rb, acc, vec + V::O); });
     // LN2 of the compact rows -> As rows 0..31; its statistics barrier retires the reads of Ac,
     // so the FFN's hidden buffers may reuse the compaction area
-    resid_ln_to_lds<32, D>(xc, s_vec + V::G2, s_vec + V::B2N, s_stat, As);
-    __syncthreads();
+    resid_ln_to_lds<32, D>(xc, vec + V::G2, vec + V::B2, s_stat, As);
+    lds_barrier();
     ffn.run(As, Hs, w.b1, xc);
 #pragma unroll
-    for (int j = 0; j < OCB; ++j) resid_add<32, D>(xc, j, 0, f32x16{}, s_vec + V::BF2);
+    for (int j = 0; j < OCB; ++j) resid_add<32, D>(xc, j, 0, f32x16{}, vec + V::F2);
     float4 gg[D / 128][4], bb[D / 128][4];
 #pragma unroll
     for (int j = 0; j < D / 128; ++j)
@@ -663,7 +668,9 @@ FE_DEV void zero_rows_bf16(bf16* Y, long long row0, long long R, const int* s_va
 //   TAIL 0: x2 = x1 + FFN(LN2(x1)) -> Xout (fp32); when Hout is set (last item layer) also
 //           Hout = LNf(x2) in bf16, with zero rows for padding rows;
 //   TAIL 1: Xout = x1, and the item layers' cross-attention queries Qout = LN2(x1) Wq + bq (bf16).
-template <int TM, int D, int TAIL>
+// NCH > 0 fixes the FFN width at 128*NCH, which lets its weight stream run three stages deep
+// (used at D = 128, where the third stage still fits the register budget).
+template <int TM, int D, int TAIL, int NCH>
 __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   constexpr int LDA = D + APAD;
   constexpr int HS_BYTES = 2 * TM * HLD * 2, QS_BYTES = 4 * 32 * 40 * 2;
@@ -684,15 +691,15 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   stage_rows<TM, D>(a.O, false, D, row0, s_valid, nullptr, nullptr, As);
   Resid<TM, D> x;
   resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
-  FfnStream<TM, D> ffn;
+  FfnStream<TM, D, NCH, NCH ? 3 : 2> ffn;
   if constexpr (TAIL == 0) ffn.start(a.w1, a.w2, a.F);
-  __syncthreads();
+  lds_barrier();
   go.run(As, LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, a.bo); });
   ColGemm<TM, D, D / 32> gq;
   if constexpr (TAIL == 1) gq.start(a.wq);
   // LN2 -> As (the barrier inside the statistics retires every read of As by the Wo product)
   resid_ln_to_lds<TM, D>(x, a.ln2g, a.ln2b, s_stat, As);
-  __syncthreads();
+  lds_barrier();
   if constexpr (TAIL == 0) {
     ffn.run(As, reinterpret_cast<bf16*>(big), a.b1, x);
 #pragma unroll
@@ -763,15 +770,18 @@ hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
 template <int TM, int D>
 hipError_t launch_post_t(const PostArgs& a, hipStream_t s) {
   dim3 grid((a.R + TM - 1) / TM);
-  if (a.tail == 0) hipLaunchKernelGGL((k_post<TM, D, 0>), grid, dim3(WG), 0, s, a);
-  else hipLaunchKernelGGL((k_post<TM, D, 1>), grid, dim3(WG), 0, s, a);
+  if (a.tail == 1) hipLaunchKernelGGL((k_post<TM, D, 1, 0>), grid, dim3(WG), 0, s, a);
+  else if (D == 128 && a.F == 4 * D) hipLaunchKernelGGL((k_post<TM, D, 0, (D == 128 ? 4 : 0)>), grid, dim3(WG), 0, s, a);
+  else hipLaunchKernelGGL((k_post<TM, D, 0, 0>), grid, dim3(WG), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// groups of up to 64 rows (the score blocks of a group are held in registers at once)
-int module_small_tile_rows(int d) { return d >= 512 ? 32 : 64; }
+// groups of up to 64 rows (the score blocks of a group are held in registers at once); at
+// d = 512 a tile's q|k|v, the double-buffered block vectors and the LN1 tile exceed the LDS of a
+// compute unit, so such modules take the separate-attention path
+int module_small_tile_rows(int d) { return d >= 512 ? 0 : 64; }
 
 hipError_t launch_module_small(ModuleArgs a, hipStream_t s) {
   if (a.n_groups <= 0) return hipSuccess;
@@ -782,7 +792,6 @@ hipError_t launch_module_small(ModuleArgs a, hipStream_t s) {
   switch (a.D) {
     case 128: return dh == 64 ? launch_module_t<64, 128, 64>(a, s) : launch_module_t<64, 128, 32>(a, s);
     case 256: return dh == 64 ? launch_module_t<64, 256, 64>(a, s) : launch_module_t<64, 256, 32>(a, s);
-    case 512: return dh == 64 ? launch_module_t<32, 512, 64>(a, s) : launch_module_t<32, 512, 32>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
