@@ -144,14 +144,14 @@ struct ColGemm {
     }
   }
   FE_DEV void start(const void* W) {
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3);   // wave within its group of four
     Wl = reinterpret_cast<const bf16x8*>(W) + (long long)wave * KS * 64 + (threadIdx.x & 63);
     load(0);
   }
   template <class Epi>
   FE_DEV void run(const bf16* As, int lda, Epi&& epi) {
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3);   // wave within its group of four
     f32x16 acc[RB][NBW];
 #pragma unroll
     for (int t = 0; t < NST; ++t) {

@@ -30,13 +30,13 @@ constexpr int HLD = HC + APAD;
 // queries of each group are computed.  One wave per (group, head, 16-query
 // tile), two such units in flight per wave: the NKB score blocks are formed first as
 // independent MFMA chains, then one softmax over the whole group, then P V.
-template <int D, int DH, int NKB, bool FIRST_TILE = false>
+template <int D, int DH, int NKB, bool FIRST_TILE = false, int WAVES = 4>
 FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng, int S, float sl2) {
   constexpr int H = D / DH, NU = 2, QT = FIRST_TILE ? 1 : NKB, UPG = H * QT;   // units per group
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g4 = lane >> 4, c16 = lane & 15;
   const int units = ng * UPG;
-  for (int u0 = wave * NU; u0 < units; u0 += 4 * NU) {
+  for (int u0 = wave * NU; u0 < units; u0 += WAVES * NU) {
     int base[NU], hcol[NU], q[NU];
     bool live[NU];
     bf16x8 qf[NU][DH / 32];
@@ -145,7 +145,7 @@ struct Resid {
 };
 
 FE_DEV int resid_col(int j, int q) {
-  return (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) + 4 * j) * 32 + 8 * q + 4 * ((threadIdx.x & 63) >> 5);
+  return (__builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3) + 4 * j) * 32 + 8 * q + 4 * ((threadIdx.x & 63) >> 5);
 }
 
 // x = rows row0.. of X (fp32 or bf16, row stride D); rows whose s_valid flag is 0 are zero.
@@ -199,7 +199,7 @@ FE_DEV void resid_add(Resid<TM, D>& x, int jj, int rb, const f32x16& acc, const 
 template <int TM, int D>
 FE_DEV void resid_stats(const Resid<TM, D>& x, float2* s_stat, float (&nm)[TM / 32], float (&rstd)[TM / 32]) {
   constexpr int RB = TM / 32, BPW = D / 128, NL = 16 * BPW;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     float sum = 0.f;
@@ -280,15 +280,15 @@ struct Vecs {
 };
 
 // Copy one block's vectors from global memory straight into the LDS block dst with
-// global_load_lds (16 bytes per lane, no registers): wave w moves the 1 KiB chunks w, w + 4, ....
+// global_load_lds (16 bytes per lane, no registers): wave w of W moves the 1 KiB chunks w, w + W, ....
 // The data is visible to other waves once each issuing wave has passed vmem_wait() and then a
 // barrier; until then dst must not be read, and it must not be written while still being read.
 template <int D>
 FE_DEV void vecs_dma(const EncW& w, float* dst) {
   using V = Vecs<D>;
   constexpr int NCHK = (V::SIZE * 4 + 1023) / 1024;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int ch = wave; ch < NCHK; ch += 4) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  for (int ch = wave; ch < NCHK; ch += nwaves) {
     const int o = ch * 256 + lane * 4;              // this lane's first float
     if (o >= V::SIZE) continue;
     const float* src = o < V::B1    ? w.ln1g + o
@@ -347,7 +347,7 @@ struct FfnStream {
     }
   }
   FE_DEV void start(const void* w1p, const void* w2p, int f) {
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3), lane = threadIdx.x & 63;
     F = f;
     W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
     W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (f / 16) * 64 + lane;
@@ -356,7 +356,7 @@ struct FfnStream {
   }
   template <class Acc>
   FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
     if constexpr (NCH > 0) {
 #pragma unroll
       for (int c = 0; c < NCH; ++c) chunk(c, NCH, As, Hs, b1, x, lane, wave);
@@ -435,10 +435,11 @@ struct ModuleSmem {
 // n_layers encoder blocks and the final LayerNorm over a tile of whole groups; one launch per
 // module.  Per block: LN1 -> As; q|k|v -> LDS; attention per (group, head) -> As; x += O Wo + bo;
 // LN2 -> As; x += FFN.  The fp32 residual x never leaves registers; the result leaves as fp32.
-template <int TM, int D, int DH, int NKB, bool CLS>
-__global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
+template <int TM, int D, int DH, int NKB, bool CLS, int G>
+__global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleArgs a) {
+  static_assert(G == 1 || !CLS, "the compacted last block runs on one wave group");
   using L = ModuleSmem<TM, D>;
-  constexpr int RB = TM / 32, OCB = D / 128;
+  constexpr int TMG = TM / G, RB = TMG / 32, OCB = D / 128;
   __shared__ __attribute__((aligned(16))) bf16 As[TM * L::LDA];
   __shared__ __attribute__((aligned(16))) char big[L::BIG];
   __shared__ __attribute__((aligned(16))) float2 s_stat[4 * TM];
@@ -447,6 +448,14 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
   bf16* QKVs = reinterpret_cast<bf16*>(big);
   bf16* Hs = reinterpret_cast<bf16*>(big);
   const int lane = threadIdx.x & 63;
+  // wave group gr (waves 4gr .. 4gr+3) owns tile rows gr*TMG .. gr*TMG + TMG - 1 for every
+  // row-wise step; attention runs over the whole tile on all 4G waves
+  const int gr = G == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x >> 8);
+  bf16* Ag = As + gr * TMG * L::LDA;
+  bf16* QKVg = QKVs + gr * TMG * L::LDQ;
+  bf16* Hg = Hs + gr * 2 * TMG * HLD;
+  float2* statg = s_stat + gr * 4 * TMG;
+  const int* validg = s_valid + gr * TMG;
 
   const int g0 = xcd_tile(blockIdx.x, gridDim.x) * a.gpt;
   const int ng = min(a.gpt, a.n_groups - g0);
@@ -455,11 +464,11 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
 
   // layer 0's vectors: DMA into LDS, published by the statistics barrier of the first LN1
   vecs_dma<D>(a.layer[0], s_vec[0]);
-  ColGemm<TM, D, 3 * D / 32> gq;
+  ColGemm<TMG, D, 3 * D / 32> gq;
   gq.start(a.layer[0].wqkv);
   if (!mark_rows<TM>(0, nrows, nullptr, 1, s_valid)) return;
-  Resid<TM, D> x;
-  resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
+  Resid<TMG, D> x;
+  resid_load<TMG, D>(x, a.Xin, a.xin_f32, row0 + gr * TMG, validg);
   vmem_wait();
 
   using V = Vecs<D>;
@@ -472,29 +481,29 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
     // vector buffer is free for layer l + 1 (waited for at the end of this layer).
     {
       float nm[RB], rstd[RB];
-      resid_stats<TM, D>(x, s_stat, nm, rstd);
+      resid_stats<TMG, D>(x, statg, nm, rstd);
       if (l + 1 < a.n_layers) vecs_dma<D>(a.layer[l + 1], s_vec[(l + 1) & 1]);
-      resid_norm_to_lds<TM, D>(x, nm, rstd, vec + V::G1, vec + V::B1, As);
+      resid_norm_to_lds<TMG, D>(x, nm, rstd, vec + V::G1, vec + V::B1, Ag);
     }
     lds_barrier();
-    gq.run(As, L::LDA, [&](int, int cb, int rb, const f32x16& acc) {
-      block_to_lds_bf16(acc, cb, rb, vec + V::QKV, QKVs, L::LDQ);
+    gq.run(Ag, L::LDA, [&](int, int cb, int rb, const f32x16& acc) {
+      block_to_lds_bf16(acc, cb, rb, vec + V::QKV, QKVg, L::LDQ);
     });
-    ColGemm<TM, D, D / 32> go;
+    ColGemm<TMG, D, D / 32> go;
     go.start(w.wo);
     lds_barrier();
-    group_attention<D, DH, NKB>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
-    FfnStream<TM, D> ffn;
+    group_attention<D, DH, NKB, false, 4 * G>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
+    FfnStream<TMG, D> ffn;
     ffn.start(w.w1, w.w2, a.F);
     lds_barrier();
-    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, vec + V::O); });
-    resid_ln_to_lds<TM, D>(x, vec + V::G2, vec + V::B2, s_stat, As);
+    go.run(Ag, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TMG, D>(x, jj, rb, acc, vec + V::O); });
+    resid_ln_to_lds<TMG, D>(x, vec + V::G2, vec + V::B2, statg, Ag);
     lds_barrier();
-    ffn.run(As, Hs, w.b1, x);
+    ffn.run(Ag, Hg, w.b1, x);
 #pragma unroll
     for (int j = 0; j < OCB; ++j)
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, vec + V::F2);
+      for (int rb = 0; rb < RB; ++rb) resid_add<TMG, D>(x, j, rb, f32x16{}, vec + V::F2);
     vmem_wait();   // this wave's share of the next layer's vectors has landed before the next barrier
   }
 
@@ -607,10 +616,10 @@ __global__ __launch_bounds__(WG, 2) void k_module_small(ModuleArgs a) {
       bb[j][q] = *reinterpret_cast<const float4*>(&a.lnfb[resid_col(j, q)]);
     }
   float nm[RB], rstd[RB];
-  resid_stats<TM, D>(x, s_stat, nm, rstd);
+  resid_stats<TMG, D>(x, statg, nm, rstd);
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int r = rb * 32 + (lane & 31);
+    const int r = gr * TMG + rb * 32 + (lane & 31);   // tile row
     if (!s_valid[r]) continue;
     long long out;
     if (a.first_row_only) {
@@ -744,27 +753,32 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   }
 }
 
-template <int TM, int D, int DH, bool CLS>
+template <int TM, int D, int DH, bool CLS, int G>
 hipError_t launch_module_c(const ModuleArgs& a, hipStream_t s) {
   const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
+  const dim3 grid(tiles), block(WG * G);
   switch ((a.S + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4, CLS>), dim3(tiles), dim3(WG), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1, CLS, G>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2, CLS, G>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3, CLS, G>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4, CLS, G>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-// first-row-only modules on 64-row tiles take the compacted last block (a 32-row tile would
-// gain nothing from compaction)
+// First-row-only modules take the compacted last block.  Launches with few tiles (at most half
+// a workgroup per compute unit) take two wave groups per tile, halving each wave's share of
+// every row-wise step: there the per-tile latency, not the compute units' throughput, sets the
+// time.
 template <int TM, int D, int DH>
 hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
-  if constexpr (TM == 64) {
-    if (a.first_row_only) return launch_module_c<TM, D, DH, true>(a, s);
+  if (a.first_row_only) return launch_module_c<TM, D, DH, true, 1>(a, s);
+  if constexpr (D == 128) {   // at d = 256 two groups per compute unit would spill registers
+    const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
+    if (tiles <= 128) return launch_module_c<TM, D, DH, false, 2>(a, s);
   }
-  return launch_module_c<TM, D, DH, false>(a, s);
+  return launch_module_c<TM, D, DH, false, 1>(a, s);
 }
 
 template <int TM, int D>
