@@ -392,8 +392,16 @@ struct Bufs {
 
 // One pre-LN encoder block over nb batches of `per` rows; attention stays inside a batch.
 // `xin` is the block input (act or fp32); the output residual stream is written to b.X.
+// The key/value projections a bf16 block's tail may also produce from the module's final
+// LayerNorm of its output (the last context block; see PostArgs).
+struct KvOut {
+  const float *lnf_g, *lnf_b;
+  const void* wkv; const float* bkv; void* kv; int layers;
+  int32_t* zero; int zero_n;   // status words this launch clears (or nullptr)
+};
+
 fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const void* xin, bool xin_f32, const Bufs& b,
-                    const int32_t* nvalid, hipStream_t s) {
+                    const int32_t* nvalid, hipStream_t s, const KvOut* kvo = nullptr) {
   const int d = m->cfg.d, F = m->cfg.ffn_dim, R = nb * per;
   const bool bf = m->bf16;
   const size_t e = bf ? 2 : 4;
@@ -415,6 +423,17 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     // output projection, residual, LN2 and FFN in one kernel
     PostArgs p{b.O, xin, xin_f32, b.X, R, per, nvalid, d, F, 0, w.wo, w.bo, w.ln2g, w.ln2b,
                w.w1, w.b1, w.w2, w.b2, nullptr, nullptr, nullptr};
+    if (kvo) {
+      p.Xout = nullptr;   // nothing reads the module's residual after its key/value projections
+      p.lnfg = kvo->lnf_g;
+      p.lnfb = kvo->lnf_b;
+      p.wkv = kvo->wkv;
+      p.bkv = kvo->bkv;
+      p.kv = kvo->kv;
+      p.kv_layers = kvo->layers;
+      p.zero = kvo->zero;
+      p.zero_n = kvo->zero_n;
+    }
     FE_LAUNCH(F_POST, s, launch_post(p, s));
     return FE_OK;
   }
@@ -612,7 +631,8 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
   const int d = m->cfg.d, R = B * T;
   int32_t* status_ctx = at<int32_t>(ws, w.status) + B;
   // the context status words start at zero: cleared before the embedding gather sets bits in
-  // them, else by the key/value projection at the end of this call (nothing else writes them)
+  // them, else by the launch that writes the key/value cache at the end of this call (nothing
+  // else writes them)
   const bool clear_late = bf && !ctx_ids;
   if (!clear_late) FE_LAUNCH(F_FILL, s, launch_fill_i32(status_ctx, B, 0, s));
   const void* src = x;
@@ -627,10 +647,16 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
     st = run_module(m, m->ctx, B, T, src, false, m->ctx_lnf_g, m->ctx_lnf_b, b.X, false, s);
     if (st != FE_OK) return st;
   } else {
+    // on bf16 models the last block's tail also applies the final LayerNorm and writes the
+    // key/value cache of every item layer
+    const KvOut kvo{m->ctx_lnf_g, m->ctx_lnf_b, m->wkv, m->bkv, kv, m->cfg.n_layers,
+                    clear_late ? status_ctx : nullptr, B};
     for (int l = 0; l < m->cfg.n_layers; ++l) {
-      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s);
+      const bool last = l + 1 == m->cfg.n_layers;
+      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s, bf && last ? &kvo : nullptr);
       if (st != FE_OK) return st;
     }
+    if (bf) return FE_OK;
   }
   // key/value projections of all item layers, with the context module's final LayerNorm fused
   // into their prologue unless the module kernel already applied it
@@ -667,10 +693,10 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
   const int R = B * Ucap;
   const size_t e = bf ? 2 : 4;
   int32_t* status_items = at<int32_t>(ws, w.status);
-  FE_LAUNCH(F_DEDUP, s, launch_dedup(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, s));
   const void* table = pool ? pool : m->emb;
   const long long table_bs = pool ? (long long)M * d : 0;
   void* G0 = at<char>(ws, w.i_g0);
+  FE_LAUNCH(F_DEDUP, s, launch_dedup(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, s));
   FE_LAUNCH(F_GATHER, s, launch_gather_rows(table, table_bs, M, uniq, Ucap, n_uniq, B, Ucap, d, G0, nullptr, 0, bf, s));
   float* G = at<float>(ws, w.i_g);
   void* qkv = at<char>(ws, w.i_qkv);

@@ -107,7 +107,8 @@ struct AttnArgs {
 // Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
 //   tail 0: Xout = x1 + FFN(LN2(x1)); with Hout != nullptr also Hout = LayerNorm(x1 + FFN)
 //           with gains lnfg, offsets lnfb (bf16), padding rows of Hout below R set to zero
-//           (Xout may then be nullptr);
+//           (Xout may then be nullptr); with kv != nullptr the key/value projections of the
+//           same LayerNorm (see the fields below);
 //   tail 1: Xout = x1 and Qout = LN2(x1) Wq + bq (bf16).
 // Rows with (r % rows_per_batch) >= nvalid[r / rows_per_batch] are padding.
 struct PostArgs {
@@ -118,6 +119,11 @@ struct PostArgs {
   const void* w1; const float* b1; const void* w2; const float* b2;
   const void* wq; const float* bq; void* Qout;
   const float *lnfg, *lnfb; void* Hout;
+  // tail 0, last context block: with kv != nullptr, for l < kv_layers
+  //   kv[(2l + j) * R * D + r * D + c] = (LayerNorm(x1 + FFN) Wkv + bkv)[r][(2l + j) * D + c]
+  //   (LayerNorm with lnfg, lnfb; Wkv [D][2 * kv_layers * D] in packed fragment order, bf16 out)
+  const void* wkv; const float* bkv; void* kv; int kv_layers;
+  int32_t* zero; int zero_n;            // zero[0 .. zero_n) is cleared (or nullptr)
 };
 
 // Device pointers of one pre-LN encoder block (matrices of bf16 models in packed fragment order).

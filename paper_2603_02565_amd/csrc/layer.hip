@@ -691,6 +691,8 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int row0 = xcd_tile(blockIdx.x, gridDim.x) * TM;
 
+  if (a.zero && blockIdx.x == 0)
+    for (int e = threadIdx.x; e < a.zero_n; e += WG) a.zero[e] = 0;
   ColGemm<TM, D, D / 32> go;
   go.start(a.wo);
   if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) {
@@ -742,6 +744,24 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
           }
       }
       zero_rows_bf16<TM, D>(H, row0, a.R, s_valid);
+    }
+    if (a.kv) {
+      // last context block: the module's final LayerNorm feeds the key/value projections of
+      // every item layer (one slab of 2D columns per layer: keys, then values)
+      float nm[TM / 32], rstd[TM / 32];
+      resid_stats<TM, D>(x, s_stat, nm, rstd);    // also retires the FFN's reads of As and big
+      resid_norm_to_lds<TM, D>(x, nm, rstd, a.lnfg, a.lnfb, As);
+      lds_barrier();
+      bf16* st = reinterpret_cast<bf16*>(big) + wave * 32 * 40;
+      for (int l = 0; l < a.kv_layers; ++l) {
+        ColGemm<TM, D, 2 * D / 32> gkv;
+        gkv.start(static_cast<const bf16x8*>(a.wkv) + (long long)l * (2 * D / 32) * (D / 16) * 64);
+        gkv.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) {
+          const int half = cb / (D / 32), c0 = (cb % (D / 32)) * 32;   // 0: keys, 1: values
+          bf16* out = static_cast<bf16*>(a.kv) + (long long)(2 * l + half) * a.R * D + (long long)row0 * D + c0;
+          store_block_bf16(acc, a.bkv + (2 * l + half) * D + c0, st, out, D, rb, s_valid);
+        });
+      }
     }
   } else {
     resid_store<TM, D>(x, a.Xout, row0, s_valid);
