@@ -63,7 +63,9 @@ def family_flops(c, U, fam_names):
     Fused kernels take the work of the stages they contain: "layer" (a whole module of short
     groups in one kernel: the sequence encoder, and the cross-sequence and context modules when
     their groups are short), "post" (output projection and FFN, or query projection, after a
-    separate attention kernel), "gemm" (q|k|v projections and the key/value cache).
+    separate attention kernel, and the key/value cache in the last context tail), "attention"
+    (with the q|k|v projection when the fused self-attention kernel applies), "gemm" (separate
+    projections).
     """
     d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
     tile = 0 if d >= 512 else 64          # module kernel: groups of up to 64 rows, d <= 256
@@ -74,21 +76,26 @@ def family_flops(c, U, fam_names):
         out[fam] = out.get(fam, 0.0) + v
 
     fused = "layer" in fam_names or "post" in fam_names
+
+    def selfattn(group):   # q|k|v projection inside the attention kernel (d = 128, head width 32)
+        return fused and d == 128 and d // c.n_heads == 32 and group <= 256
+
     for rows, groups, size, first in ((B * T, B, T, False), (B * K * S, B * K, S, True), (B * K, B, K, False)):
         proj, attn, tail = module_parts(d, F, n, rows, groups, size, first)
         if fused and size <= tile:
             add("layer", proj + attn + tail)
         elif fused:
-            add("gemm", proj)
+            add("attention" if selfattn(size) else "gemm", proj)
             add("attention", attn)
             add("post", tail)
         else:
             add("gemm", proj + tail)
             add("attention", attn)
-    add("gemm", 4.0 * n * B * T * d * d)                      # key/value cache of the item layers
+    # key/value cache of the item layers: in the last context tail when that tail is fused
+    add("post" if fused and T > tile else "gemm", 4.0 * n * B * T * d * d)
     # distinct items: q|k|v, self-attention, output + query projections, cross-attention, FFN
     add("attention", sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U))
-    add("gemm", n * 6.0 * d * d * rows_item)
+    add("attention" if selfattn(min(c.M, K * c.L)) else "gemm", n * 6.0 * d * d * rows_item)
     add("post" if fused else "gemm", n * (6.0 * d * d + 4.0 * d * F) * rows_item)
     return out
 

@@ -406,19 +406,25 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   const bool bf = m->bf16;
   const size_t e = bf ? 2 : 4;
   const float scale = 1.0f / sqrtf((float)(d / m->cfg.n_heads));
-  GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
-  g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
-  fe_status st0 = run_proj(m, g, s);
-  if (st0 != FE_OK) return st0;
-  AttnArgs a{};
-  a.Q = b.qkv; a.q_bs = (long long)per * 3 * d; a.q_rs = 3 * d;
-  a.K = static_cast<const char*>(b.qkv) + d * e; a.k_bs = a.q_bs; a.k_rs = 3 * d;
-  a.V = static_cast<const char*>(b.qkv) + 2 * d * e; a.v_bs = a.q_bs; a.v_rs = 3 * d;
-  a.O = b.O; a.o_bs = (long long)per * d; a.o_rs = d;
-  a.B = nb; a.nq = per; a.nk = per; a.n_heads = m->cfg.n_heads; a.dh = d / m->cfg.n_heads;
-  a.q_valid = nvalid; a.k_valid = nvalid;
-  a.scale = scale;
-  FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+  if (bf && self_attention_fits(d, m->cfg.n_heads, per)) {
+    // LN1, q|k|v of one head and attention in one kernel per (batch, head)
+    SelfAttnArgs sa{xin, xin_f32, nb, per, nvalid, w.ln1g, w.ln1b, w.wqkv, w.bqkv, b.O, m->cfg.n_heads, scale};
+    FE_LAUNCH(F_ATTN, s, launch_self_attention(sa, d, s));
+  } else {
+    GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
+    g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
+    fe_status st0 = run_proj(m, g, s);
+    if (st0 != FE_OK) return st0;
+    AttnArgs a{};
+    a.Q = b.qkv; a.q_bs = (long long)per * 3 * d; a.q_rs = 3 * d;
+    a.K = static_cast<const char*>(b.qkv) + d * e; a.k_bs = a.q_bs; a.k_rs = 3 * d;
+    a.V = static_cast<const char*>(b.qkv) + 2 * d * e; a.v_bs = a.q_bs; a.v_rs = 3 * d;
+    a.O = b.O; a.o_bs = (long long)per * d; a.o_rs = d;
+    a.B = nb; a.nq = per; a.nk = per; a.n_heads = m->cfg.n_heads; a.dh = d / m->cfg.n_heads;
+    a.q_valid = nvalid; a.k_valid = nvalid;
+    a.scale = scale;
+    FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+  }
   if (bf) {
     // output projection, residual, LN2 and FFN in one kernel
     PostArgs p{b.O, xin, xin_f32, b.X, R, per, nvalid, d, F, 0, w.wo, w.bo, w.ln2g, w.ln2b,
@@ -437,7 +443,7 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     FE_LAUNCH(F_POST, s, launch_post(p, s));
     return FE_OK;
   }
-  g = gemm(b.O, d, false, R, d, d, w.wo, w.bo, b.X, d, true, EPI_RESID);
+  GemmArgs g = gemm(b.O, d, false, R, d, d, w.wo, w.bo, b.X, d, true, EPI_RESID);
   g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = nvalid; g.rows_per_batch = per;
   fe_status st = run_proj(m, g, s);
   if (st != FE_OK) return st;
@@ -708,26 +714,32 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     const ItemW& iw = m->item[l];
     const void* xin = l == 0 ? G0 : static_cast<const void*>(G);
     const bool xin_f32 = l > 0;
-    GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, iw.wqkv, iw.bqkv, qkv, 3 * d, false, EPI_STORE);
-    g.ln_g = iw.ln1g; g.ln_b = iw.ln1b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-    st = run_proj(m, g, s);
-    if (st != FE_OK) return st;
-    AttnArgs a{};
-    a.Q = qkv; a.q_bs = (long long)Ucap * 3 * d; a.q_rs = 3 * d;
-    a.K = static_cast<const char*>(qkv) + d * e; a.k_bs = a.q_bs; a.k_rs = 3 * d;
-    a.V = static_cast<const char*>(qkv) + 2 * d * e; a.v_bs = a.q_bs; a.v_rs = 3 * d;
-    a.O = O; a.o_bs = (long long)Ucap * d; a.o_rs = d;
-    a.B = B; a.nq = Ucap; a.nk = Ucap; a.n_heads = m->cfg.n_heads; a.dh = dh;
-    a.q_valid = n_uniq; a.k_valid = n_uniq;
-    a.scale = 1.0f / sqrtf((float)dh);
-    FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+    if (bf && self_attention_fits(d, m->cfg.n_heads, Ucap)) {
+      SelfAttnArgs sa{xin, xin_f32, B, Ucap, n_uniq, iw.ln1g, iw.ln1b, iw.wqkv, iw.bqkv, O, m->cfg.n_heads,
+                      1.0f / sqrtf((float)dh)};
+      FE_LAUNCH(F_ATTN, s, launch_self_attention(sa, d, s));
+    } else {
+      GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, iw.wqkv, iw.bqkv, qkv, 3 * d, false, EPI_STORE);
+      g.ln_g = iw.ln1g; g.ln_b = iw.ln1b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
+      st = run_proj(m, g, s);
+      if (st != FE_OK) return st;
+      AttnArgs a{};
+      a.Q = qkv; a.q_bs = (long long)Ucap * 3 * d; a.q_rs = 3 * d;
+      a.K = static_cast<const char*>(qkv) + d * e; a.k_bs = a.q_bs; a.k_rs = 3 * d;
+      a.V = static_cast<const char*>(qkv) + 2 * d * e; a.v_bs = a.q_bs; a.v_rs = 3 * d;
+      a.O = O; a.o_bs = (long long)Ucap * d; a.o_rs = d;
+      a.B = B; a.nq = Ucap; a.nk = Ucap; a.n_heads = m->cfg.n_heads; a.dh = dh;
+      a.q_valid = n_uniq; a.k_valid = n_uniq;
+      a.scale = 1.0f / sqrtf((float)dh);
+      FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
+    }
     if (bf) {
       // x1 = x + O Wo + bo -> G, and the cross-attention queries q = LN2(x1) Wq + bq -> Qc
       PostArgs p{O, xin, xin_f32, G, R, Ucap, n_uniq, d, F, 1, iw.wo, iw.bo, iw.ln2g, iw.ln2b,
                  nullptr, nullptr, nullptr, nullptr, iw.wq, iw.bq, Qc};
       FE_LAUNCH(F_POST, s, launch_post(p, s));
     } else {
-      g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
+      GemmArgs g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
       g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
       st = run_proj(m, g, s);
       if (st != FE_OK) return st;
@@ -755,7 +767,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }
-    g = gemm(O, d, false, R, d, d, iw.wo2, iw.bo2, G, d, true, EPI_RESID);
+    GemmArgs g = gemm(O, d, false, R, d, d, iw.wo2, iw.bo2, G, d, true, EPI_RESID);
     g.res = G; g.ldr = d; g.res_f32 = true; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
     st = run_proj(m, g, s);
     if (st != FE_OK) return st;

@@ -104,6 +104,22 @@ struct AttnArgs {
   float scale;
 };
 
+// Self-attention of a pre-LN block with the q|k|v projection inside (bf16 models, d = 128,
+// head width 32, at most 256 rows per batch): for every batch b and head h,
+//   O[b*per + r][h*32 ..] = softmax(q k^T * scale) v over the batch's valid rows,
+//   q|k|v = LN1(X) Wqkv + bqkv restricted to head h.
+// X is [B*per][d] (fp32 when x_f32, else act); rows r >= nvalid[b] are padding (O not written).
+struct SelfAttnArgs {
+  const void* X; int x_f32;
+  int B, per; const int32_t* nvalid;
+  const float *ln_g, *ln_b;
+  const void* wqkv; const float* bqkv;
+  void* O;
+  int n_heads; float scale;
+};
+bool self_attention_fits(int d, int n_heads, int per);
+hipError_t launch_self_attention(const SelfAttnArgs& a, int d, hipStream_t s);
+
 // Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
 //   tail 0: Xout = x1 + FFN(LN2(x1)); with Hout != nullptr also Hout = LayerNorm(x1 + FFN)
 //           with gains lnfg, offsets lnfb (bf16), padding rows of Hout below R set to zero
