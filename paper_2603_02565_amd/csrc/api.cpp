@@ -285,7 +285,7 @@ fe_status check_config(const fe_config* c) {
 struct Ws {
   size_t status;                                        // int32 [2][B]: items, context
   size_t c_xin, c_x, c_qkv, c_o, c_h;                   // context stage
-  size_t i_g0, i_g, i_qkv, i_o, i_q, i_h;               // item stage
+  size_t i_g0, i_g, i_g1, i_qkv, i_o, i_q, i_h;         // item stage
   size_t s_x, s_qkv, s_o, s_h, s_c;                     // sequence + cross stages
   size_t total;
 };
@@ -322,6 +322,7 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     Bump b{base};
     w.i_g0 = b.take(R * d * e);
     w.i_g = b.take(R * d * 4);
+    w.i_g1 = b.take(R * d * 4);
     w.i_qkv = b.take(R * 3 * d * e);
     w.i_o = b.take(R * d * e);
     w.i_q = b.take(R * d * e);
@@ -705,6 +706,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
   FE_LAUNCH(F_DEDUP, s, launch_dedup(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, s));
   FE_LAUNCH(F_GATHER, s, launch_gather_rows(table, table_bs, M, uniq, Ucap, n_uniq, B, Ucap, d, G0, nullptr, 0, bf, s));
   float* G = at<float>(ws, w.i_g);
+  float* G1 = at<float>(ws, w.i_g1);
   void* qkv = at<char>(ws, w.i_qkv);
   void* O = at<char>(ws, w.i_o);
   void* Qc = at<char>(ws, w.i_q);
@@ -733,6 +735,21 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       a.scale = 1.0f / sqrtf((float)dh);
       FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
     }
+    const void* Kc = static_cast<const char*>(kv) + (size_t)(2 * l) * B * T * d * e;
+    const void* Vc = static_cast<const char*>(kv) + (size_t)(2 * l + 1) * B * T * d * e;
+    if (bf && cross_attention_fits(d, m->cfg.n_heads, Ucap, T)) {
+      // x1 = x + O Wo + bo -> G1, queries LN2(x1) Wq + bq and the cross-attention in one kernel
+      // per (request, head); its output goes to Qc (every head's workgroup reads all of O)
+      CrossAttnArgs ca{O, xin, xin_f32, G1, B, Ucap, n_uniq, iw.wo, iw.bo, iw.ln2g, iw.ln2b, iw.wq, iw.bq,
+                       Kc, Vc, T, Qc, m->cfg.n_heads, 1.0f / sqrtf((float)dh)};
+      FE_LAUNCH(F_ATTN, s, launch_cross_attention(ca, d, s));
+      const bool last = l + 1 == m->cfg.n_layers;
+      PostArgs p{Qc, G1, 1, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
+                 iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr,
+                 last ? m->item_lnf_g : nullptr, last ? m->item_lnf_b : nullptr, last ? H : nullptr};
+      FE_LAUNCH(F_POST, s, launch_post(p, s));
+      continue;
+    }
     if (bf) {
       // x1 = x + O Wo + bo -> G, and the cross-attention queries q = LN2(x1) Wq + bq -> Qc
       PostArgs p{O, xin, xin_f32, G, R, Ucap, n_uniq, d, F, 1, iw.wo, iw.bo, iw.ln2g, iw.ln2b,
@@ -751,8 +768,8 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     }
     AttnArgs c{};
     c.Q = Qc; c.q_bs = (long long)Ucap * d; c.q_rs = d;
-    c.K = static_cast<const char*>(kv) + (size_t)(2 * l) * B * T * d * e; c.k_bs = (long long)T * d; c.k_rs = d;
-    c.V = static_cast<const char*>(kv) + (size_t)(2 * l + 1) * B * T * d * e; c.v_bs = (long long)T * d; c.v_rs = d;
+    c.K = Kc; c.k_bs = (long long)T * d; c.k_rs = d;
+    c.V = Vc; c.v_bs = (long long)T * d; c.v_rs = d;
     c.O = O; c.o_bs = (long long)Ucap * d; c.o_rs = d;
     c.B = B; c.nq = Ucap; c.nk = T; c.n_heads = m->cfg.n_heads; c.dh = dh;
     c.q_valid = n_uniq; c.k_valid = nullptr;

@@ -120,6 +120,24 @@ struct SelfAttnArgs {
 bool self_attention_fits(int d, int n_heads, int per);
 hipError_t launch_self_attention(const SelfAttnArgs& a, int d, hipStream_t s);
 
+// Second half of an item layer's attention (bf16 models, d = 128, head width 32, at most 256
+// rows per batch and 256 context keys): for every batch b,
+//   x1 = Xin + O Wo + bo, written to Xout (fp32) for the valid rows;
+//   O2[b*per + r][h*32 ..] = softmax(q k^T * scale) v for every head h, with q = LN2(x1) Wq + bq
+//   and k, v the head's columns of Kc, Vc [B][T][d] (act).
+// O (act, all heads of the self-attention) and O2 must differ, and so must Xin and Xout: every
+// head's workgroup reads the whole rows of O and Xin.
+struct CrossAttnArgs {
+  const void* O; const void* Xin; int xin_f32; float* Xout;
+  int B, per; const int32_t* nvalid;
+  const void* wo; const float* bo; const float *ln2g, *ln2b; const void* wq; const float* bq;
+  const void* Kc; const void* Vc; int T;
+  void* O2;
+  int n_heads; float scale;
+};
+bool cross_attention_fits(int d, int n_heads, int per, int T);
+hipError_t launch_cross_attention(const CrossAttnArgs& a, int d, hipStream_t s);
+
 // Tail of a block after attention (bf16 models): x1 = Xin + O Wo + bo, then
 //   tail 0: Xout = x1 + FFN(LN2(x1)); with Hout != nullptr also Hout = LayerNorm(x1 + FFN)
 //           with gains lnfg, offsets lnfb (bf16), padding rows of Hout below R set to zero
