@@ -260,6 +260,22 @@ def main() -> int:
     U = bufs["n_uniq"].cpu().numpy().tolist()
     asm_bytes = assemble_bytes(c, U)
 
+    # ---- the same pass captured once as a HIP graph and replayed K times
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(args.steps):
+        graph.replay()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    graph_ms = g0.elapsed_time(g1) / args.steps
+    del graph
+
     # ---- kernel-timing region: the same steps with HIP events around every launch
     fam = {}
     if not args.no_trace:
@@ -281,6 +297,7 @@ def main() -> int:
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "graph_replay": {"ms_per_step": round(graph_ms, 5), "value": round(c.B * c.K / (graph_ms / 1e3), 1)},
         "U_mean": round(float(np.mean(U)), 2), "rho": round(c.K * c.L / float(np.mean(U)), 3),
     }
     if fam:
