@@ -150,15 +150,17 @@ def cpu_baseline(c, W, I, seconds: float):
                       f"re-encoded per list, item set re-encoded per occurrence) in {dt:.1f} s on {cpu}"}
 
 
+# sources that define the module kernel, its launch shapes and the arguments it is given
+TRAFFIC_SOURCES = ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp")
+
+
 def sources_digest() -> str:
-    """sha256 over the HIP library sources and headers (identifies the kernels a profile saw)."""
+    """sha256 over the sources of the module kernel (identifies the kernel a traffic profile saw)."""
     import hashlib
     h = hashlib.sha256()
-    for d in (os.path.join(ROOT, "paper_2603_02565_amd", "csrc"), os.path.join(ROOT, "include")):
-        for f in sorted(os.listdir(d)):
-            if f.endswith((".hip", ".cpp", ".h")):
-                with open(os.path.join(d, f), "rb") as fh:
-                    h.update(f.encode() + b"\0" + fh.read())
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2603_02565_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
@@ -203,6 +205,7 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the traced pass (for profiler runs)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph-replay timing (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB copy (to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -261,20 +264,22 @@ def main() -> int:
     asm_bytes = assemble_bytes(c, U)
 
     # ---- the same pass captured once as a HIP graph and replayed K times
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        step()
-    for _ in range(args.warmup):
-        graph.replay()
-    torch.cuda.synchronize()
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    for _ in range(args.steps):
-        graph.replay()
-    g1.record(stream)
-    torch.cuda.synchronize()
-    graph_ms = g0.elapsed_time(g1) / args.steps
-    del graph
+    graph_ms = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = g0.elapsed_time(g1) / args.steps
+        del graph
 
     # ---- kernel-timing region: the same steps with HIP events around every launch
     fam = {}
@@ -297,7 +302,8 @@ def main() -> int:
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
-        "graph_replay": {"ms_per_step": round(graph_ms, 5), "value": round(c.B * c.K / (graph_ms / 1e3), 1)},
+        "graph_replay": None if graph_ms is None else {"ms_per_step": round(graph_ms, 5),
+                                                       "value": round(c.B * c.K / (graph_ms / 1e3), 1)},
         "U_mean": round(float(np.mean(U)), 2), "rho": round(c.K * c.L / float(np.mean(U)), 3),
     }
     if fam:
