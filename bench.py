@@ -100,6 +100,18 @@ def family_flops(c, U, fam_names):
     return out
 
 
+def naive_flops(c, U):
+    """Algorithmic flops of the candidate-factorised evaluator (context encoded once per list,
+    distinct-element set encoded once per element occurrence; SeqEnc, cross-sequence module as
+    in the joint pass)."""
+    d, F, n, B, T, K, L, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L, c.L + 1
+    ctx = sum(module_parts(d, F, n, T, 1, T)) + 4.0 * n * T * d * d
+    items = [n * (4.0 * u * u * d + 4.0 * u * T * d) + n * (12.0 * d * d + 4.0 * d * F) * u for u in U]
+    seq = sum(module_parts(d, F, n, B * K * S, B * K, S, True))
+    cross = sum(module_parts(d, F, n, B * K, B, K))
+    return B * K * ctx + K * L * sum(items) + seq + cross
+
+
 def cpu_baseline(c, W, I, seconds: float):
     """The float64 oracle, in its candidate-factorised order, on this host for a bounded time.
 
@@ -206,6 +218,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the traced pass (for profiler runs)")
     ap.add_argument("--no-graph", action="store_true", help="skip the graph-replay timing (for profiler runs)")
+    ap.add_argument("--no-naive", action="store_true",
+                    help="skip timing the candidate-factorised evaluator (no reuse) on the GPU")
+    ap.add_argument("--naive-steps", type=int, default=5)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB copy (to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -343,6 +358,34 @@ def main() -> int:
         out["mfma_util_matrix_stages"] = round(mm_flops / (mm_ms / 1e3) / 1e12 / peak, 4)
         out["kernel_ms_per_step"] = round(sum(v[0] for v in fam.values()) / args.steps, 5)
         out["stages"] = stages
+    if not args.no_naive:
+        # the same network with every reuse taken out (fe_evaluate_naive), same inputs, same GPU
+        ev.allocate_naive(c.B, c.T, c.M, c.K, c.L, token_ids=ids is not None)
+
+        def naive_step():
+            ev.run_naive(x=x, ctx_ids=ids, pool=pool, lists=lists)
+
+        naive_step()
+        torch.cuda.synchronize()
+        n0, n1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n0.record(stream)
+        for _ in range(args.naive_steps):
+            naive_step()
+        n1.record(stream)
+        torch.cuda.synchronize()
+        naive_ms = n0.elapsed_time(n1) / args.naive_steps
+        same = bool(torch.equal(ev.naive_buffers["best"], bufs["best"]))
+        jf = sum(family_flops(c, U, {"layer", "post", "attention", "gemm"}).values())
+        nf = naive_flops(c, U)
+        out["naive_gpu"] = {
+            "ms_per_step": round(naive_ms, 4), "value": round(c.B * c.K / (naive_ms / 1e3), 1), "unit": "lists/s",
+            "steps": args.naive_steps, "t_joint_over_t_ind": round(ms_per_step / naive_ms, 6),
+            "flops_joint_over_ind": round(jf / nf, 6), "one_over_rho": round(float(np.mean(U)) / (c.K * c.L), 4),
+            "tflops": round(nf / (naive_ms / 1e3) / 1e12, 1), "same_selection": same,
+            "what": "context encoded once per list, distinct-element set once per element occurrence, "
+                    "each list assembled from its own encodings (fe_evaluate_naive)"}
+        ev.naive_buffers = None
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(c, W, I, args.cpu_seconds)
     ev.close()

@@ -206,6 +206,33 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
 fe_status fe_score_select(const fe_model* m, int B, int K, const float* Cp, float* scores, int32_t* best,
                           void* stream);
 
+/*
+ * Baseline, outside the joint pass: the candidate-factorised evaluator (E^ind,
+ * Section 3) of the same network on the GPU, with every reuse taken out.  The
+ * context is encoded once per list (B*K context encodings, each list with its
+ * own key/value cache) and the distinct-element set once per element
+ * occurrence (L set encodings per list, against that list's cache), the cost
+ * structure of Appendix A.3 extended to the context side.  Each list is then
+ * assembled from its own encodings; SeqEnc, the cross-sequence module and the
+ * head run as in the joint pass.  QKV-Cache reuses exact results (Section
+ * 4.2), so the outputs equal those of the five calls; only the work differs.
+ *
+ * Arguments are those of the five calls: x [B][T][d] act or ctx_ids [B][T]
+ * int32 (exactly one), pool [B][M][d] act or NULL on a vocabulary model,
+ * lists [B][K][L] int32.  Outputs Cp [B][K][d] fp32, scores [B][K] fp32,
+ * best [B] int32 (device, caller-owned).  ws is a device workspace of at least
+ * fe_naive_workspace_size bytes (token_ids = 1 when ctx_ids will be given);
+ * it holds the joint pass's workspace for B*K requests, per-list copies of
+ * the inputs and per-list caches, so B*K must pass the same envelope and
+ * int32 limits as a batch of B*K requests (FE_EINVAL / FE_EUNSUPPORTED
+ * otherwise).  Asynchronous on `stream`; errors as for the five calls.
+ */
+fe_status fe_naive_workspace_size(const fe_model* m, int B, int T, int M, int K, int L, int token_ids,
+                                  size_t* bytes);
+fe_status fe_evaluate_naive(const fe_model* m, int B, int T, int M, int K, int L, const void* x,
+                            const int32_t* ctx_ids, const void* pool, const int32_t* lists, float* Cp,
+                            float* scores, int32_t* best, void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -343,6 +343,35 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
   return w;
 }
 
+// Workspace of the candidate-factorised evaluator: the joint pass's workspace at B*K requests,
+// then the per-list copies of the inputs, the per-list key/value caches, the per-list item
+// encodings and the assembled sequences.
+struct NaiveWs {
+  size_t inner, inner_bytes, xin, kv, pool, lists, uniq, n_uniq, slot, H, slot_k, seq, total;
+};
+
+NaiveWs naive_layout(const fe_model* m, long long B, long long T, long long M, long long K, long long L, bool ids,
+                     bool own_pool) {
+  const long long BK = B * K, d = m->cfg.d, n = m->cfg.n_layers, Ucap = std::min(M, K * L);
+  const size_t e = m->bf16 ? 2 : 4;
+  NaiveWs w{};
+  Bump b{0};
+  w.inner_bytes = layout(m, BK, T, M, K, L).total;
+  w.inner = b.take(w.inner_bytes);
+  w.xin = b.take(ids ? BK * T * 4 : BK * T * d * e);
+  w.kv = b.take(n * 2 * BK * T * d * e);
+  w.pool = own_pool ? b.take(BK * M * d * e) : 0;
+  w.lists = b.take(BK * K * L * 4);
+  w.uniq = b.take(BK * Ucap * 4);
+  w.n_uniq = b.take(BK * 4);
+  w.slot = b.take(BK * K * L * 4);
+  w.H = b.take(BK * Ucap * d * e);
+  w.slot_k = b.take(BK * L * 4);
+  w.seq = b.take(B * K * (L + 1) * d * e);
+  w.total = (b.at + 255) & ~size_t(255);
+  return w;
+}
+
 template <typename T> T* at(void* base, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(base) + off); }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -848,6 +877,77 @@ fe_status fe_score_select(const fe_model* m, int B, int K, const float* Cp, floa
   if (!aligned16(Cp)) return fail(FE_EINVAL, "Cp must be 16-byte aligned");
   FE_LAUNCH(F_SCORE, static_cast<hipStream_t>(stream), launch_score_select(Cp, B, K, m->cfg.d, m->head_w, m->head_b, scores, best, static_cast<hipStream_t>(stream)));
   return FE_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Candidate-factorised evaluator on the GPU (a baseline for the joint pass)
+// ------------------------------------------------------------------------------------------
+fe_status fe_naive_workspace_size(const fe_model* m, int B, int T, int M, int K, int L, int token_ids, size_t* bytes) {
+  fe_status st = check_dims(m, B, T, M, K, L);
+  if (st != FE_OK) return st;
+  st = check_dims(m, (long long)B * K, T, M, K, L);
+  if (st != FE_OK) return st;
+  if (!bytes) return fail(FE_EINVAL, "bytes is NULL");
+  *bytes = naive_layout(m, B, T, M, K, L, token_ids != 0, true).total;
+  return FE_OK;
+}
+
+fe_status fe_evaluate_naive(const fe_model* m, int B, int T, int M, int K, int L, const void* x, const int32_t* ctx_ids,
+                            const void* pool, const int32_t* lists, float* Cp, float* scores, int32_t* best, void* ws,
+                            size_t ws_bytes, void* stream) {
+  fe_status st = check_dims(m, B, T, M, K, L);
+  if (st != FE_OK) return st;
+  const long long BKl = (long long)B * K;
+  st = check_dims(m, BKl, T, M, K, L);
+  if (st != FE_OK) return st;
+  if ((x == nullptr) == (ctx_ids == nullptr)) return fail(FE_EINVAL, "give exactly one of x and ctx_ids");
+  if (ctx_ids && !m->emb) return fail(FE_EINVAL, "ctx_ids given but the model has no vocabulary");
+  if (!pool && !m->emb) return fail(FE_EINVAL, "pool is NULL and the model has no vocabulary");
+  if (!pool && M != m->cfg.vocab) return fail(FE_EINVAL, "token-id items need M == vocab (%d)", m->cfg.vocab);
+  if (!lists || !Cp || !scores || !best || !ws) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(x) || !aligned16(ctx_ids) || !aligned16(pool) || !aligned16(lists) || !aligned16(Cp) ||
+      !aligned16(ws))
+    return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const NaiveWs w = naive_layout(m, B, T, M, K, L, ctx_ids != nullptr, true);
+  if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int BK = (int)BKl, d = m->cfg.d, Ucap = std::min(M, K * L);
+  const size_t e = m->bf16 ? 2 : 4;
+  void* inner = at<char>(ws, w.inner);
+  // the context once per list: request b's context rows copied to each of its K lists
+  void* xin = at<char>(ws, w.xin);
+  if (ctx_ids) FE_LAUNCH(F_GATHER, s, launch_repeat_blocks(ctx_ids, xin, (long long)T * 4, B, K, s));
+  else FE_LAUNCH(F_GATHER, s, launch_repeat_blocks(x, xin, (long long)T * d * e, B, K, s));
+  void* kv = at<char>(ws, w.kv);
+  st = fe_encode_context(m, BK, T, ctx_ids ? nullptr : xin, ctx_ids ? at<int32_t>(ws, w.xin) : nullptr, kv, inner,
+                         w.inner_bytes, stream);
+  if (st != FE_OK) return st;
+  // every list sees its request's pool and the request's K lists (so the distinct set is U(z))
+  const void* pool_k = nullptr;
+  if (pool) {
+    FE_LAUNCH(F_GATHER, s, launch_repeat_blocks(pool, at<char>(ws, w.pool), (long long)M * d * e, B, K, s));
+    pool_k = at<char>(ws, w.pool);
+  }
+  int32_t* lists_k = at<int32_t>(ws, w.lists);
+  FE_LAUNCH(F_GATHER, s, launch_repeat_blocks(lists, lists_k, (long long)K * L * 4, B, K, s));
+  // the distinct-element set encoded once per element occurrence: L encodings per list, each
+  // against that list's own context cache (every one of them yields the same rows)
+  int32_t* slot_all = at<int32_t>(ws, w.slot);
+  void* H = at<char>(ws, w.H);
+  for (int j = 0; j < L; ++j) {
+    st = fe_encode_items(m, BK, M, pool_k, lists_k, K, L, kv, T, at<int32_t>(ws, w.uniq), at<int32_t>(ws, w.n_uniq),
+                         slot_all, H, inner, w.inner_bytes, stream);
+    if (st != FE_OK) return st;
+  }
+  // each list assembled from its own encodings, then SeqEnc, cross-sequence module and head
+  int32_t* slot_k = at<int32_t>(ws, w.slot_k);
+  FE_LAUNCH(F_GATHER, s, launch_take_list_slots(slot_all, slot_k, BK, K, L, s));
+  void* seq = at<char>(ws, w.seq);
+  st = fe_assemble(m, BK, 1, L, Ucap, slot_k, H, seq, stream);
+  if (st != FE_OK) return st;
+  st = fe_cross_sequence(m, B, K, L, seq, Cp, inner, w.inner_bytes, stream);
+  if (st != FE_OK) return st;
+  return fe_score_select(m, B, K, Cp, scores, best, stream);
 }
 
 }  // extern "C"

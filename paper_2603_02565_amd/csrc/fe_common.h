@@ -194,6 +194,10 @@ hipError_t launch_layernorm_masked(const void* X, int x_f32, long long x_rs, int
                                    const float* b, void* Y, int y_f32, long long y_rs, const int32_t* nvalid,
                                    int rpb, bool bf16_model, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s);
+// dst block b*reps + r = src block b (r < reps); block_bytes a multiple of 4
+hipError_t launch_repeat_blocks(const void* src, void* dst, long long block_bytes, int nblk, int reps, hipStream_t s);
+// slot_k[q][j] = slot_all[q][q % K][j] (q < BK; slot_all [BK][K][L], slot_k [BK][L])
+hipError_t launch_take_list_slots(const int32_t* slot_all, int32_t* slot_k, int BK, int K, int L, hipStream_t s);
 hipError_t launch_dedup(const int32_t* lists, int B, int KL, int M, int U_cap, int32_t* uniq,
                         int32_t* n_uniq, int32_t* slot, int32_t* status, hipStream_t s);
 hipError_t launch_gather_rows(const void* table, long long table_bs, int n_rows_table, const int32_t* idx,

@@ -207,6 +207,25 @@ __global__ void k_fill_i32(int32_t* p, int n, int32_t v) {
   if (i < n) p[i] = v;
 }
 
+// dst block (b * reps + r) = src block b, blocks of `words` 32-bit words (grid-stride; r < reps)
+__global__ void k_repeat_blocks(const uint32_t* src, uint32_t* dst, long long words, int nblk, int reps) {
+  const long long total = (long long)nblk * reps * words;
+  for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < total; e += (long long)gridDim.x * 256) {
+    const long long blk = e / words, w = e - blk * words;
+    dst[e] = src[(blk / reps) * words + w];
+  }
+}
+
+// slot_k[q][j] = slot_all[q][q % K][j] for q < BK: list (q % K)'s ranks out of the slot map of all K
+// lists that request q saw
+__global__ void k_take_list_slots(const int32_t* slot_all, int32_t* slot_k, int BK, int K, int L) {
+  const long long n = (long long)BK * L;
+  for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < n; e += (long long)gridDim.x * 256) {
+    const long long q = e / L, j = e - q * L;
+    slot_k[e] = slot_all[(q * K + q % K) * L + j];
+  }
+}
+
 int grid_for(long long work) {
   long long g = (work + 255) / 256;
   if (g > 65536) g = 65536;
@@ -218,6 +237,21 @@ int grid_for(long long work) {
 hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_fill_i32, dim3((n + 255) / 256), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_repeat_blocks(const void* src, void* dst, long long block_bytes, int nblk, int reps, hipStream_t s) {
+  if (block_bytes % 4 != 0) return hipErrorInvalidValue;
+  const long long words = block_bytes / 4;
+  if (words == 0 || nblk <= 0 || reps <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_repeat_blocks, dim3(grid_for((long long)nblk * reps * words)), dim3(256), 0, s,
+                     static_cast<const uint32_t*>(src), static_cast<uint32_t*>(dst), words, nblk, reps);
+  return hipGetLastError();
+}
+
+hipError_t launch_take_list_slots(const int32_t* slot_all, int32_t* slot_k, int BK, int K, int L, hipStream_t s) {
+  if (BK <= 0 || L <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_take_list_slots, dim3(grid_for((long long)BK * L)), dim3(256), 0, s, slot_all, slot_k, BK, K, L);
   return hipGetLastError();
 }
 

@@ -22,7 +22,8 @@ FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
 
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
-            "fe_score_select", "fe_trace_enable", "fe_trace_read", "fe_trace_family")
+            "fe_score_select", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
+            "fe_trace_family")
 FE_TRACE_FAMILIES = 11
 
 
@@ -64,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_assemble": (S, [P, I, I, I, I, P, P, P, P]),
         "fe_cross_sequence": (S, [P, I, I, I, P, P, P, Z, P]),
         "fe_score_select": (S, [P, I, I, P, P, P, P]),
+        "fe_naive_workspace_size": (S, [P, I, I, I, I, I, I, ctypes.POINTER(Z)]),
+        "fe_evaluate_naive": (S, [P, I, I, I, I, I, P, P, P, P, P, P, P, P, Z, P]),
         "fe_trace_enable": (S, [I]),
         "fe_trace_read": (S, [P, P]),
         "fe_trace_family": (ctypes.c_char_p, [I]),
@@ -190,6 +193,20 @@ def fe_score_select(model: int, B: int, K: int, Cp, scores, best, stream=None) -
            "fe_score_select")
 
 
+def fe_naive_workspace_size(model: int, B: int, T: int, M: int, K: int, L: int, token_ids: bool) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().fe_naive_workspace_size(model, B, T, M, K, L, 1 if token_ids else 0, ctypes.byref(n)),
+           "fe_naive_workspace_size")
+    return n.value
+
+
+def fe_evaluate_naive(model: int, B: int, T: int, M: int, K: int, L: int, x, ctx_ids, pool, lists, Cp, scores, best,
+                      ws, stream=None) -> None:
+    _check(load_library().fe_evaluate_naive(model, B, T, M, K, L, _ptr(x), _ptr(ctx_ids), _ptr(pool), _ptr(lists),
+                                            _ptr(Cp), _ptr(scores), _ptr(best), _ptr(ws),
+                                            ws.numel() * ws.element_size(), _stream(stream)), "fe_evaluate_naive")
+
+
 def fe_trace_enable(on: bool) -> None:
     _check(load_library().fe_trace_enable(1 if on else 0), "fe_trace_enable")
 
@@ -224,6 +241,7 @@ class Evaluator:
         self.act = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.handle = fe_model_create(self.cfg, pack_params(params, n_layers, vocab))
         self.buffers = None
+        self.naive_buffers = None
 
     def close(self) -> None:
         if self.handle:
@@ -269,4 +287,26 @@ class Evaluator:
         fe_assemble(h, B, K, L, b["U_cap"], b["slot"], b["H"], b["seq"], stream)
         fe_cross_sequence(h, B, K, L, b["seq"], b["Cp"], b["ws"], stream)
         fe_score_select(h, B, K, b["Cp"], b["scores"], b["best"], stream)
+        return b
+
+    def allocate_naive(self, B: int, T: int, M: int, K: int, L: int, token_ids: bool) -> Dict:
+        """Outputs and workspace of the candidate-factorised baseline (fe_evaluate_naive)."""
+        import torch
+        dev = torch.device("cuda", torch.cuda.current_device())
+        ws_bytes = fe_naive_workspace_size(self.handle, B, T, M, K, L, token_ids)
+        self.naive_buffers = dict(
+            shape=(B, T, M, K, L),
+            Cp=torch.empty((B, K, self.d), dtype=torch.float32, device=dev),
+            scores=torch.empty((B, K), dtype=torch.float32, device=dev),
+            best=torch.empty((B,), dtype=torch.int32, device=dev),
+            ws=torch.empty((ws_bytes,), dtype=torch.uint8, device=dev),
+        )
+        return self.naive_buffers
+
+    def run_naive(self, x=None, ctx_ids=None, pool=None, lists=None, stream=None) -> Dict:
+        """Enqueue the candidate-factorised evaluator (no reuse) on resident device tensors."""
+        b = self.naive_buffers
+        B, T, M, K, L = b["shape"]
+        fe_evaluate_naive(self.handle, B, T, M, K, L, x, ctx_ids, pool, lists, b["Cp"], b["scores"], b["best"],
+                          b["ws"], stream)
         return b
