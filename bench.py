@@ -221,6 +221,8 @@ def main() -> int:
     ap.add_argument("--no-naive", action="store_true",
                     help="skip timing the candidate-factorised evaluator (no reuse) on the GPU")
     ap.add_argument("--naive-steps", type=int, default=5)
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip timing the pass without cross-sequence interaction (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB copy (to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -278,6 +280,32 @@ def main() -> int:
     U = bufs["n_uniq"].cpu().numpy().tolist()
     asm_bytes = assemble_bytes(c, U)
 
+    # ---- the pass without cross-sequence interaction (SeqEnc output scored directly)
+    no_cross_ms = None
+    C_ind = torch.empty((c.B, c.K, c.d), dtype=torch.float32, device=dev)
+
+    def step_no_cross():
+        b, h = bufs, ev.handle
+        fe.fe_encode_context(h, c.B, c.T, x, ids, b["kv"], b["ws"])
+        fe.fe_encode_items(h, c.B, c.M, pool, lists, c.K, c.L, b["kv"], c.T, b["uniq"], b["n_uniq"], b["slot"], b["H"],
+                           b["ws"])
+        fe.fe_assemble(h, c.B, c.K, c.L, b["U_cap"], b["slot"], b["H"], b["seq"])
+        fe.fe_encode_sequences(h, c.B, c.K, c.L, b["seq"], C_ind, b["ws"])
+        fe.fe_score_select(h, c.B, c.K, C_ind, b["scores"], b["best"])
+
+    if not args.no_variants:
+        for _ in range(args.warmup):
+            step_no_cross()
+        v0, v1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        v0.record(stream)
+        for _ in range(args.steps):
+            step_no_cross()
+        v1.record(stream)
+        torch.cuda.synchronize()
+        no_cross_ms = v0.elapsed_time(v1) / args.steps
+        step()                 # leave the full pass's outputs in the buffers
+        torch.cuda.synchronize()
+
     # ---- the same pass captured once as a HIP graph and replayed K times
     graph_ms = None
     if not args.no_graph:
@@ -317,6 +345,8 @@ def main() -> int:
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "without_cross_sequence": None if no_cross_ms is None else {
+            "ms_per_step": round(no_cross_ms, 5), "value": round(c.B * c.K / (no_cross_ms / 1e3), 1)},
         "graph_replay": None if graph_ms is None else {"ms_per_step": round(graph_ms, 5),
                                                        "value": round(c.B * c.K / (graph_ms / 1e3), 1)},
         "U_mean": round(float(np.mean(U)), 2), "rho": round(c.K * c.L / float(np.mean(U)), 3),

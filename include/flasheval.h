@@ -207,6 +207,33 @@ fe_status fe_score_select(const fe_model* m, int B, int K, const float* Cp, floa
                           void* stream);
 
 /*
+ * Section 4.4 variant without cross-sequence interaction (the "- CrossSeq"
+ * ablation of Appendix B.4): SeqEnc only, C[b][k] = c_k, the final-LayerNorm
+ * [CLS] row of list k, so every list is scored on its own representation
+ * (pass C to fe_score_select or fe_score_objectives in place of Cp).  seq
+ * [B][K][L+1][d] act in, C [B][K][d] fp32 out; ws as for fe_cross_sequence.
+ */
+fe_status fe_encode_sequences(const fe_model* m, int B, int K, int L, const void* seq, float* C, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
+ * Section 4.4, multi-objective form: n_obj task-specific linear heads on the
+ * shared C'_k and a fusion of their predictions.  The paper leaves the fusion
+ * open; here it is the weighted sum with caller weights:
+ *   obj_scores[b][k][t] = Cp[b][k] . head_w[t] + head_b[t]          (fp32)
+ *   scores[b][k]        = sum_t fuse_w[t] * obj_scores[b][k][t]     (t = 0, 1, ...)
+ *   best[b]             = smallest k with the largest fused score (NaN skipped,
+ *                         -1 if all NaN), as in fe_score_select.
+ * head_w [n_obj][d], head_b [n_obj], fuse_w [n_obj] are caller-owned fp32
+ * device arrays (they are not model parameters); 1 <= n_obj <= 8
+ * (FE_EUNSUPPORTED otherwise).  Cp [B][K][d] fp32 (or C of
+ * fe_encode_sequences), obj_scores [B][K][n_obj], scores [B][K], best [B].
+ */
+fe_status fe_score_objectives(const fe_model* m, int B, int K, const float* Cp, int n_obj, const float* head_w,
+                              const float* head_b, const float* fuse_w, float* obj_scores, float* scores,
+                              int32_t* best, void* stream);
+
+/*
  * Baseline, outside the joint pass: the candidate-factorised evaluator (E^ind,
  * Section 3) of the same network on the GPU, with every reuse taken out.  The
  * context is encoded once per list (B*K context encodings, each list with its

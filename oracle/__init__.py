@@ -7,6 +7,7 @@ with the HIP library.
 from .evaluator import (  # noqa: F401
     LN_EPS, layer_norm, softmax_rows, attention, self_attention_block, ffn, encoder_block,
     encoder_stack, context_rows, encode_context, distinct_items, item_rows, encode_items,
-    assemble_one, encode_sequence, cross_sequence, score, select, evaluate_naive, evaluate_cached,
+    assemble_one, encode_sequence, cross_sequence, score, score_objectives, select, evaluate_naive,
+    evaluate_cached,
 )
 from .brute import evaluate_brute  # noqa: F401

@@ -207,6 +207,15 @@ def score(W: Params, Cp: np.ndarray) -> np.ndarray:
     return Cp @ _f64(W["head.w"]) + _f64(W["head.b"])[0]
 
 
+def score_objectives(Cp: np.ndarray, head_w: np.ndarray, head_b: np.ndarray,
+                     fuse_w: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Multi-objective head (Section 4.4): task heads s^t_k = C'_k . w_t + b_t on the shared C'_k,
+    fused into s_k = sum_t alpha_t s^t_k.  The paper leaves the fusion module open; this reading
+    is a weighted sum with given weights.  Returns (per-task scores [K][n_obj], fused [K])."""
+    obj = Cp @ _f64(head_w).T + _f64(head_b)
+    return obj, obj @ _f64(fuse_w)
+
+
 def select(s: np.ndarray) -> int:
     """argmax_k s_k (eq. (1)); smallest index among ties; NaN never selected; all NaN -> -1."""
     best, best_v = -1, None
@@ -227,7 +236,7 @@ def _requests(cfg, requests: Optional[Sequence[int]]) -> List[int]:
 
 
 def evaluate_naive(cfg, W: Params, inp: Dict, requests: Optional[Sequence[int]] = None,
-                   lists_limit: Optional[int] = None) -> Dict[int, Dict[str, np.ndarray]]:
+                   lists_limit: Optional[int] = None, cross_seq: bool = True) -> Dict[int, Dict[str, np.ndarray]]:
     """The oracle: candidate-factorised recomputation of the joint network.
 
     For every list k the context is encoded again; for every occurrence
@@ -235,6 +244,9 @@ def evaluate_naive(cfg, W: Params, inp: Dict, requests: Optional[Sequence[int]] 
     lists[k][j] is taken from it.  Only the cross-sequence module, which acts
     on all K lists at once, runs once per request.  `lists_limit` stops after
     that many lists (used to time a bounded sample; scores are then absent).
+    `cross_seq=False` is the variant without cross-sequence interaction
+    (the "- CrossSeq" ablation of Appendix B.4): C' = c, each list scored on
+    its own representation.
     """
     out = {}
     for b in _requests(cfg, requests):
@@ -252,7 +264,7 @@ def evaluate_naive(cfg, W: Params, inp: Dict, requests: Optional[Sequence[int]] 
             c[k] = encode_sequence(cfg, W, assemble_one(W, rows))
         res = {"c": c}
         if n_lists == K:
-            Cp = cross_sequence(cfg, W, c)
+            Cp = cross_sequence(cfg, W, c) if cross_seq else c
             s = score(W, Cp)
             res.update(Cp=Cp, scores=s, best=select(s))
         out[b] = res
@@ -260,11 +272,12 @@ def evaluate_naive(cfg, W: Params, inp: Dict, requests: Optional[Sequence[int]] 
 
 
 def evaluate_cached(cfg, W: Params, inp: Dict, requests: Optional[Sequence[int]] = None,
-                    stages: bool = False) -> Dict[int, Dict[str, np.ndarray]]:
+                    stages: bool = False, cross_seq: bool = True) -> Dict[int, Dict[str, np.ndarray]]:
     """The same network in the joint pass's order: context and item set encoded once.
 
     With `stages=True` every intermediate is returned too: kv (list of
-    (K_l, V_l)), uniq, slot, H (U x d), seq (K x (L+1) x d).
+    (K_l, V_l)), uniq, slot, H (U x d), seq (K x (L+1) x d).  `cross_seq`
+    as in `evaluate_naive`.
     """
     out = {}
     for b in _requests(cfg, requests):
@@ -275,7 +288,7 @@ def evaluate_cached(cfg, W: Params, inp: Dict, requests: Optional[Sequence[int]]
         H = encode_items(cfg, W, item_rows(cfg, W, inp, b, uniq), kv)
         seq = np.stack([assemble_one(W, H[slot[k]]) for k in range(K)])
         c = np.stack([encode_sequence(cfg, W, seq[k]) for k in range(K)])
-        Cp = cross_sequence(cfg, W, c)
+        Cp = cross_sequence(cfg, W, c) if cross_seq else c
         s = score(W, Cp)
         res = {"c": c, "Cp": Cp, "scores": s, "best": select(s)}
         if stages:

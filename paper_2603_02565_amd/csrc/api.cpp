@@ -499,6 +499,19 @@ fe_status run_module(const fe_model* m, const std::vector<EncW>& ws, int ngroups
   return FE_OK;
 }
 
+// SeqEnc over every list of the batch: c_k = final LayerNorm of each list's [CLS] row (row 0 of
+// every (L+1)-row group), fp32 [B*K][d]
+fe_status seq_encode(const fe_model* m, int B, int K, int L, const void* seq, float* c, const Bufs& b, hipStream_t s) {
+  const int d = m->cfg.d, S = L + 1;
+  if (module_fits(m, S)) return run_module(m, m->seq, B * K, S, seq, false, m->seq_lnf_g, m->seq_lnf_b, c, true, s);
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    fe_status st = enc_block(m, m->seq[l], B * K, S, l == 0 ? seq : b.X, l > 0, b, nullptr, s);
+    if (st != FE_OK) return st;
+  }
+  FE_LAUNCH(F_LN, s, launch_layernorm(b.X, 1, (long long)S * d, B * K, d, m->seq_lnf_g, m->seq_lnf_b, c, 1, d, m->bf16, s));
+  return FE_OK;
+}
+
 fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s) {
   if (m->bf16) FE_LAUNCH(F_GEMM, s, launch_proj(g, s));
   else FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
@@ -846,20 +859,11 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool bf = m->bf16;
-  const int d = m->cfg.d, S = L + 1;
+  const int d = m->cfg.d;
   Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h)};
-  // c_k = final LayerNorm of each list's [CLS] row (row 0 of every S-row group)
   float* c = at<float>(ws, w.s_c);
-  if (module_fits(m, S)) {
-    st = run_module(m, m->seq, B * K, S, seq, false, m->seq_lnf_g, m->seq_lnf_b, c, true, s);
-    if (st != FE_OK) return st;
-  } else {
-    for (int l = 0; l < m->cfg.n_layers; ++l) {
-      st = enc_block(m, m->seq[l], B * K, S, l == 0 ? seq : b.X, l > 0, b, nullptr, s);
-      if (st != FE_OK) return st;
-    }
-    FE_LAUNCH(F_LN, s, launch_layernorm(b.X, 1, (long long)S * d, B * K, d, m->seq_lnf_g, m->seq_lnf_b, c, 1, d, bf, s));
-  }
+  st = seq_encode(m, B, K, L, seq, c, b, s);
+  if (st != FE_OK) return st;
   if (module_fits(m, K)) return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
   Bufs bc{c, b.qkv, b.O, b.Hf};
   for (int l = 0; l < m->cfg.n_layers; ++l) {
@@ -867,6 +871,33 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
     if (st != FE_OK) return st;
   }
   FE_LAUNCH(F_LN, s, launch_layernorm(c, 1, d, B * K, d, m->cross_lnf_g, m->cross_lnf_b, Cp, 1, d, bf, s));
+  return FE_OK;
+}
+
+fe_status fe_encode_sequences(const fe_model* m, int B, int K, int L, const void* seq, float* C, void* ws,
+                              size_t ws_bytes, void* stream) {
+  fe_status st = check_dims(m, B, 1, 1, K, L);
+  if (st != FE_OK) return st;
+  if (!seq || !C || !ws) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(seq) || !aligned16(C) || !aligned16(ws)) return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const Ws w = layout(m, B, 1, 1, K, L);
+  if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
+  Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h)};
+  return seq_encode(m, B, K, L, seq, C, b, static_cast<hipStream_t>(stream));
+}
+
+fe_status fe_score_objectives(const fe_model* m, int B, int K, const float* Cp, int n_obj, const float* head_w,
+                              const float* head_b, const float* fuse_w, float* obj_scores, float* scores, int32_t* best,
+                              void* stream) {
+  fe_status st = check_dims(m, B, 1, 1, K, 1);
+  if (st != FE_OK) return st;
+  if (n_obj < 1 || n_obj > FE_MAX_OBJECTIVES) return fail(FE_EUNSUPPORTED, "n_obj=%d outside [1, %d]", n_obj, FE_MAX_OBJECTIVES);
+  if (!Cp || !head_w || !head_b || !fuse_w || !obj_scores || !scores || !best)
+    return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(Cp) || !aligned16(head_w)) return fail(FE_EINVAL, "Cp and head_w must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  FE_LAUNCH(F_SCORE, s, launch_score_objectives(Cp, B, K, m->cfg.d, n_obj, head_w, head_b, fuse_w, obj_scores, scores,
+                                                best, s));
   return FE_OK;
 }
 

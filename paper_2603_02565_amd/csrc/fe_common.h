@@ -167,6 +167,7 @@ struct EncW {
   const float *ln2g, *ln2b; const void* w1; const float* b1; const void* w2; const float* b2;
 };
 constexpr int FE_MAX_LAYERS = 8;
+constexpr int FE_MAX_OBJECTIVES = 8;   // task heads of fe_score_objectives
 
 // A whole encoder module over short groups (bf16 models): n_layers pre-LN blocks over groups of
 // S consecutive rows (attention inside a group), then the module's final LayerNorm.  Y receives
@@ -205,5 +206,7 @@ hipError_t launch_gather_rows(const void* table, long long table_bs, int n_rows_
                               int32_t* status, int status_bit, bool bf16_model, hipStream_t s);
 hipError_t launch_assemble(const int32_t* slot, const void* H, int B, int K, int L, int U_cap, int d,
                            const void* cls, const void* pos, void* seq, bool bf16_model, hipStream_t s);
+hipError_t launch_score_objectives(const float* Cp, int B, int K, int d, int nobj, const float* W, const float* bias,
+                                   const float* alpha, float* obj, float* fused, int32_t* best, hipStream_t s);
 hipError_t launch_score_select(const float* Cp, int B, int K, int d, const float* w, const float* bias,
                                float* scores, int32_t* best, hipStream_t s);

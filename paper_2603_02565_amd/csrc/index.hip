@@ -132,6 +132,35 @@ __global__ __launch_bounds__(256) void k_assemble(const int32_t* __restrict__ sl
   }
 }
 
+// Smallest index of the largest non-NaN value of s_score[0..K), -1 if every value is NaN; every
+// thread of the 256-thread block calls it and gets the result.
+FE_DEV int block_select(const float* s_score, int K, float* s_val, int* s_idx) {
+  const int tid = threadIdx.x;
+  float bv = 0.f;
+  int bi = -1;
+  for (int k = tid; k < K; k += 256) {
+    const float v = s_score[k];
+    if (v != v) continue;
+    if (bi < 0 || v > bv) { bv = v; bi = k; }
+  }
+  s_val[tid] = bv;
+  s_idx[tid] = bi;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if (tid < off) {
+      const float ov = s_val[tid + off];
+      const int oi = s_idx[tid + off];
+      const int mi = s_idx[tid];
+      if (oi >= 0 && (mi < 0 || ov > s_val[tid] || (ov == s_val[tid] && oi < mi))) {
+        s_val[tid] = ov;
+        s_idx[tid] = oi;
+      }
+    }
+    __syncthreads();
+  }
+  return s_idx[0];
+}
+
 // ------------------------------------------------------------------------------------------
 // Score head and selection: one workgroup per request (XCD-contiguous, like the cross-sequence
 // module that wrote Cp).  A group of LPR = min(16, D/4) lanes forms one dot product (lane l sums
@@ -177,29 +206,56 @@ __global__ __launch_bounds__(256) void k_score_select(const float* __restrict__ 
     }
   }
   __syncthreads();
-  float bv = 0.f;
-  int bi = -1;
-  for (int k = tid; k < K; k += 256) {
-    const float v = s_score[k];
-    if (v != v) continue;
-    if (bi < 0 || v > bv) { bv = v; bi = k; }
-  }
-  s_val[tid] = bv;
-  s_idx[tid] = bi;
+  const int bi = block_select(s_score, K, s_val, s_idx);
+  if (tid == 0) best[b] = bi;
+}
+
+// Section 4.4, multi-objective form: NOBJ task heads on the shared C'_k, fused by a weighted sum.
+// One workgroup per request; head weights staged in LDS; each LPR-lane group takes one list at a
+// time, reads C'_k once and forms every head's dot product from it.
+//   obj[b][k][t] = C'_k . W[t] + bias[t];   fused[b][k] = sum_t alpha[t] obj[b][k][t] (t ascending)
+//   best[b] = smallest k with the largest fused score, NaN skipped, -1 if all NaN.
+template <int D>
+__global__ __launch_bounds__(256) void k_score_objectives(const float* __restrict__ Cp, int K, int nobj,
+                                                          const float* __restrict__ W, const float* __restrict__ bias,
+                                                          const float* __restrict__ alpha, float* __restrict__ obj,
+                                                          float* __restrict__ fused, int32_t* __restrict__ best) {
+  constexpr int LPR = D / 4 < 16 ? D / 4 : 16, NV = D / (4 * LPR), NG = 256 / LPR;
+  __shared__ __attribute__((aligned(16))) float s_w[FE_MAX_OBJECTIVES * D];
+  __shared__ float s_val[256];
+  __shared__ int s_idx[256];
+  __shared__ float s_score[4096];
+  const int b = xcd_tile(blockIdx.x, gridDim.x), tid = threadIdx.x, l16 = tid % LPR, grp = tid / LPR;
+  for (int e = tid; e < nobj * D; e += 256) s_w[e] = W[e];
   __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (tid < off) {
-      const float ov = s_val[tid + off];
-      const int oi = s_idx[tid + off];
-      const int mi = s_idx[tid];
-      if (oi >= 0 && (mi < 0 || ov > s_val[tid] || (ov == s_val[tid] && oi < mi))) {
-        s_val[tid] = ov;
-        s_idx[tid] = oi;
+  const float* cb = Cp + (long long)b * K * D;
+  for (int k = grp; k < K; k += NG) {
+    float4 xv[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) xv[i] = *reinterpret_cast<const float4*>(&cb[(long long)k * D + 4 * (l16 + LPR * i)]);
+    float f = 0.f;
+    for (int t = 0; t < nobj; ++t) {
+      const float4* wt = reinterpret_cast<const float4*>(s_w + t * D);
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const float4 wv = wt[l16 + LPR * i];
+        acc += xv[i].x * wv.x + xv[i].y * wv.y + xv[i].z * wv.z + xv[i].w * wv.w;
       }
+#pragma unroll
+      for (int o = 1; o < LPR; o <<= 1) acc += __shfl_xor(acc, o, LPR);
+      const float st = acc + bias[t];
+      if (l16 == 0) obj[((long long)b * K + k) * nobj + t] = st;
+      f = t == 0 ? alpha[0] * st : fmaf(alpha[t], st, f);
     }
-    __syncthreads();
+    if (l16 == 0) {
+      fused[(long long)b * K + k] = f;
+      s_score[k] = f;
+    }
   }
-  if (tid == 0) best[b] = s_idx[0];
+  __syncthreads();
+  const int bi = block_select(s_score, K, s_val, s_idx);
+  if (tid == 0) best[b] = bi;
 }
 
 __global__ void k_fill_i32(int32_t* p, int n, int32_t v) {
@@ -285,6 +341,22 @@ hipError_t launch_assemble(const int32_t* slot, const void* H, int B, int K, int
     hipLaunchKernelGGL(k_assemble<float>, dim3(grid_for(work)), dim3(256), 0, s, slot, static_cast<const float*>(H), B,
                        K, L, U_cap, d, static_cast<const float*>(cls), static_cast<const float*>(pos),
                        static_cast<float*>(seq));
+  return hipGetLastError();
+}
+
+hipError_t launch_score_objectives(const float* Cp, int B, int K, int d, int nobj, const float* W, const float* bias,
+                                   const float* alpha, float* obj, float* fused, int32_t* best, hipStream_t s) {
+  if (nobj < 1 || nobj > FE_MAX_OBJECTIVES || K > 4096) return hipErrorInvalidValue;
+#define FE_OBJ(DD) hipLaunchKernelGGL(k_score_objectives<DD>, dim3(B), dim3(256), 0, s, Cp, K, nobj, W, bias, alpha, obj, fused, best)
+  switch (d) {
+    case 32: FE_OBJ(32); break;
+    case 64: FE_OBJ(64); break;
+    case 128: FE_OBJ(128); break;
+    case 256: FE_OBJ(256); break;
+    case 512: FE_OBJ(512); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef FE_OBJ
   return hipGetLastError();
 }
 

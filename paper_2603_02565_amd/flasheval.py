@@ -22,7 +22,7 @@ FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
 
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
-            "fe_score_select", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
+            "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
             "fe_trace_family")
 FE_TRACE_FAMILIES = 11
 
@@ -65,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_assemble": (S, [P, I, I, I, I, P, P, P, P]),
         "fe_cross_sequence": (S, [P, I, I, I, P, P, P, Z, P]),
         "fe_score_select": (S, [P, I, I, P, P, P, P]),
+        "fe_encode_sequences": (S, [P, I, I, I, P, P, P, Z, P]),
+        "fe_score_objectives": (S, [P, I, I, P, I, P, P, P, P, P, P, P]),
         "fe_naive_workspace_size": (S, [P, I, I, I, I, I, I, ctypes.POINTER(Z)]),
         "fe_evaluate_naive": (S, [P, I, I, I, I, I, P, P, P, P, P, P, P, P, Z, P]),
         "fe_trace_enable": (S, [I]),
@@ -191,6 +193,18 @@ def fe_cross_sequence(model: int, B: int, K: int, L: int, seq, Cp, ws, stream=No
 def fe_score_select(model: int, B: int, K: int, Cp, scores, best, stream=None) -> None:
     _check(load_library().fe_score_select(model, B, K, _ptr(Cp), _ptr(scores), _ptr(best), _stream(stream)),
            "fe_score_select")
+
+
+def fe_encode_sequences(model: int, B: int, K: int, L: int, seq, C, ws, stream=None) -> None:
+    _check(load_library().fe_encode_sequences(model, B, K, L, _ptr(seq), _ptr(C), _ptr(ws),
+                                              ws.numel() * ws.element_size(), _stream(stream)), "fe_encode_sequences")
+
+
+def fe_score_objectives(model: int, B: int, K: int, Cp, n_obj: int, head_w, head_b, fuse_w, obj_scores, scores, best,
+                        stream=None) -> None:
+    _check(load_library().fe_score_objectives(model, B, K, _ptr(Cp), n_obj, _ptr(head_w), _ptr(head_b), _ptr(fuse_w),
+                                              _ptr(obj_scores), _ptr(scores), _ptr(best), _stream(stream)),
+           "fe_score_objectives")
 
 
 def fe_naive_workspace_size(model: int, B: int, T: int, M: int, K: int, L: int, token_ids: bool) -> int:

@@ -355,3 +355,65 @@ def test_golden_reuse_example():
     assert slot.tolist() == g["slot"]
     assert len(uniq) == g["U"]
     assert lists.size / len(uniq) == g["rho"]
+
+
+# ----------------------------------------------------------- head-side variants (Section 4.4)
+
+def test_without_cross_sequence_variant_matches_torch(cfg1_small):
+    """The "- CrossSeq" variant (C' = c) against the pass rebuilt from torch layers without the
+    cross-sequence module, and the naive order against the cached one."""
+    c, W, I = cfg1_small
+    o = oracle.evaluate_cached(c, W, I, requests=[0], cross_seq=False)[0]
+    t = evaluate_torch(c, W, I, 0, cross_seq=False)
+    assert _rel(o["Cp"], t["Cp"]) < 1e-12
+    assert _rel(o["scores"], t["scores"]) < 1e-12
+    n = oracle.evaluate_naive(c, W, I, requests=[0], cross_seq=False)[0]
+    assert _rel(n["scores"], o["scores"]) < 1e-12
+    full = oracle.evaluate_cached(c, W, I, requests=[0])[0]
+    assert np.array_equal(o["Cp"], full["c"])          # C' is SeqEnc's output, untouched
+    assert not np.allclose(o["scores"], full["scores"])  # and the interaction does change scores
+
+
+def test_without_cross_sequence_variant_scores_lists_independently(cfg1_small):
+    """Without the interaction, a list whose items and U(z) stay the same keeps its score bit for
+    bit while the other lists are reordered or replaced by other lists over the same items."""
+    c, W, I = cfg1_small
+    a = oracle.evaluate_cached(c, W, I, requests=[0], cross_seq=False)[0]["scores"]
+    lists = I["lists"].copy()
+    lists[0, [1, 2, 3]] = lists[0, [3, 1, 2]]
+    b = oracle.evaluate_cached(c, W, _with_lists(I, lists), requests=[0], cross_seq=False)[0]["scores"]
+    assert b[0] == a[0] and b[4] == a[4] and b[5] == a[5]
+    assert b[1] == a[3] and b[2] == a[1] and b[3] == a[2]
+
+
+def _objective_heads(d, n_obj, seed=7):
+    rng = np.random.default_rng(seed)
+    return rng.normal(0, 0.05, (n_obj, d)), rng.normal(0, 0.05, n_obj), rng.uniform(-1, 1, n_obj)
+
+
+def test_multi_objective_head_reduces_to_single_head(cfg0):
+    """One task head with fusion weight 1 is the model's own linear head."""
+    c, W, I = cfg0
+    Cp = oracle.evaluate_cached(c, W, I)[0]["Cp"]
+    obj, fused = oracle.score_objectives(Cp, W["head.w"][None], W["head.b"], np.ones(1))
+    ref = oracle.score(W, Cp)
+    assert _rel(obj[:, 0], ref) < 1e-12 and _rel(fused, ref) < 1e-12
+
+
+def test_multi_objective_head_brute_force_and_linearity(cfg0):
+    """Per-task scores by scalar loops; the fused score of linear heads is the single linear head
+    with w = sum_t alpha_t w_t and b = sum_t alpha_t b_t."""
+    c, W, I = cfg0
+    Cp = oracle.evaluate_cached(c, W, I)[0]["Cp"]
+    hw, hb, al = _objective_heads(c.d, 3)
+    obj, fused = oracle.score_objectives(Cp, hw, hb, al)
+    for k in range(Cp.shape[0]):
+        f = 0.0
+        for t in range(3):
+            s = sum(float(Cp[k, i]) * float(hw[t, i]) for i in range(c.d)) + float(hb[t])
+            assert abs(obj[k, t] - s) <= 1e-12 * (1 + abs(s))
+            f += float(al[t]) * s
+        assert abs(fused[k] - f) <= 1e-12 * (1 + abs(f))
+    w_eq, b_eq = al @ hw, al @ hb
+    assert _rel(fused, Cp @ w_eq + b_eq) < 1e-12
+    assert oracle.select(fused) == int(np.argmax(fused))

@@ -81,7 +81,7 @@ def _stack(W, module: str, x: torch.Tensor, cfg) -> torch.Tensor:
 
 
 @torch.no_grad()
-def evaluate_torch(cfg, W, inp, b: int):
+def evaluate_torch(cfg, W, inp, b: int, cross_seq: bool = True):
     """Scores of request b.  Items are indexed with torch.unique (sorted) and gathered by inverse."""
     lists = torch.as_tensor(np.asarray(inp["lists"][b], dtype=np.int64))
     if cfg.vocab:
@@ -99,7 +99,7 @@ def evaluate_torch(cfg, W, inp, b: int):
     pos = _t(W["pos"])
     seq = torch.cat([(_t(W["cls"]) + pos[0]).expand(K, 1, cfg.d), H[inv] + pos[1:L + 1]], dim=1)
     c = _stack(W, "seq", seq, cfg)[:, 0]
-    Cp = _stack(W, "cross", c[None], cfg)[0]
+    Cp = _stack(W, "cross", c[None], cfg)[0] if cross_seq else c
     head = nn.Linear(cfg.d, 1, dtype=torch.float64)
     head.weight.copy_(_t(W["head.w"])[None])
     head.bias.copy_(_t(W["head.b"]))
