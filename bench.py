@@ -28,6 +28,7 @@ METRIC = "candidate lists scored/sec at K=50 (B=64,L=10); MFMA util %; p50 laten
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12     # dense bf16 matrix-core peak, 2516.6 TFLOP/s
 PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+ASM_REPS = 100           # assembly launches per captured graph (gather-stage timing)
 
 
 def assemble_bytes(c, U):
@@ -324,6 +325,46 @@ def main() -> int:
         graph_ms = g0.elapsed_time(g1) / args.steps
         del graph
 
+    # ---- the assembly alone: ASM_REPS launches of fe_assemble on the pass's own buffers, captured
+    #      as one HIP graph so that the launches run back to back on the device (per-launch host
+    #      calls would otherwise leave gaps longer than the kernel); average duration per launch
+    asm_loop_us = copy_ref = None
+    if not args.no_trace:
+        b = bufs
+        asm_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(asm_graph):
+            for _ in range(ASM_REPS):
+                fe.fe_assemble(ev.handle, c.B, c.K, c.L, b["U_cap"], b["slot"], b["H"], b["seq"])
+        asm_graph.replay()
+        torch.cuda.synchronize()
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        for _ in range(5):
+            asm_graph.replay()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        asm_loop_us = a0.elapsed_time(a1) * 1e3 / (5 * ASM_REPS)
+        del asm_graph
+        # reference point: torch's device copy of a tensor the size of seq, timed the same way
+        seq_copy = torch.empty_like(b["seq"])
+        copy_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(copy_graph):
+            for _ in range(ASM_REPS):
+                seq_copy.copy_(b["seq"])
+        copy_graph.replay()
+        torch.cuda.synchronize()
+        a0.record(stream)
+        for _ in range(5):
+            copy_graph.replay()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        copy_us = a0.elapsed_time(a1) * 1e3 / (5 * ASM_REPS)
+        copy_bytes = 2 * seq_copy.numel() * seq_copy.element_size()
+        copy_ref = {"avg_launch_us": round(copy_us, 3), "bytes_per_launch": copy_bytes,
+                    "GBps": round(copy_bytes / (copy_us / 1e6) / 1e9, 1),
+                    "what": "torch copy_ of a tensor the size of seq (read + write), back to back from a HIP graph"}
+        del copy_graph, seq_copy
+
     # ---- kernel-timing region: the same steps with HIP events around every launch
     fam = {}
     if not args.no_trace:
@@ -365,8 +406,16 @@ def main() -> int:
                 tf = flops[name] / (fam[name][0] / args.steps / 1e3) / 1e12
                 stages[name].update(tflops=round(tf, 2), mfma_frac=round(tf / peak, 4))
         if "assemble" in stages:
-            gbs = asm_bytes / (fam["assemble"][0] / args.steps / 1e3) / 1e9
-            stages["assemble"].update(GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
+            # per-launch events add their own overhead to a kernel this short: the back-to-back
+            # average from the graph of assembly launches is the duration the fraction uses
+            stages["assemble"]["traced_avg_launch_us"] = stages["assemble"]["avg_launch_us"]
+            if asm_loop_us is not None:
+                stages["assemble"]["avg_launch_us"] = round(asm_loop_us, 3)
+            gbs = asm_bytes / (stages["assemble"]["avg_launch_us"] / 1e6) / 1e9
+            stages["assemble"].update(bytes_per_launch=int(asm_bytes), GBps=round(gbs, 1),
+                                      hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
+                                      timing=f"mean of {5 * ASM_REPS} back-to-back launches replayed from a HIP graph",
+                                      copy_reference=copy_ref)
         dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
         dom_ms, dom_n = fam[dom]
         avg_s = dom_ms / dom_n / 1e3

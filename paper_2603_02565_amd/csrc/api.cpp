@@ -745,8 +745,13 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
   const void* table = pool ? pool : m->emb;
   const long long table_bs = pool ? (long long)M * d : 0;
   void* G0 = at<char>(ws, w.i_g0);
-  FE_LAUNCH(F_DEDUP, s, launch_dedup(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, s));
-  FE_LAUNCH(F_GATHER, s, launch_gather_rows(table, table_bs, M, uniq, Ucap, n_uniq, B, Ucap, d, G0, nullptr, 0, bf, s));
+  if (dedup_gather_fits(Ucap, d, bf)) {
+    FE_LAUNCH(F_DEDUP, s, launch_dedup_gather(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, table, table_bs, d,
+                                              G0, bf, s));
+  } else {
+    FE_LAUNCH(F_DEDUP, s, launch_dedup(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, s));
+    FE_LAUNCH(F_GATHER, s, launch_gather_rows(table, table_bs, M, uniq, Ucap, n_uniq, B, Ucap, d, G0, nullptr, 0, bf, s));
+  }
   float* G = at<float>(ws, w.i_g);
   float* G1 = at<float>(ws, w.i_g1);
   void* qkv = at<char>(ws, w.i_qkv);

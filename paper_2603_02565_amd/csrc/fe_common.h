@@ -201,6 +201,12 @@ hipError_t launch_repeat_blocks(const void* src, void* dst, long long block_byte
 hipError_t launch_take_list_slots(const int32_t* slot_all, int32_t* slot_k, int BK, int K, int L, hipStream_t s);
 hipError_t launch_dedup(const int32_t* lists, int B, int KL, int M, int U_cap, int32_t* uniq,
                         int32_t* n_uniq, int32_t* slot, int32_t* status, hipStream_t s);
+// U(z) and the element rows in one launch (one workgroup per request), when
+// dedup_gather_fits: out [B][U_cap][d] as launch_gather_rows with idx = uniq, nvalid = n_uniq.
+bool dedup_gather_fits(int U_cap, int d, bool bf16_model);
+hipError_t launch_dedup_gather(const int32_t* lists, int B, int KL, int M, int U_cap, int32_t* uniq, int32_t* n_uniq,
+                               int32_t* slot, int32_t* status, const void* table, long long table_bs, int d,
+                               void* out, bool bf16_model, hipStream_t s);
 hipError_t launch_gather_rows(const void* table, long long table_bs, int n_rows_table, const int32_t* idx,
                               int idx_bs, const int32_t* nvalid, int B, int rows, int d, void* out,
                               int32_t* status, int status_bit, bool bf16_model, hipStream_t s);

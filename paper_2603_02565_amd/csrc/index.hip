@@ -5,6 +5,8 @@
 #include "fe_common.h"
 #include "flasheval.h"
 
+#include <climits>
+
 namespace {
 
 // ------------------------------------------------------------------------------------------
@@ -12,15 +14,37 @@ namespace {
 // an exclusive scan of per-word popcounts gives every element its rank, so uniq comes out in
 // ascending order and slot = rank(element) is exact and deterministic.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_dedup(const int32_t* __restrict__ lists, int KL, int M, int U_cap,
-                                               int32_t* __restrict__ uniq, int32_t* __restrict__ n_uniq,
-                                               int32_t* __restrict__ slot, int32_t* __restrict__ status) {
-  extern __shared__ uint32_t sm[];
-  __shared__ uint32_t s_part[256];
+
+// Exclusive prefix sum of one value per thread over the 256-thread workgroup (wave scans on
+// lane shuffles, then the four wave totals through LDS); *total receives the sum of all values.
+FE_DEV uint32_t block_exclusive_scan(uint32_t x, uint32_t* s_wave, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += t;
+  }
+  if (lane == 63) s_wave[wave] = inc;
+  __syncthreads();
+  uint32_t before = 0;
+  for (int w = 0; w < wave; ++w) before += s_wave[w];
+  *total = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
+  return before + inc - x;
+}
+
+// The distinct set of request b = xcd_tile(blockIdx.x, B) (XCD-contiguous requests, so the
+// kernels after it, mapped the same way, read slot and the element rows from their own L2):
+// writes uniq (ascending, padded with -1 up to U_cap),
+// n_uniq, slot and the status word, and, when s_uniq != nullptr, the distinct ids into LDS
+// s_uniq[0 .. U).  bits and pre are LDS arrays of (M + 31) / 32 words.  Returns U; the ids in
+// s_uniq are visible to the whole workgroup when it returns.
+FE_DEV int dedup_request(const int32_t* __restrict__ lists, int KL, int M, int U_cap, int32_t* __restrict__ uniq,
+                         int32_t* __restrict__ n_uniq, int32_t* __restrict__ slot, int32_t* __restrict__ status,
+                         uint32_t* bits, uint32_t* pre, int32_t* s_uniq) {
+  __shared__ uint32_t s_wave[4];
   const int W = (M + 31) >> 5;
-  uint32_t* bits = sm;
-  uint32_t* pre = sm + W;
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int b = xcd_tile(blockIdx.x, gridDim.x), tid = threadIdx.x;
   const int32_t* lb = lists + (long long)b * KL;
 
   for (int i = tid; i < W; i += 256) bits[i] = 0u;
@@ -38,23 +62,18 @@ __global__ __launch_bounds__(256) void k_dedup(const int32_t* __restrict__ lists
   const int w0 = min(W, tid * chunk), w1 = min(W, w0 + chunk);
   uint32_t local = 0;
   for (int w = w0; w < w1; ++w) local += __popc(bits[w]);
-  s_part[tid] = local;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const uint32_t add = tid >= off ? s_part[tid - off] : 0u;
-    __syncthreads();
-    s_part[tid] += add;
-    __syncthreads();
-  }
-  const uint32_t total = s_part[255];
-  uint32_t run = s_part[tid] - local;
+  uint32_t total;
+  uint32_t run = block_exclusive_scan(local, s_wave, &total);
   int32_t* ub = uniq + (long long)b * U_cap;
   for (int w = w0; w < w1; ++w) {
     pre[w] = run;
     uint32_t m = bits[w];
     while (m) {
       const int t = __ffs(m) - 1;
-      ub[run++] = (w << 5) + t;
+      const int id = (w << 5) + t;
+      ub[run] = id;
+      if (s_uniq) s_uniq[run] = id;
+      ++run;
       m &= m - 1;
     }
   }
@@ -70,6 +89,49 @@ __global__ __launch_bounds__(256) void k_dedup(const int32_t* __restrict__ lists
   if (tid == 0) {
     n_uniq[b] = (int32_t)total;
     status[b] = bad ? FE_DEV_BAD_INDEX : 0;
+  }
+  return (int)total;
+}
+
+__global__ __launch_bounds__(256) void k_dedup(const int32_t* __restrict__ lists, int KL, int M, int U_cap,
+                                               int32_t* __restrict__ uniq, int32_t* __restrict__ n_uniq,
+                                               int32_t* __restrict__ slot, int32_t* __restrict__ status) {
+  extern __shared__ uint32_t sm[];
+  const int W = (M + 31) >> 5;
+  dedup_request(lists, KL, M, U_cap, uniq, n_uniq, slot, status, sm, sm + W, nullptr);
+}
+
+// The distinct set and its element rows in one launch, for requests whose rows are few:
+// out[b][r] = table[b][uniq[b][r]] (VPR 16-byte vectors per row) for r < U, zero rows up to
+// U_cap.  Each thread keeps NI row loads in flight.
+template <int VPR>
+__global__ __launch_bounds__(256) void k_dedup_gather(const int32_t* __restrict__ lists, int KL, int M, int U_cap,
+                                                      int32_t* __restrict__ uniq, int32_t* __restrict__ n_uniq,
+                                                      int32_t* __restrict__ slot, int32_t* __restrict__ status,
+                                                      const uint4* __restrict__ table, long long table_bs_v,
+                                                      uint4* __restrict__ out) {
+  extern __shared__ uint32_t sm[];
+  const int W = (M + 31) >> 5;
+  int32_t* s_uniq = reinterpret_cast<int32_t*>(sm + 2 * W);
+  const int U = dedup_request(lists, KL, M, U_cap, uniq, n_uniq, slot, status, sm, sm + W, s_uniq);
+  constexpr int RPI = 256 / VPR, NI = 8;
+  const int b = xcd_tile(blockIdx.x, gridDim.x);
+  const int v = threadIdx.x % VPR, rr = threadIdx.x / VPR;
+  const uint4* tb = table + b * table_bs_v;
+  uint4* ob = out + (long long)b * U_cap * VPR;
+  for (int r0 = rr; r0 < U_cap; r0 += NI * RPI) {
+    uint4 val[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = r0 + i * RPI;
+      val[i] = make_uint4(0u, 0u, 0u, 0u);
+      if (r < U) val[i] = tb[(long long)s_uniq[r] * VPR + v];
+    }
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = r0 + i * RPI;
+      if (r < U_cap) ob[(long long)r * VPR + v] = val[i];
+    }
   }
 }
 
@@ -99,66 +161,96 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint4* __restrict__ t
 
 // ------------------------------------------------------------------------------------------
 // Sequence assembly: seq[b][k][0] = cls + pos[0], seq[b][k][j+1] = H[b][slot] + pos[j+1].
-// Each thread produces one 16-byte vector of one output row; the sum is taken in fp32 and
-// rounded once.  Pure data movement: bound by the HBM write of seq.
+// Pure data movement, bound by the HBM write of seq and by the latency of its two dependent
+// loads (slot, then the element row).  A row is VPR 16-byte vectors; a workgroup owns
+// NI * (256 / VPR) consecutive output rows and each thread NI of them (one vector each), so a
+// thread's NI slot loads, then its NI row loads, are in flight together.
+// Workgroups take XCD-contiguous row ranges (xcd_tile): XCD x assembles the lists of the x-th
+// eighth of the requests, whose element rows H the item kernels wrote through that XCD's L2,
+// and whose sequences the sequence encoder reads there next.  The sum is taken in fp32 and
+// rounded once; an occurrence whose slot lies outside [0, U_cap) gives a zero row.
 // ------------------------------------------------------------------------------------------
-template <typename T>
+template <typename T, int VPR, int NI>
 __global__ __launch_bounds__(256) void k_assemble(const int32_t* __restrict__ slot, const T* __restrict__ H,
-                                                  int B, int K, int L, int U_cap, int d, const T* __restrict__ cls,
+                                                  int K, int L, int U_cap, int rows, const T* __restrict__ cls,
                                                   const T* __restrict__ pos, T* __restrict__ seq) {
-  constexpr int VEC = 16 / sizeof(T);
-  const int vpr = d / VEC;
+  constexpr int VEC = 16 / sizeof(T), RPI = 256 / VPR;
   const int S = L + 1;
-  const long long total = (long long)B * K * S * vpr;
-  for (long long e = blockIdx.x * 256ll + threadIdx.x; e < total; e += (long long)gridDim.x * 256) {
-    const long long orow = e / vpr;
-    const int v = (int)(e - orow * vpr);
-    const long long bk = orow / S;
-    const int j = (int)(orow - bk * S);
-    const int b = (int)(bk / K);
-    T src[VEC], pv[VEC], res[VEC];
-    *reinterpret_cast<uint4*>(pv) = reinterpret_cast<const uint4*>(pos + (long long)j * d)[v];
-    bool zero = false;
-    if (j == 0) {
-      *reinterpret_cast<uint4*>(src) = reinterpret_cast<const uint4*>(cls)[v];
-    } else {
-      const int s = slot[bk * L + (j - 1)];
-      if (s >= 0 && s < U_cap) *reinterpret_cast<uint4*>(src) = reinterpret_cast<const uint4*>(H + ((long long)b * U_cap + s) * d)[v];
-      else zero = true;
-    }
+  const int v = threadIdx.x % VPR, rr = threadIdx.x / VPR;
+  const int row0 = xcd_tile(blockIdx.x, gridDim.x) * (RPI * NI) + rr;
+  const uint4* H4 = reinterpret_cast<const uint4*>(H);
+  int src[NI], jpos[NI];   // src: H vector index, -1 for [CLS], -2 for a zero row
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) res[i] = zero ? from_f32<T>(0.f) : from_f32<T>(to_f32(src[i]) + to_f32(pv[i]));
-    reinterpret_cast<uint4*>(seq)[e] = *reinterpret_cast<uint4*>(res);
+  for (int i = 0; i < NI; ++i) {
+    const int r = row0 + i * RPI;
+    const int bk = r / S, j = r - bk * S;
+    jpos[i] = j;
+    src[i] = -2;
+    if (r < rows) {
+      if (j == 0) {
+        src[i] = -1;
+      } else {
+        const int s = slot[bk * L + j - 1];
+        if (s >= 0 && s < U_cap) src[i] = ((bk / K) * U_cap + s) * VPR + v;
+      }
+    }
+  }
+  uint4 a[NI], p[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    a[i] = src[i] >= 0 ? H4[src[i]] : reinterpret_cast<const uint4*>(cls)[v];
+    p[i] = reinterpret_cast<const uint4*>(pos)[jpos[i] * VPR + v];
+  }
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int r = row0 + i * RPI;
+    if (r >= rows) continue;
+    const T* x = reinterpret_cast<const T*>(&a[i]);
+    const T* q = reinterpret_cast<const T*>(&p[i]);
+    T res[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) res[e] = src[i] == -2 ? from_f32<T>(0.f) : from_f32<T>(to_f32(x[e]) + to_f32(q[e]));
+    reinterpret_cast<uint4*>(seq)[r * VPR + v] = *reinterpret_cast<const uint4*>(res);
   }
 }
 
 // Smallest index of the largest non-NaN value of s_score[0..K), -1 if every value is NaN; every
-// thread of the 256-thread block calls it and gets the result.
+// thread of the 256-thread block calls it and gets the result.  Candidates are merged by the
+// total order (larger value first, then smaller index) -- within each wave by a shuffle
+// butterfly, then across the four waves through s_val / s_idx -- so the result does not depend
+// on the merge order.
+FE_DEV void select_merge(float& bv, int& bi, float ov, int oi) {
+  if (oi >= 0 && (bi < 0 || ov > bv || (ov == bv && oi < bi))) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
 FE_DEV int block_select(const float* s_score, int K, float* s_val, int* s_idx) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   float bv = 0.f;
   int bi = -1;
   for (int k = tid; k < K; k += 256) {
     const float v = s_score[k];
     if (v != v) continue;
-    if (bi < 0 || v > bv) { bv = v; bi = k; }
+    select_merge(bv, bi, v, k);
   }
-  s_val[tid] = bv;
-  s_idx[tid] = bi;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    select_merge(bv, bi, ov, oi);
+  }
+  if (lane == 0) {
+    s_val[wave] = bv;
+    s_idx[wave] = bi;
+  }
   __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (tid < off) {
-      const float ov = s_val[tid + off];
-      const int oi = s_idx[tid + off];
-      const int mi = s_idx[tid];
-      if (oi >= 0 && (mi < 0 || ov > s_val[tid] || (ov == s_val[tid] && oi < mi))) {
-        s_val[tid] = ov;
-        s_idx[tid] = oi;
-      }
-    }
-    __syncthreads();
-  }
-  return s_idx[0];
+  float rv = s_val[0];
+  int ri = s_idx[0];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) select_merge(rv, ri, s_val[w], s_idx[w]);
+  return ri;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -318,6 +410,35 @@ hipError_t launch_dedup(const int32_t* lists, int B, int KL, int M, int U_cap, i
   return hipGetLastError();
 }
 
+bool dedup_gather_fits(int U_cap, int d, bool bf16_model) {
+  const long long bytes = (long long)U_cap * d * (bf16_model ? 2 : 4);
+  return bytes <= (128 << 10);
+}
+
+hipError_t launch_dedup_gather(const int32_t* lists, int B, int KL, int M, int U_cap, int32_t* uniq, int32_t* n_uniq,
+                               int32_t* slot, int32_t* status, const void* table, long long table_bs, int d,
+                               void* out, bool bf16_model, hipStream_t s) {
+  if (!dedup_gather_fits(U_cap, d, bf16_model)) return hipErrorInvalidValue;
+  const int esz = bf16_model ? 2 : 4;
+  const int vpr = d * esz / 16;
+  const size_t lds = (2 * (size_t)((M + 31) / 32) + U_cap) * sizeof(uint32_t);
+  const uint4* t = static_cast<const uint4*>(table);
+  uint4* o = static_cast<uint4*>(out);
+  const long long tbs = table_bs * esz / 16;
+#define FE_DG(V) hipLaunchKernelGGL(k_dedup_gather<V>, dim3(B), dim3(256), lds, s, lists, KL, M, U_cap, uniq, n_uniq, \
+                                    slot, status, t, tbs, o)
+  switch (vpr) {
+    case 8: FE_DG(8); break;
+    case 16: FE_DG(16); break;
+    case 32: FE_DG(32); break;
+    case 64: FE_DG(64); break;
+    case 128: FE_DG(128); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef FE_DG
+  return hipGetLastError();
+}
+
 hipError_t launch_gather_rows(const void* table, long long table_bs, int n_rows_table, const int32_t* idx, int idx_bs,
                               const int32_t* nvalid, int B, int rows, int d, void* out, int32_t* status,
                               int status_bit, bool bf16_model, hipStream_t s) {
@@ -330,17 +451,42 @@ hipError_t launch_gather_rows(const void* table, long long table_bs, int n_rows_
   return hipGetLastError();
 }
 
+template <typename T, int VPR>
+void assemble_as(const int32_t* slot, const void* H, int K, int L, int U_cap, int rows, const void* cls,
+                 const void* pos, void* seq, hipStream_t s) {
+  constexpr int NI = 1, RPB = NI * (256 / VPR);   // one row per thread: more workgroups beat more rows in flight per thread
+  const int grid = (rows + RPB - 1) / RPB;
+  hipLaunchKernelGGL((k_assemble<T, VPR, NI>), dim3(grid), dim3(256), 0, s, slot, static_cast<const T*>(H), K, L,
+                     U_cap, rows, static_cast<const T*>(cls), static_cast<const T*>(pos), static_cast<T*>(seq));
+}
+
 hipError_t launch_assemble(const int32_t* slot, const void* H, int B, int K, int L, int U_cap, int d, const void* cls,
                            const void* pos, void* seq, bool bf16_model, hipStream_t s) {
-  const int esz = bf16_model ? 2 : 4;
-  const long long work = (long long)B * K * (L + 1) * (d * esz / 16);
-  if (bf16_model)
-    hipLaunchKernelGGL(k_assemble<bf16>, dim3(grid_for(work)), dim3(256), 0, s, slot, static_cast<const bf16*>(H), B, K,
-                       L, U_cap, d, static_cast<const bf16*>(cls), static_cast<const bf16*>(pos), static_cast<bf16*>(seq));
-  else
-    hipLaunchKernelGGL(k_assemble<float>, dim3(grid_for(work)), dim3(256), 0, s, slot, static_cast<const float*>(H), B,
-                       K, L, U_cap, d, static_cast<const float*>(cls), static_cast<const float*>(pos),
-                       static_cast<float*>(seq));
+  const long long rows = (long long)B * K * (L + 1);
+  const long long vpr = (long long)d * (bf16_model ? 2 : 4) / 16;
+  // every vector index of seq and H must fit the kernel's 32-bit arithmetic
+  if (rows * vpr > INT_MAX || (long long)B * U_cap * vpr > INT_MAX) return hipErrorInvalidValue;
+  if (rows == 0) return hipSuccess;
+  const int R = (int)rows;
+#define FE_ASM(TT, V) assemble_as<TT, V>(slot, H, K, L, U_cap, R, cls, pos, seq, s)
+  if (bf16_model) {
+    switch (vpr) {
+      case 16: FE_ASM(bf16, 16); break;
+      case 32: FE_ASM(bf16, 32); break;
+      case 64: FE_ASM(bf16, 64); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (vpr) {
+      case 8: FE_ASM(float, 8); break;
+      case 16: FE_ASM(float, 16); break;
+      case 32: FE_ASM(float, 32); break;
+      case 64: FE_ASM(float, 64); break;
+      case 128: FE_ASM(float, 128); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+#undef FE_ASM
   return hipGetLastError();
 }
 
