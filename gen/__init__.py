@@ -19,6 +19,9 @@ Workloads (numbered 0..4):
   3  long context            B=16, T=2048, d=256, H=8, n=2, M=500,  K=100, L=20
   4  text hypotheses         B=8,  T=1024, d=512, H=8, n=4, V=32000, K=16, L=64
 
+Any workload can be taken with attention="linear" (the kernelized-attention
+variant); the model parameters and inputs do not depend on that choice.
+
 Sampling rules:
   * context and pool rows ~ N(0, 1) (workload 4: context rows are token ids
     uniform over the vocabulary, embedded by the model table E).
@@ -68,6 +71,8 @@ class Config:
     zipf_s: float = 0.0
     vocab: int = 0           # >0: items and context are token ids into E[vocab][d]
     pos_kind: str = "learned"  # "learned" or "sinusoid"
+    attention: str = "softmax"  # "softmax", or "linear": kernelized attention in the context,
+                                # item->context and cross-sequence modules
     weight_seed: int = 0
     input_seed: int = 0
     list_seed: int = 0
@@ -92,7 +97,8 @@ class Config:
 
     @property
     def label(self) -> str:
-        return f"cfg{self.cid}" + (f"_K{self.K}" if self.cid == 2 else "")
+        return f"cfg{self.cid}" + (f"_K{self.K}" if self.cid == 2 else "") + \
+            ("_linear" if self.attention == "linear" else "")
 
 
 _BASE = {
@@ -133,6 +139,8 @@ def config(cid: int, K: Optional[int] = None, **overrides) -> Config:
         cfg = replace(cfg, **overrides)
     if cfg.d % cfg.n_heads:
         raise ValueError("d must be a multiple of n_heads")
+    if cfg.attention not in ("softmax", "linear"):
+        raise ValueError(f"attention must be 'softmax' or 'linear', got {cfg.attention!r}")
     return cfg
 
 

@@ -68,6 +68,37 @@ def _mha(qs: Mat, ks: Mat, vs: Mat, n_heads: int) -> Mat:
     return out
 
 
+def _phi(t: float) -> float:
+    """elu(t) + 1."""
+    return t + 1.0 if t > 0.0 else math.exp(t)
+
+
+def _mha_linear(qs: Mat, ks: Mat, vs: Mat, n_heads: int) -> Mat:
+    """Per query row and head: weight of key r = sum_t phi(q_t) phi(k_r,t); output = weighted sum
+    of the values over the sum of the weights (kernelized attention, no scale)."""
+    d = len(qs[0])
+    dh = d // n_heads
+    out = []
+    for q in qs:
+        row = [0.0] * d
+        for h in range(n_heads):
+            lo = h * dh
+            ws = []
+            for kk in ks:
+                acc = 0.0
+                for t in range(dh):
+                    acc += _phi(q[lo + t]) * _phi(kk[lo + t])
+                ws.append(acc)
+            tot = sum(ws)
+            for t in range(dh):
+                acc = 0.0
+                for r in range(len(vs)):
+                    acc += ws[r] * vs[r][lo + t]
+                row[lo + t] = acc / tot
+        out.append(row)
+    return out
+
+
 class _P:
     def __init__(self, W: Dict):
         self.W = W
@@ -76,14 +107,14 @@ class _P:
         return _tolist(self.W[name])
 
 
-def _self_attn(X: Mat, P: _P, p: str, n_heads: int) -> Mat:
+def _self_attn(X: Mat, P: _P, p: str, n_heads: int, linear: bool = False) -> Mat:
     d = len(X[0])
     wqkv, bqkv = P[f"{p}.wqkv"], P[f"{p}.bqkv"]
     qkv = [_vecmat(x, wqkv, bqkv) for x in X]
     q = [r[:d] for r in qkv]
     k = [r[d:2 * d] for r in qkv]
     v = [r[2 * d:] for r in qkv]
-    o = _mha(q, k, v, n_heads)
+    o = _mha_linear(q, k, v, n_heads) if linear else _mha(q, k, v, n_heads)
     return [_vecmat(r, P[f"{p}.wo"], P[f"{p}.bo"]) for r in o]
 
 
@@ -99,16 +130,16 @@ def _add(A: Mat, B: Mat) -> Mat:
     return [[a + b for a, b in zip(ra, rb)] for ra, rb in zip(A, B)]
 
 
-def _enc(X: Mat, P: _P, p: str, n_heads: int) -> Mat:
+def _enc(X: Mat, P: _P, p: str, n_heads: int, linear: bool = False) -> Mat:
     Xn = [_ln(x, P[f"{p}.ln1.g"], P[f"{p}.ln1.b"]) for x in X]
-    X = _add(X, _self_attn(Xn, P, p, n_heads))
+    X = _add(X, _self_attn(Xn, P, p, n_heads, linear))
     Xn = [_ln(x, P[f"{p}.ln2.g"], P[f"{p}.ln2.b"]) for x in X]
     return _add(X, _ffn(Xn, P, p))
 
 
-def _stack(X: Mat, P: _P, module: str, n_layers: int, n_heads: int) -> Mat:
+def _stack(X: Mat, P: _P, module: str, n_layers: int, n_heads: int, linear: bool = False) -> Mat:
     for l in range(n_layers):
-        X = _enc(X, P, f"{module}.{l}", n_heads)
+        X = _enc(X, P, f"{module}.{l}", n_heads, linear)
     return [_ln(x, P[f"{module}.lnf.g"], P[f"{module}.lnf.b"]) for x in X]
 
 
@@ -116,12 +147,14 @@ def evaluate_brute(cfg, W: Dict, inp: Dict, b: int = 0) -> Dict:
     """Scores, selection and intermediates of request b, by explicit loops."""
     P = _P(W)
     nh, nl = cfg.n_heads, cfg.n_layers
+    # linear-attention variant: context, item->context and cross-sequence attention are linear
+    lin = getattr(cfg, "attention", "softmax") == "linear"
     if cfg.vocab:
         E = P["emb"]
         X = [list(E[t]) for t in _tolist(inp["ctx_ids"][b])]
     else:
         X = [list(r) for r in _tolist(inp["x"][b])]
-    Q = _stack(X, P, "ctx", nl, nh)
+    Q = _stack(X, P, "ctx", nl, nh, lin)
     kv = []
     for l in range(nl):
         p = f"ctx.kv.{l}"
@@ -141,7 +174,7 @@ def evaluate_brute(cfg, W: Dict, inp: Dict, b: int = 0) -> Dict:
         Gn = [_ln(g, P[f"{p}.ln1.g"], P[f"{p}.ln1.b"]) for g in G]
         G = _add(G, _self_attn(Gn, P, p, nh))
         qs = [_vecmat(_ln(g, P[f"{p}.ln2.g"], P[f"{p}.ln2.b"]), P[f"{p}.wq"], P[f"{p}.bq"]) for g in G]
-        o = _mha(qs, kv[l][0], kv[l][1], nh)
+        o = _mha_linear(qs, kv[l][0], kv[l][1], nh) if lin else _mha(qs, kv[l][0], kv[l][1], nh)
         G = _add(G, [_vecmat(r, P[f"{p}.wo2"], P[f"{p}.bo2"]) for r in o])
         Gn = [_ln(g, P[f"{p}.ln3.g"], P[f"{p}.ln3.b"]) for g in G]
         G = _add(G, _ffn(Gn, P, p))
@@ -154,7 +187,7 @@ def evaluate_brute(cfg, W: Dict, inp: Dict, b: int = 0) -> Dict:
             h = H[uniq.index(t)]
             seq.append([h[i] + pos[j + 1][i] for i in range(len(h))])
         cs.append(_stack(seq, P, "seq", nl, nh)[0])
-    Cp = _stack(cs, P, "cross", nl, nh)
+    Cp = _stack(cs, P, "cross", nl, nh, lin)
     w, bias = P["head.w"], P["head.b"]
     scores = [sum(c[i] * w[i] for i in range(len(w))) + bias[0] for c in Cp]
     best = -1

@@ -35,6 +35,13 @@ The paper leaves the layer internals open; this oracle fixes them as follows
     min-argmax tie rule of the label construction, Appendix B.1); NaN scores
     never win and an all-NaN vector selects -1.
 
+Linear-attention variant (cfg.attention == "linear"; the deployment setting
+of Appendix B.3, which serves both evaluators with the kernelized attention
+of the cited linear-attention work): the context self-attention, the items'
+cross-attention to the context and the cross-sequence attention use
+phi(q) . phi(k) weights with phi = elu + 1, no scale, normalised by their
+sum; the item-set self-attention and SeqEnc keep softmax.
+
 Two evaluation orders are provided:
   * `evaluate_naive` -- the oracle proper.  It follows the cost structure of
     the candidate-factorised evaluator (Section 4 and Appendix A.3): the
@@ -98,11 +105,70 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_heads: int) -> np.n
     return out
 
 
-def self_attention_block(x: np.ndarray, W: Params, p: str, n_heads: int) -> np.ndarray:
+def elu_plus_one(x: np.ndarray) -> np.ndarray:
+    """Feature map of kernelized attention: phi(x) = elu(x) + 1, i.e. x + 1 for x > 0 and
+    exp(x) otherwise (the map of the linear attention the paper's deployment uses, App. B.3)."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def linear_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_heads: int) -> np.ndarray:
+    """Multi-head linear attention on already projected q [nq,d], k, v [nk,d], in its defining
+    form: per head, the weight of key j for query i is phi(q_i) . phi(k_j), and the output is the
+    weighted sum of the values divided by the sum of the weights.  No scale and no mask (callers
+    pass exactly the valid keys)."""
+    d = q.shape[-1]
+    dh = d // n_heads
+    out = np.empty((q.shape[0], d), dtype=np.float64)
+    for h in range(n_heads):
+        cols = slice(h * dh, (h + 1) * dh)
+        w = elu_plus_one(q[:, cols]) @ elu_plus_one(k[:, cols]).T
+        out[:, cols] = (w @ v[:, cols]) / w.sum(axis=1, keepdims=True)
+    return out
+
+
+def linear_kv_state(k: np.ndarray, v: np.ndarray, n_heads: int) -> np.ndarray:
+    """Key/value cache of a linear-attention module: per head h, the sums over all keys t of
+    phi(k_t) v_t^T (dh x dh) and of phi(k_t) (dh).  Returned as [n_heads][dh + 1][dh]: rows
+    0..dh-1 hold the first sum (row i = feature i of phi(k)), row dh the second.  A query q then
+    attends as (phi(q)^T S) / (phi(q) . z), which equals `linear_attention` by associativity."""
+    d = k.shape[-1]
+    dh = d // n_heads
+    st = np.zeros((n_heads, dh + 1, dh), dtype=np.float64)
+    for h in range(n_heads):
+        cols = slice(h * dh, (h + 1) * dh)
+        fk = elu_plus_one(k[:, cols])
+        for t in range(k.shape[0]):
+            st[h, :dh] += np.outer(fk[t], v[t, cols])
+            st[h, dh] += fk[t]
+    return st
+
+
+def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_heads: int, kind: str = "softmax") -> np.ndarray:
+    """Scaled dot-product attention (kind "softmax") or linear attention (kind "linear")."""
+    if kind == "linear":
+        return linear_attention(q, k, v, n_heads)
+    if kind != "softmax":
+        raise ValueError(f"unknown attention kind {kind!r}")
+    return attention(q, k, v, n_heads)
+
+
+def module_attention(cfg, module: str) -> str:
+    """Attention kind of a module.  With cfg.attention == "linear", the attentions over sets
+    whose size grows with the workload -- the context self-attention ("ctx"), the items'
+    cross-attention to the context ("item_cross") and the cross-sequence attention over the K
+    lists ("cross") -- are linear; the item-set self-attention ("item_self") and SeqEnc ("seq")
+    stay softmax."""
+    if getattr(cfg, "attention", "softmax") == "linear" and module in ("ctx", "item_cross", "cross"):
+        return "linear"
+    return "softmax"
+
+
+def self_attention_block(x: np.ndarray, W: Params, p: str, n_heads: int, kind: str = "softmax") -> np.ndarray:
     """MHA(x, x) with the packed q|k|v projection `{p}.wqkv` and output projection `{p}.wo`."""
     d = x.shape[-1]
     qkv = x @ _f64(W[f"{p}.wqkv"]) + _f64(W[f"{p}.bqkv"])
-    o = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], n_heads)
+    o = attend(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], n_heads, kind)
     return o @ _f64(W[f"{p}.wo"]) + _f64(W[f"{p}.bo"])
 
 
@@ -111,17 +177,18 @@ def ffn(x: np.ndarray, W: Params, p: str) -> np.ndarray:
     return h @ _f64(W[f"{p}.w2"]) + _f64(W[f"{p}.b2"])
 
 
-def encoder_block(x: np.ndarray, W: Params, p: str, n_heads: int) -> np.ndarray:
+def encoder_block(x: np.ndarray, W: Params, p: str, n_heads: int, kind: str = "softmax") -> np.ndarray:
     """Pre-LN encoder block: x + MHA(LN1 x); then + FFN(LN2 x)."""
-    x = x + self_attention_block(layer_norm(x, W[f"{p}.ln1.g"], W[f"{p}.ln1.b"]), W, p, n_heads)
+    x = x + self_attention_block(layer_norm(x, W[f"{p}.ln1.g"], W[f"{p}.ln1.b"]), W, p, n_heads, kind)
     x = x + ffn(layer_norm(x, W[f"{p}.ln2.g"], W[f"{p}.ln2.b"]), W, p)
     return x
 
 
-def encoder_stack(x: np.ndarray, W: Params, module: str, n_layers: int, n_heads: int) -> np.ndarray:
+def encoder_stack(x: np.ndarray, W: Params, module: str, n_layers: int, n_heads: int,
+                  kind: str = "softmax") -> np.ndarray:
     """n pre-LN encoder blocks followed by the module's final LayerNorm."""
     for l in range(n_layers):
-        x = encoder_block(x, W, f"{module}.{l}", n_heads)
+        x = encoder_block(x, W, f"{module}.{l}", n_heads, kind)
     return layer_norm(x, W[f"{module}.lnf.g"], W[f"{module}.lnf.b"])
 
 
@@ -142,7 +209,7 @@ def encode_context(cfg, W: Params, X: np.ndarray) -> Tuple[np.ndarray, List[Tupl
     Returns the encoded context Q (T x d) and, for every item layer l,
     (K_l, V_l) = (Q Wk_l + bk_l, Q Wv_l + bv_l).
     """
-    Q = encoder_stack(X, W, "ctx", cfg.n_layers, cfg.n_heads)
+    Q = encoder_stack(X, W, "ctx", cfg.n_layers, cfg.n_heads, module_attention(cfg, "ctx"))
     kv = []
     for l in range(cfg.n_layers):
         p = f"ctx.kv.{l}"
@@ -172,9 +239,10 @@ def encode_items(cfg, W: Params, G: np.ndarray, kv: List[Tuple[np.ndarray, np.nd
     items as queries against the context cache, and FFN; then the final LayerNorm gives H."""
     for l in range(cfg.n_layers):
         p = f"item.{l}"
-        G = G + self_attention_block(layer_norm(G, W[f"{p}.ln1.g"], W[f"{p}.ln1.b"]), W, p, cfg.n_heads)
+        G = G + self_attention_block(layer_norm(G, W[f"{p}.ln1.g"], W[f"{p}.ln1.b"]), W, p, cfg.n_heads,
+                                     module_attention(cfg, "item_self"))
         q = layer_norm(G, W[f"{p}.ln2.g"], W[f"{p}.ln2.b"]) @ _f64(W[f"{p}.wq"]) + _f64(W[f"{p}.bq"])
-        o = attention(q, kv[l][0], kv[l][1], cfg.n_heads)
+        o = attend(q, kv[l][0], kv[l][1], cfg.n_heads, module_attention(cfg, "item_cross"))
         G = G + o @ _f64(W[f"{p}.wo2"]) + _f64(W[f"{p}.bo2"])
         h = layer_norm(G, W[f"{p}.ln3.g"], W[f"{p}.ln3.b"])
         G = G + np.maximum(h @ _f64(W[f"{p}.w1"]) + _f64(W[f"{p}.b1"]), 0.0) @ _f64(W[f"{p}.w2"]) \
@@ -194,12 +262,12 @@ def assemble_one(W: Params, rows: np.ndarray) -> np.ndarray:
 
 def encode_sequence(cfg, W: Params, seq: np.ndarray) -> np.ndarray:
     """SeqEnc over one assembled list; c_k is the final-normalised [CLS] row (Section 4.3)."""
-    return encoder_stack(seq, W, "seq", cfg.n_layers, cfg.n_heads)[0]
+    return encoder_stack(seq, W, "seq", cfg.n_layers, cfg.n_heads, module_attention(cfg, "seq"))[0]
 
 
 def cross_sequence(cfg, W: Params, c: np.ndarray) -> np.ndarray:
     """Self-attention over the set {c_1..c_K} with no positions (Section 4.4)."""
-    return encoder_stack(c, W, "cross", cfg.n_layers, cfg.n_heads)
+    return encoder_stack(c, W, "cross", cfg.n_layers, cfg.n_heads, module_attention(cfg, "cross"))
 
 
 def score(W: Params, Cp: np.ndarray) -> np.ndarray:
