@@ -304,14 +304,14 @@ def test_planted_mistakes_are_caught(cfg0, monkeypatch, mistake):
     elif mistake == "transpose_wo":
         orig_sab = ev.self_attention_block
 
-        def sab(x, W_, p, nh):
+        def sab(x, W_, p, nh, kind="softmax"):
             W3 = dict(W_)
             W3[f"{p}.wo"] = np.ascontiguousarray(W_[f"{p}.wo"].T)
-            return orig_sab(x, W3, p, nh)
+            return orig_sab(x, W3, p, nh, kind)
         monkeypatch.setattr(ev, "self_attention_block", sab)
     elif mistake == "drop_ffn_residual":
-        def enc(x, W_, p, nh):
-            x = x + ev.self_attention_block(ev.layer_norm(x, W_[f"{p}.ln1.g"], W_[f"{p}.ln1.b"]), W_, p, nh)
+        def enc(x, W_, p, nh, kind="softmax"):
+            x = x + ev.self_attention_block(ev.layer_norm(x, W_[f"{p}.ln1.g"], W_[f"{p}.ln1.b"]), W_, p, nh, kind)
             return ev.ffn(ev.layer_norm(x, W_[f"{p}.ln2.g"], W_[f"{p}.ln2.b"]), W_, p)
         monkeypatch.setattr(ev, "encoder_block", enc)
     elif mistake == "head_slice":
