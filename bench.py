@@ -246,7 +246,7 @@ def main() -> int:
     torch.cuda.set_device(0)
     c = gen.config(args.workload, K=args.K) if args.workload == 2 else gen.config(args.workload)
     W, I = gen.make_weights(c), gen.make_inputs(c)
-    ev = fe.Evaluator(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, c.dtype, W)
+    ev = fe.Evaluator(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, c.dtype, W, attention=c.attention)
     bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
     act = torch.bfloat16 if c.dtype == "bf16" else torch.float32
     dev = torch.device("cuda", 0)

@@ -71,6 +71,18 @@ typedef enum {
 
 typedef enum { FE_F32 = 0, FE_BF16 = 1 } fe_dtype;
 
+/*
+ * Attention form.  FE_ATTN_SOFTMAX: scaled dot-product attention everywhere (Section 4).
+ * FE_ATTN_LINEAR: the deployment setting of Appendix B.3, which serves the evaluator with
+ * linear (kernelized) attention: in the context self-attention, the items' cross-attention to
+ * the context and the cross-sequence attention -- the attentions over sets that grow with the
+ * workload (T context rows, K lists) -- the weight of key k for query q is phi(q) . phi(k)
+ * with phi(x) = elu(x) + 1, no scale, and the output is the weighted sum of the values over
+ * the sum of the weights.  The item-set self-attention and SeqEnc keep softmax.  The context-side
+ * cache then becomes a fixed-size per-head state (see fe_encode_context).
+ */
+typedef enum { FE_ATTN_SOFTMAX = 0, FE_ATTN_LINEAR = 1 } fe_attention;
+
 /* Device status bits (per request). */
 #define FE_DEV_BAD_INDEX 1  /* a list entry outside [0, M): its slot is -1, fe_assemble writes a zero row */
 #define FE_DEV_BAD_TOKEN 2  /* a context token id outside [0, vocab): its row is embedded as zeros */
@@ -83,6 +95,7 @@ typedef struct {
   int32_t max_L;     /* longest list; the position table has max_L + 1 rows */
   int32_t vocab;     /* > 0: the model owns an embedding table E[vocab][d]; 0: none */
   int32_t dtype;     /* fe_dtype of activations and matrices */
+  int32_t attention; /* fe_attention */
 } fe_config;
 
 typedef struct fe_model fe_model; /* opaque; immutable after creation */
@@ -135,6 +148,13 @@ void fe_model_destroy(fe_model* m);
  */
 fe_status fe_workspace_size(const fe_model* m, int B, int T, int M, int K, int L, size_t* bytes);
 
+/*
+ * Bytes of fe_encode_context's output kv for B requests of T context rows:
+ *   FE_ATTN_SOFTMAX  n_layers * 2 * B * T * d * sizeof(act)   ([n][2][B][T][d] act)
+ *   FE_ATTN_LINEAR   n_layers * B * H * (dh + 1) * dh * 4     ([n][B][H][dh+1][dh] fp32)
+ */
+fe_status fe_kv_size(const fe_model* m, int B, int T, size_t* bytes);
+
 /* Message of the last non-OK status returned on this thread ("" if none). */
 const char* fe_last_error(void);
 
@@ -151,7 +171,12 @@ fe_status fe_read_device_status(const fe_model* m, const void* ws, int B, void* 
  * plus bias.  Exactly one of
  *   x       [B][T][d] act  -- context vectors, or
  *   ctx_ids [B][T] int32   -- token ids embedded through the model's table
- * is non-NULL.  Output kv [n_layers][2][B][T][d] act (index 0 = keys, 1 = values).
+ * is non-NULL.  Output kv (fe_kv_size bytes):
+ *   FE_ATTN_SOFTMAX  [n_layers][2][B][T][d] act (index 0 = keys, 1 = values);
+ *   FE_ATTN_LINEAR   [n_layers][B][H][dh + 1][dh] fp32: for item layer l, request b and head h,
+ *                    rows i < dh hold sum_t phi(K_l[t])_i V_l[t] over the head's columns and row
+ *                    dh holds sum_t phi(K_l[t]) -- everything the items' linear cross-attention
+ *                    needs, independent of T.
  */
 fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, const int32_t* ctx_ids, void* kv,
                             void* ws, size_t ws_bytes, void* stream);
@@ -161,7 +186,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
  *   pool   [B][M][d] act, or NULL on a model with a vocabulary (then the
  *          elements are token ids and M must equal vocab).
  *   lists  [B][K][L] int32 element indices into the pool (0-based).
- *   kv     output of fe_encode_context for the same B and T.
+ *   kv     output of fe_encode_context for the same B and T (and model).
  * Outputs:
  *   uniq   [B][U_cap] int32  distinct indices of each request, ascending,
  *                            padded with -1;

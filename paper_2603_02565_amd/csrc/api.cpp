@@ -262,6 +262,8 @@ Offsets pack_all(Packer& P, const fe_config& c) {
 fe_status check_config(const fe_config* c) {
   if (!c) return fail(FE_EINVAL, "config is NULL");
   if (c->dtype != FE_F32 && c->dtype != FE_BF16) return fail(FE_EINVAL, "dtype %d is not FE_F32 or FE_BF16", c->dtype);
+  if (c->attention != FE_ATTN_SOFTMAX && c->attention != FE_ATTN_LINEAR)
+    return fail(FE_EINVAL, "attention %d is not FE_ATTN_SOFTMAX or FE_ATTN_LINEAR", c->attention);
   if (c->d <= 0 || c->n_heads <= 0 || c->n_layers <= 0 || c->ffn_dim <= 0 || c->max_L <= 0 || c->vocab < 0)
     return fail(FE_EINVAL, "config sizes must be positive");
   if (c->d % c->n_heads) return fail(FE_EINVAL, "d=%d is not a multiple of n_heads=%d", c->d, c->n_heads);
@@ -284,6 +286,8 @@ fe_status check_config(const fe_config* c) {
 // ------------------------------------------------------------------------------------------
 struct Ws {
   size_t status;                                        // int32 [2][B]: items, context
+  size_t lin_st;                                        // linear models: fp32 [B][H][dh+1][dh], one module's state
+  size_t c_kvp;                                         // linear models: act [n][2][B][T][d] item-layer keys/values
   size_t c_xin, c_x, c_qkv, c_o, c_h;                   // context stage
   size_t i_g0, i_g, i_g1, i_qkv, i_o, i_q, i_h;         // item stage
   size_t s_x, s_qkv, s_o, s_h, s_c;                     // sequence + cross stages
@@ -305,10 +309,14 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
   Ws w{};
   Bump b0{0};
   w.status = b0.take(2 * B * 4);
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  const long long H = m->cfg.n_heads, dh = d / H;
+  if (lin) w.lin_st = b0.take(B * H * (dh + 1) * dh * 4);
   size_t base = b0.at, end = base;
   {  // context
     const long long R = B * T;
     Bump b{base};
+    if (lin) w.c_kvp = b.take(2 * m->cfg.n_layers * R * d * e);
     w.c_xin = b.take(R * d * e);
     w.c_x = b.take(R * d * 4);
     w.c_qkv = b.take(R * 3 * d * e);
@@ -343,6 +351,14 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
   return w;
 }
 
+// Bytes of fe_encode_context's output: the keys and values of every item layer, [n][2][B][T][d]
+// act; on linear-attention models their per-head state, [n][B][H][dh+1][dh] fp32.
+size_t kv_bytes(const fe_model* m, long long B, long long T) {
+  const long long d = m->cfg.d, n = m->cfg.n_layers, H = m->cfg.n_heads, dh = d / H;
+  if (m->cfg.attention == FE_ATTN_LINEAR) return (size_t)(n * B * H * (dh + 1) * dh * 4);
+  return (size_t)(n * 2 * B * T * d * (m->bf16 ? 2 : 4));
+}
+
 // Workspace of the candidate-factorised evaluator: the joint pass's workspace at B*K requests,
 // then the per-list copies of the inputs, the per-list key/value caches, the per-list item
 // encodings and the assembled sequences.
@@ -359,7 +375,7 @@ NaiveWs naive_layout(const fe_model* m, long long B, long long T, long long M, l
   w.inner_bytes = layout(m, BK, T, M, K, L).total;
   w.inner = b.take(w.inner_bytes);
   w.xin = b.take(ids ? BK * T * 4 : BK * T * d * e);
-  w.kv = b.take(n * 2 * BK * T * d * e);
+  w.kv = b.take(kv_bytes(m, BK, T));
   w.pool = own_pool ? b.take(BK * M * d * e) : 0;
   w.lists = b.take(BK * K * L * 4);
   w.uniq = b.take(BK * Ucap * 4);
@@ -430,13 +446,26 @@ struct KvOut {
   int32_t* zero; int zero_n;   // status words this launch clears (or nullptr)
 };
 
+// lin_st != nullptr: the block's attention is linear, through the state buffer lin_st
+// (fp32 [nb][H][dh+1][dh]).
 fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const void* xin, bool xin_f32, const Bufs& b,
-                    const int32_t* nvalid, hipStream_t s, const KvOut* kvo = nullptr) {
+                    const int32_t* nvalid, hipStream_t s, const KvOut* kvo = nullptr, float* lin_st = nullptr) {
   const int d = m->cfg.d, F = m->cfg.ffn_dim, R = nb * per;
   const bool bf = m->bf16;
   const size_t e = bf ? 2 : 4;
   const float scale = 1.0f / sqrtf((float)(d / m->cfg.n_heads));
-  if (bf && self_attention_fits(d, m->cfg.n_heads, per)) {
+  if (lin_st) {
+    // LN1 and q|k|v, the per-head state of the batch's keys and values, then every query row
+    GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
+    g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
+    fe_status st0 = run_proj(m, g, s);
+    if (st0 != FE_OK) return st0;
+    const int H = m->cfg.n_heads, dh = d / H;
+    const char* qkv = static_cast<const char*>(b.qkv);
+    FE_LAUNCH(F_ATTN, s, launch_lin_state(qkv + d * e, qkv + 2 * d * e, (long long)per * 3 * d, 3 * d, nb, per, nvalid,
+                                          H, dh, lin_st, bf, s));
+    FE_LAUNCH(F_ATTN, s, launch_lin_apply(qkv, 3 * d, lin_st, nb, per, nvalid, H, dh, b.O, d, bf, s));
+  } else if (bf && self_attention_fits(d, m->cfg.n_heads, per)) {
     // LN1, q|k|v of one head and attention in one kernel per (batch, head)
     SelfAttnArgs sa{xin, xin_f32, nb, per, nvalid, w.ln1g, w.ln1b, w.wqkv, w.bqkv, b.O, m->cfg.n_heads, scale};
     FE_LAUNCH(F_ATTN, s, launch_self_attention(sa, d, s));
@@ -654,6 +683,14 @@ fe_status fe_workspace_size(const fe_model* m, int B, int T, int M, int K, int L
   return FE_OK;
 }
 
+fe_status fe_kv_size(const fe_model* m, int B, int T, size_t* bytes) {
+  fe_status st = check_dims(m, B, T, 1, 1, 1);
+  if (st != FE_OK) return st;
+  if (!bytes) return fail(FE_EINVAL, "bytes is NULL");
+  *bytes = kv_bytes(m, B, T);
+  return FE_OK;
+}
+
 fe_status fe_read_device_status(const fe_model* m, const void* ws, int B, void* stream, int32_t* host_out) {
   if (!m || !ws || !host_out || B < 1) return fail(FE_EINVAL, "bad arguments to fe_read_device_status");
   std::vector<int32_t> tmp(2 * (size_t)B);
@@ -691,35 +728,54 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
     src = at<char>(ws, w.c_xin);
   }
   Bufs b{at<float>(ws, w.c_x), at<char>(ws, w.c_qkv), at<char>(ws, w.c_o), at<char>(ws, w.c_h)};
-  const bool whole = module_fits(m, T);
+  // linear models: the item layers' keys and values go to the workspace first, and kv receives
+  // their per-head state
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  float* lin_st = lin ? at<float>(ws, w.lin_st) : nullptr;
+  void* kvp = lin ? at<char>(ws, w.c_kvp) : kv;
+  const bool whole = !lin && module_fits(m, T);
   if (whole) {
     st = run_module(m, m->ctx, B, T, src, false, m->ctx_lnf_g, m->ctx_lnf_b, b.X, false, s);
     if (st != FE_OK) return st;
   } else {
     // on bf16 models the last block's tail also applies the final LayerNorm and writes the
-    // key/value cache of every item layer
-    const KvOut kvo{m->ctx_lnf_g, m->ctx_lnf_b, m->wkv, m->bkv, kv, m->cfg.n_layers,
+    // key/value projections of every item layer
+    const KvOut kvo{m->ctx_lnf_g, m->ctx_lnf_b, m->wkv, m->bkv, kvp, m->cfg.n_layers,
                     clear_late ? status_ctx : nullptr, B};
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       const bool last = l + 1 == m->cfg.n_layers;
-      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s, bf && last ? &kvo : nullptr);
+      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s, bf && last ? &kvo : nullptr, lin_st);
       if (st != FE_OK) return st;
     }
-    if (bf) return FE_OK;
   }
-  // key/value projections of all item layers, with the context module's final LayerNorm fused
-  // into their prologue unless the module kernel already applied it
-  GemmArgs g = gemm(b.X, d, true, R, d, 2 * m->cfg.n_layers * d, m->wkv, m->bkv, kv, d, false, EPI_STORE);
-  if (!whole) {
-    g.ln_g = m->ctx_lnf_g;
-    g.ln_b = m->ctx_lnf_b;
+  if (!bf || whole) {
+    // key/value projections of all item layers, with the context module's final LayerNorm fused
+    // into their prologue unless the module kernel already applied it
+    GemmArgs g = gemm(b.X, d, true, R, d, 2 * m->cfg.n_layers * d, m->wkv, m->bkv, kvp, d, false, EPI_STORE);
+    if (!whole) {
+      g.ln_g = m->ctx_lnf_g;
+      g.ln_b = m->ctx_lnf_b;
+    }
+    g.col_block = d; g.col_block_stride = (long long)R * d;
+    if (clear_late) {
+      g.zero = status_ctx;
+      g.zero_n = B;
+    }
+    st = run_proj(m, g, s);
+    if (st != FE_OK) return st;
   }
-  g.col_block = d; g.col_block_stride = (long long)R * d;
-  if (clear_late) {
-    g.zero = status_ctx;
-    g.zero_n = B;
+  if (lin) {
+    // the linear-attention cache: per item layer and head, sum_t phi(k_t) v_t^T and sum_t phi(k_t)
+    const int H = m->cfg.n_heads, dh = d / H;
+    const size_t e = bf ? 2 : 4;
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      const char* K = static_cast<const char*>(kvp) + (size_t)(2 * l) * R * d * e;
+      const char* V = static_cast<const char*>(kvp) + (size_t)(2 * l + 1) * R * d * e;
+      float* out = static_cast<float*>(kv) + (size_t)l * B * H * (dh + 1) * dh;
+      FE_LAUNCH(F_ATTN, s, launch_lin_state(K, V, (long long)T * d, d, B, T, nullptr, H, dh, out, bf, s));
+    }
   }
-  return run_proj(m, g, s);
+  return FE_OK;
 }
 
 fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, const int32_t* lists, int K, int L,
@@ -782,9 +838,10 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       a.scale = 1.0f / sqrtf((float)dh);
       FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
     }
+    const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
     const void* Kc = static_cast<const char*>(kv) + (size_t)(2 * l) * B * T * d * e;
     const void* Vc = static_cast<const char*>(kv) + (size_t)(2 * l + 1) * B * T * d * e;
-    if (bf && cross_attention_fits(d, m->cfg.n_heads, Ucap, T)) {
+    if (!lin && bf && cross_attention_fits(d, m->cfg.n_heads, Ucap, T)) {
       // x1 = x + O Wo + bo -> G1, queries LN2(x1) Wq + bq and the cross-attention in one kernel
       // per (request, head); its output goes to Qc (every head's workgroup reads all of O)
       CrossAttnArgs ca{O, xin, xin_f32, G1, B, Ucap, n_uniq, iw.wo, iw.bo, iw.ln2g, iw.ln2b, iw.wq, iw.bq,
@@ -813,15 +870,21 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       st = run_proj(m, g, s);
       if (st != FE_OK) return st;
     }
-    AttnArgs c{};
-    c.Q = Qc; c.q_bs = (long long)Ucap * d; c.q_rs = d;
-    c.K = Kc; c.k_bs = (long long)T * d; c.k_rs = d;
-    c.V = Vc; c.v_bs = (long long)T * d; c.v_rs = d;
-    c.O = O; c.o_bs = (long long)Ucap * d; c.o_rs = d;
-    c.B = B; c.nq = Ucap; c.nk = T; c.n_heads = m->cfg.n_heads; c.dh = dh;
-    c.q_valid = n_uniq; c.k_valid = nullptr;
-    c.scale = 1.0f / sqrtf((float)dh);
-    FE_LAUNCH(F_ATTN, s, launch_attention(c, bf, s));
+    if (lin) {
+      // linear attention of the queries against item layer l's context state
+      const float* stl = static_cast<const float*>(kv) + (size_t)l * B * m->cfg.n_heads * (dh + 1) * dh;
+      FE_LAUNCH(F_ATTN, s, launch_lin_apply(Qc, d, stl, B, Ucap, n_uniq, m->cfg.n_heads, dh, O, d, bf, s));
+    } else {
+      AttnArgs c{};
+      c.Q = Qc; c.q_bs = (long long)Ucap * d; c.q_rs = d;
+      c.K = Kc; c.k_bs = (long long)T * d; c.k_rs = d;
+      c.V = Vc; c.v_bs = (long long)T * d; c.v_rs = d;
+      c.O = O; c.o_bs = (long long)Ucap * d; c.o_rs = d;
+      c.B = B; c.nq = Ucap; c.nk = T; c.n_heads = m->cfg.n_heads; c.dh = dh;
+      c.q_valid = n_uniq; c.k_valid = nullptr;
+      c.scale = 1.0f / sqrtf((float)dh);
+      FE_LAUNCH(F_ATTN, s, launch_attention(c, bf, s));
+    }
     if (bf) {
       // the last layer also applies the module's final LayerNorm and writes H directly
       const bool last = l + 1 == m->cfg.n_layers;
@@ -869,10 +932,13 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   float* c = at<float>(ws, w.s_c);
   st = seq_encode(m, B, K, L, seq, c, b, s);
   if (st != FE_OK) return st;
-  if (module_fits(m, K)) return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  if (!lin && module_fits(m, K))
+    return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
   Bufs bc{c, b.qkv, b.O, b.Hf};
+  float* lin_st = lin ? at<float>(ws, w.lin_st) : nullptr;
   for (int l = 0; l < m->cfg.n_layers; ++l) {
-    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s);
+    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin_st);
     if (st != FE_OK) return st;
   }
   FE_LAUNCH(F_LN, s, launch_layernorm(c, 1, d, B * K, d, m->cross_lnf_g, m->cross_lnf_b, Cp, 1, d, bf, s));

@@ -194,6 +194,15 @@ hipError_t launch_layernorm(const void* X, int x_f32, long long x_rs, int R, int
 hipError_t launch_layernorm_masked(const void* X, int x_f32, long long x_rs, int R, int d, const float* g,
                                    const float* b, void* Y, int y_f32, long long y_rs, const int32_t* nvalid,
                                    int rpb, bool bf16_model, hipStream_t s);
+// Linear attention (phi = elu + 1).  State of keys K and values V (act) per (batch, head):
+// St [B][H][dh + 1][dh] fp32 (rows 0..dh-1: sum_t phi(k_t) v_t^T, row dh: sum_t phi(k_t)); key row t
+// of batch b at K + b*bs + t*rs + h*dh elements (V likewise), keys t < nvalid[b] (or nk).
+hipError_t launch_lin_state(const void* K, const void* V, long long bs, int rs, int B, int nk, const int32_t* nvalid,
+                            int H, int dh, float* St, bool bf16_model, hipStream_t s);
+// O[b*rpb + r][h*dh + j] = (phi(q) S)_j / (phi(q) . z) for q = Q[b*rpb + r][h*dh ..], rows r < rpb
+// and r < nvalid[b] (others untouched); row strides q_rs, o_rs (elements, 16-byte multiples).
+hipError_t launch_lin_apply(const void* Q, int q_rs, const float* St, int B, int rpb, const int32_t* nvalid, int H,
+                            int dh, void* O, int o_rs, bool bf16_model, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int n, int32_t v, hipStream_t s);
 // dst block b*reps + r = src block b (r < reps); block_bytes a multiple of 4
 hipError_t launch_repeat_blocks(const void* src, void* dst, long long block_bytes, int nblk, int reps, hipStream_t s);

@@ -18,9 +18,10 @@ LIB_PATH = os.path.join(_PKG, "libflasheval.so")
 
 FE_OK, FE_EINVAL, FE_EUNSUPPORTED, FE_ENOMEM, FE_EHIP = range(5)
 FE_F32, FE_BF16 = 0, 1
+FE_ATTN_SOFTMAX, FE_ATTN_LINEAR = 0, 1
 FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
 
-EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_last_error",
+EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_kv_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
             "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
             "fe_trace_family")
@@ -36,7 +37,7 @@ class FeError(RuntimeError):
 class fe_config(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_layers", ctypes.c_int32),
                 ("ffn_dim", ctypes.c_int32), ("max_L", ctypes.c_int32), ("vocab", ctypes.c_int32),
-                ("dtype", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("attention", ctypes.c_int32)]
 
 
 _lib = None
@@ -58,6 +59,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_model_create": (S, [cfgp, P, Z, ctypes.POINTER(P)]),
         "fe_model_destroy": (None, [P]),
         "fe_workspace_size": (S, [P, I, I, I, I, I, ctypes.POINTER(Z)]),
+        "fe_kv_size": (S, [P, I, I, ctypes.POINTER(Z)]),
         "fe_last_error": (ctypes.c_char_p, []),
         "fe_read_device_status": (S, [P, P, I, P, P]),
         "fe_encode_context": (S, [P, I, I, P, P, P, P, Z, P]),
@@ -161,6 +163,12 @@ def fe_workspace_size(model: int, B: int, T: int, M: int, K: int, L: int) -> int
     return n.value
 
 
+def fe_kv_size(model: int, B: int, T: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().fe_kv_size(model, B, T, ctypes.byref(n)), "fe_kv_size")
+    return n.value
+
+
 def fe_read_device_status(model: int, ws, B: int, stream=None) -> np.ndarray:
     out = np.zeros(B, dtype=np.int32)
     _check(load_library().fe_read_device_status(model, _ptr(ws), B, _stream(stream), out.ctypes.data),
@@ -246,12 +254,16 @@ class Evaluator:
     """
 
     def __init__(self, d: int, n_heads: int, n_layers: int, ffn_dim: int, max_L: int, vocab: int, dtype: str,
-                 params: Dict[str, np.ndarray]):
+                 params: Dict[str, np.ndarray], attention: str = "softmax"):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("Evaluator needs a HIP device")
-        self.cfg = fe_config(d, n_heads, n_layers, ffn_dim, max_L, vocab, FE_BF16 if dtype == "bf16" else FE_F32)
-        self.d, self.n_layers, self.vocab = d, n_layers, vocab
+        if attention not in ("softmax", "linear"):
+            raise ValueError(f"attention must be 'softmax' or 'linear', got {attention!r}")
+        self.cfg = fe_config(d, n_heads, n_layers, ffn_dim, max_L, vocab, FE_BF16 if dtype == "bf16" else FE_F32,
+                             FE_ATTN_LINEAR if attention == "linear" else FE_ATTN_SOFTMAX)
+        self.d, self.n_layers, self.vocab, self.n_heads = d, n_layers, vocab, n_heads
+        self.attention = attention
         self.act = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.handle = fe_model_create(self.cfg, pack_params(params, n_layers, vocab))
         self.buffers = None
@@ -277,7 +289,7 @@ class Evaluator:
         i32 = torch.int32
         self.buffers = dict(
             shape=(B, T, M, K, L), U_cap=U_cap,
-            kv=torch.empty((n, 2, B, T, d), dtype=self.act, device=dev),
+            kv=self._kv_tensor(B, T, dev),
             uniq=torch.empty((B, U_cap), dtype=i32, device=dev),
             n_uniq=torch.empty((B,), dtype=i32, device=dev),
             slot=torch.empty((B, K, L), dtype=i32, device=dev),
@@ -289,6 +301,19 @@ class Evaluator:
             ws=torch.empty((ws_bytes,), dtype=torch.uint8, device=dev),
         )
         return self.buffers
+
+    def _kv_tensor(self, B: int, T: int, dev):
+        """fe_encode_context's output: keys/values [n][2][B][T][d] act, or on linear-attention
+        models the per-head state [n][B][H][dh+1][dh] fp32 (fe_kv_size bytes either way)."""
+        import torch
+        n, d, H = self.n_layers, self.d, self.n_heads
+        if self.attention == "linear":
+            shape, dt = (n, B, H, d // H + 1, d // H), torch.float32
+        else:
+            shape, dt = (n, 2, B, T, d), self.act
+        t = torch.empty(shape, dtype=dt, device=dev)
+        assert t.numel() * t.element_size() == fe_kv_size(self.handle, B, T)
+        return t
 
     def run(self, x=None, ctx_ids=None, pool=None, lists=None, stream=None) -> Dict:
         """Enqueue the five calls on device tensors already resident on the GPU."""

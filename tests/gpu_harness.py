@@ -41,7 +41,8 @@ def score_scale(W, Cp_ref) -> float:
 
 
 def make_evaluator(cfg, W) -> fe.Evaluator:
-    return fe.Evaluator(cfg.d, cfg.n_heads, cfg.n_layers, cfg.ffn, cfg.max_L, cfg.vocab, cfg.dtype, W)
+    return fe.Evaluator(cfg.d, cfg.n_heads, cfg.n_layers, cfg.ffn, cfg.max_L, cfg.vocab, cfg.dtype, W,
+                        attention=cfg.attention)
 
 
 def upload(cfg, I: Dict) -> Dict[str, Optional[torch.Tensor]]:

@@ -58,6 +58,7 @@ def test_param_count_matches_generator(cid):
     ("ffn_dim", 320, fe.FE_EUNSUPPORTED),   # not a multiple of 128 on a bf16 model
     ("max_L", 128, fe.FE_EUNSUPPORTED),
     ("dtype", 7, fe.FE_EINVAL),
+    ("attention", 2, fe.FE_EINVAL),        # neither softmax nor linear
 ])
 def test_config_validation(field, value, status):
     c = gen.config(1)
