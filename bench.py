@@ -16,6 +16,7 @@ from __future__ import annotations
 
 import argparse
 import json
+from dataclasses import replace
 import os
 import sys
 import time
@@ -66,9 +67,12 @@ def family_flops(c, U, fam_names):
     their groups are short), "post" (output projection and FFN, or query projection, after a
     separate attention kernel, and the key/value cache in the last context tail), "attention"
     (with the q|k|v projection when the fused self-attention kernel applies), "gemm" (separate
-    projections).
+    projections), "linear" (linear attention: per head the state sum_t phi(k_t) v_t^T, 2 dh^2
+    flops per key, and its application, 2 dh (dh + 1) per query).
     """
     d, F, n, B, T, K, S = c.d, c.ffn, c.n_layers, c.B, c.T, c.K, c.L + 1
+    dh = d // c.n_heads
+    lin = c.attention == "linear"
     tile = 0 if d >= 512 else 64          # module kernel: groups of up to 64 rows, d <= 256
     rows_item = sum(U)
     out = {k: 0.0 for k in fam_names}
@@ -81,9 +85,20 @@ def family_flops(c, U, fam_names):
     def selfattn(group):   # q|k|v projection inside the attention kernel (d = 128, head width 32)
         return fused and d == 128 and d // c.n_heads == 32 and group <= 256
 
-    for rows, groups, size, first in ((B * T, B, T, False), (B * K * S, B * K, S, True), (B * K, B, K, False)):
+    def lin_state(keys):   # state of every head over `keys` key rows (z included)
+        return 2.0 * keys * d * dh + keys * d
+
+    def lin_apply(queries):
+        return 2.0 * queries * d * (dh + 1)
+
+    for name, (rows, groups, size, first) in (("ctx", (B * T, B, T, False)), ("seq", (B * K * S, B * K, S, True)),
+                                              ("cross", (B * K, B, K, False))):
         proj, attn, tail = module_parts(d, F, n, rows, groups, size, first)
-        if fused and size <= tile:
+        if lin and name != "seq":
+            add("gemm", proj)
+            add("linear", n * (lin_state(rows) + lin_apply(rows)))
+            add("post" if fused else "gemm", tail)
+        elif fused and size <= tile:
             add("layer", proj + attn + tail)
         elif fused:
             add("attention" if selfattn(size) else "gemm", proj)
@@ -93,12 +108,34 @@ def family_flops(c, U, fam_names):
             add("gemm", proj + tail)
             add("attention", attn)
     # key/value cache of the item layers: in the last context tail when that tail is fused
-    add("post" if fused and T > tile else "gemm", 4.0 * n * B * T * d * d)
+    add("post" if fused and (lin or T > tile) else "gemm", 4.0 * n * B * T * d * d)
+    if lin:
+        add("linear", n * lin_state(B * T))       # the cache's per-head state, per item layer
     # distinct items: q|k|v, self-attention, output + query projections, cross-attention, FFN
-    add("attention", sum(n * (4.0 * u * u * d + 4.0 * u * T * d) for u in U))
+    add("attention", sum(n * 4.0 * u * u * d for u in U))
+    if lin:
+        add("linear", n * lin_apply(rows_item))
+    else:
+        add("attention", sum(n * 4.0 * u * T * d for u in U))
     add("attention" if selfattn(min(c.M, K * c.L)) else "gemm", n * 6.0 * d * d * rows_item)
     add("post" if fused else "gemm", n * (6.0 * d * d + 4.0 * d * F) * rows_item)
     return out
+
+
+def linear_bytes(c, U):
+    """Algorithmic HBM bytes of the linear-attention kernels in one pass: each state kernel reads
+    the keys and values once and writes the fp32 state; each apply kernel reads the queries and
+    the state and writes the output rows."""
+    d, n, B, T, K = c.d, c.n_layers, c.B, c.T, c.K
+    H, dh = c.n_heads, c.d // c.n_heads
+    esz = 2 if c.dtype == "bf16" else 4
+    st = lambda groups: groups * H * (dh + 1) * dh * 4
+    total = 0.0
+    for rows, groups in ((B * T, B), (B * K, B)):                 # context, cross-sequence modules
+        total += n * (2 * rows * d * esz + st(groups) + rows * d * esz + st(groups) + rows * d * esz)
+    total += n * (2 * B * T * d * esz + st(B))                     # the item layers' context state
+    total += n * (2 * sum(U) * d * esz + st(B))                    # the items' cross-attention
+    return total
 
 
 def naive_flops(c, U):
@@ -195,6 +232,48 @@ def measured_traffic(family: str):
     return t.get("bytes_per_launch")
 
 
+MATRIX_FAMILIES = ("gemm", "ffn", "attention", "layer", "post")
+
+
+def stage_table(c, U, fam, steps):
+    """Per kernel family: time per step, launches, mean launch time; TFLOP/s and the MFMA
+    fraction of the matrix-product families; GB/s and the HBM fraction of the linear-attention
+    kernels (bandwidth-bound: a few flops per byte of keys, values and queries)."""
+    stages = {}
+    for name, (ms, n) in fam.items():
+        if n == 0:
+            continue
+        stages[name] = {"ms_per_step": round(ms / steps, 5), "launches_per_step": n // steps,
+                        "avg_launch_us": round(ms * 1e3 / n, 3)}
+    peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
+    flops = family_flops(c, U, set(stages))
+    for name in MATRIX_FAMILIES:
+        if name in stages and flops.get(name, 0.0) > 0:
+            tf = flops[name] / (fam[name][0] / steps / 1e3) / 1e12
+            stages[name].update(tflops=round(tf, 2), mfma_frac=round(tf / peak, 4))
+    if "linear" in stages:
+        nbytes = linear_bytes(c, U)
+        gbs = nbytes / (fam["linear"][0] / steps / 1e3) / 1e9
+        stages["linear"].update(bytes_per_step=int(nbytes), GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
+                                gflops_per_step=round(flops.get("linear", 0.0) / 1e9, 3))
+    return stages, flops
+
+
+def time_pass(step, stream, steps, warmup):
+    """Mean device time of `steps` back-to-back passes (after `warmup`), in ms."""
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
 def copy_calibration() -> int:
     """A plain elementwise copy of 256 MiB (fp32 x 1.0), three times: reads and writes 256 MiB each."""
     import torch
@@ -215,6 +294,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=1, choices=[1, 2, 3, 4])
     ap.add_argument("--K", type=int, default=None, help="lists per request for workload 2")
+    ap.add_argument("--attention", choices=["softmax", "linear"], default="softmax",
+                    help="attention form of the model (linear: the kernelized variant of Appendix B.3)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the traced pass (for profiler runs)")
@@ -245,6 +326,7 @@ def main() -> int:
         return 1
     torch.cuda.set_device(0)
     c = gen.config(args.workload, K=args.K) if args.workload == 2 else gen.config(args.workload)
+    c = replace(c, attention=args.attention)
     W, I = gen.make_weights(c), gen.make_inputs(c)
     ev = fe.Evaluator(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, c.dtype, W, attention=c.attention)
     bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
@@ -381,7 +463,8 @@ def main() -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": c.dtype,
         "data": "synthetic (seeded; random-init weights)",
         "config": {"workload": f"{c.name}: B={c.B} T={c.T} d={c.d} heads={c.n_heads} layers={c.n_layers} "
-                               f"F={c.ffn} M={c.M} K={c.K} L={c.L}",
+                               f"F={c.ffn} M={c.M} K={c.K} L={c.L}"
+                               + (" (linear attention)" if c.attention == "linear" else ""),
                    "B": c.B, "T": c.T, "d": c.d, "M": c.M, "K": c.K, "L": c.L, "parallelism": "none (1 GPU)"},
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
@@ -393,18 +476,8 @@ def main() -> int:
         "U_mean": round(float(np.mean(U)), 2), "rho": round(c.K * c.L / float(np.mean(U)), 3),
     }
     if fam:
-        stages = {}
-        for name, (ms, n) in fam.items():
-            if n == 0:
-                continue
-            stages[name] = {"ms_per_step": round(ms / args.steps, 5), "launches_per_step": n // args.steps,
-                            "avg_launch_us": round(ms * 1e3 / n, 3)}
         peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
-        flops = family_flops(c, U, set(stages))
-        for name in ("gemm", "ffn", "attention", "layer", "post"):
-            if name in stages and flops.get(name, 0.0) > 0:
-                tf = flops[name] / (fam[name][0] / args.steps / 1e3) / 1e12
-                stages[name].update(tflops=round(tf, 2), mfma_frac=round(tf / peak, 4))
+        stages, flops = stage_table(c, U, fam, args.steps)
         if "assemble" in stages:
             # per-launch events add their own overhead to a kernel this short: the back-to-back
             # average from the graph of assembly launches is the duration the fraction uses
@@ -416,7 +489,7 @@ def main() -> int:
                                       hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
                                       timing=f"mean of {5 * ASM_REPS} back-to-back launches replayed from a HIP graph",
                                       copy_reference=copy_ref)
-        dom = max(stages, key=lambda k: stages[k]["ms_per_step"])
+        dom = max((k for k in stages if k != "linear"), key=lambda k: stages[k]["ms_per_step"])
         dom_ms, dom_n = fam[dom]
         avg_s = dom_ms / dom_n / 1e3
         if flops.get(dom, 0.0) > 0:
@@ -431,12 +504,37 @@ def main() -> int:
             out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": measured_traffic(dom),
                                "avg_launch_us": round(avg_s * 1e6, 3), "launches_per_step": dom_n // args.steps}
-        mm_fams = [k for k in ("gemm", "ffn", "attention", "layer", "post") if k in stages]
+        mm_fams = [k for k in MATRIX_FAMILIES if k in stages]
         mm_ms = sum(fam[k][0] for k in mm_fams) / args.steps
         mm_flops = sum(flops.get(k, 0.0) for k in mm_fams)
         out["mfma_util_matrix_stages"] = round(mm_flops / (mm_ms / 1e3) / 1e12 / peak, 4)
         out["kernel_ms_per_step"] = round(sum(v[0] for v in fam.values()) / args.steps, 5)
         out["stages"] = stages
+    if not args.no_variants and c.attention == "softmax":
+        # the linear-attention variant (the deployment setting of Appendix B.3) on the same weights
+        # and inputs: same shapes, the context, item->context and cross-sequence attention linear
+        cl = replace(c, attention="linear")
+        ev_lin = fe.Evaluator(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, c.dtype, W, attention="linear")
+        ev_lin.allocate(c.B, c.T, c.M, c.K, c.L)
+
+        def step_lin():
+            ev_lin.run(x=x, ctx_ids=ids, pool=pool, lists=lists)
+
+        lin_ms = time_pass(step_lin, stream, args.steps, args.warmup)
+        entry = {"ms_per_step": round(lin_ms, 5), "value": round(c.B * c.K / (lin_ms / 1e3), 1),
+                 "what": "same workload with linear attention (phi = elu + 1) in the context, item->context and "
+                         "cross-sequence attention; the context cache is the per-head state"}
+        if not args.no_trace:
+            fe.fe_trace_enable(True)
+            for _ in range(args.steps):
+                step_lin()
+            torch.cuda.synchronize()
+            lfam = fe.fe_trace_read()
+            fe.fe_trace_enable(False)
+            entry["stages"], _ = stage_table(cl, U, lfam, args.steps)
+        out["linear_attention"] = entry
+        ev_lin.close()
+        torch.cuda.empty_cache()
     if not args.no_naive:
         # the same network with every reuse taken out (fe_evaluate_naive), same inputs, same GPU
         ev.allocate_naive(c.B, c.T, c.M, c.K, c.L, token_ids=ids is not None)

@@ -19,13 +19,14 @@ extern "C" {
 #endif
 
 /* Kernel families, in the order of fe_trace_read's index. */
-#define FE_TRACE_FAMILIES 11
+#define FE_TRACE_FAMILIES 12
 /* 0 "gemm" (projections and the key/value cache; on fp32 models also the FFN), 1 "attention",
  * 2 "layernorm", 3 "dedup", 4 "gather", 5 "assemble", 6 "score_select", 7 "fill",
  * 8 "ffn" (kept for index stability; no kernel of this family is launched), 9 "layer" (a whole
  * encoder module -- every block and the final LayerNorm -- in one kernel, for short attention
  * groups), 10 "post" (output projection, residual, LayerNorm and FFN or query projection after
- * a separate attention kernel) */
+ * a separate attention kernel), 11 "linear" (the state and state-apply kernels of linear
+ * attention) */
 
 /* Turn tracing on (1) or off (0).  Turning it on discards earlier records. */
 fe_status fe_trace_enable(int on);

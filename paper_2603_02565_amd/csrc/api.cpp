@@ -26,9 +26,9 @@ thread_local std::string g_err;
 // ------------------------------------------------------------------------------------------
 // Kernel timing (flasheval_trace.h): events recorded around each launch while enabled.
 // ------------------------------------------------------------------------------------------
-enum Fam { F_GEMM = 0, F_ATTN, F_LN, F_DEDUP, F_GATHER, F_ASSEMBLE, F_SCORE, F_FILL, F_FFN, F_LAYER, F_POST };
+enum Fam { F_GEMM = 0, F_ATTN, F_LN, F_DEDUP, F_GATHER, F_ASSEMBLE, F_SCORE, F_FILL, F_FFN, F_LAYER, F_POST, F_LIN };
 const char* const kFamName[FE_TRACE_FAMILIES] = {"gemm", "attention", "layernorm", "dedup", "gather", "assemble",
-                                                 "score_select", "fill", "ffn", "layer", "post"};
+                                                 "score_select", "fill", "ffn", "layer", "post", "linear"};
 struct TraceRec { int fam; hipEvent_t a, b; };
 std::mutex g_trace_mu;
 bool g_trace_on = false;
@@ -462,9 +462,9 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     if (st0 != FE_OK) return st0;
     const int H = m->cfg.n_heads, dh = d / H;
     const char* qkv = static_cast<const char*>(b.qkv);
-    FE_LAUNCH(F_ATTN, s, launch_lin_state(qkv + d * e, qkv + 2 * d * e, (long long)per * 3 * d, 3 * d, nb, per, nvalid,
+    FE_LAUNCH(F_LIN, s, launch_lin_state(qkv + d * e, qkv + 2 * d * e, (long long)per * 3 * d, 3 * d, nb, per, nvalid,
                                           H, dh, lin_st, bf, s));
-    FE_LAUNCH(F_ATTN, s, launch_lin_apply(qkv, 3 * d, lin_st, nb, per, nvalid, H, dh, b.O, d, bf, s));
+    FE_LAUNCH(F_LIN, s, launch_lin_apply(qkv, 3 * d, lin_st, nb, per, nvalid, H, dh, b.O, d, bf, s));
   } else if (bf && self_attention_fits(d, m->cfg.n_heads, per)) {
     // LN1, q|k|v of one head and attention in one kernel per (batch, head)
     SelfAttnArgs sa{xin, xin_f32, nb, per, nvalid, w.ln1g, w.ln1b, w.wqkv, w.bqkv, b.O, m->cfg.n_heads, scale};
@@ -772,7 +772,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
       const char* K = static_cast<const char*>(kvp) + (size_t)(2 * l) * R * d * e;
       const char* V = static_cast<const char*>(kvp) + (size_t)(2 * l + 1) * R * d * e;
       float* out = static_cast<float*>(kv) + (size_t)l * B * H * (dh + 1) * dh;
-      FE_LAUNCH(F_ATTN, s, launch_lin_state(K, V, (long long)T * d, d, B, T, nullptr, H, dh, out, bf, s));
+      FE_LAUNCH(F_LIN, s, launch_lin_state(K, V, (long long)T * d, d, B, T, nullptr, H, dh, out, bf, s));
     }
   }
   return FE_OK;
@@ -873,7 +873,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     if (lin) {
       // linear attention of the queries against item layer l's context state
       const float* stl = static_cast<const float*>(kv) + (size_t)l * B * m->cfg.n_heads * (dh + 1) * dh;
-      FE_LAUNCH(F_ATTN, s, launch_lin_apply(Qc, d, stl, B, Ucap, n_uniq, m->cfg.n_heads, dh, O, d, bf, s));
+      FE_LAUNCH(F_LIN, s, launch_lin_apply(Qc, d, stl, B, Ucap, n_uniq, m->cfg.n_heads, dh, O, d, bf, s));
     } else {
       AttnArgs c{};
       c.Q = Qc; c.q_bs = (long long)Ucap * d; c.q_rs = d;

@@ -25,7 +25,7 @@ EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspa
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
             "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
             "fe_trace_family")
-FE_TRACE_FAMILIES = 11
+FE_TRACE_FAMILIES = 12
 
 
 class FeError(RuntimeError):

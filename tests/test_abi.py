@@ -85,5 +85,5 @@ def test_trace_toggle_without_launches():
     out = fe.fe_trace_read()
     fe.fe_trace_enable(False)
     assert set(out) == {"gemm", "attention", "layernorm", "dedup", "gather", "assemble", "score_select", "fill", "ffn",
-                        "layer", "post"}
+                        "layer", "post", "linear"}
     assert all(v == (0.0, 0) for v in out.values())
