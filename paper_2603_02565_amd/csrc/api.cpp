@@ -284,13 +284,20 @@ fe_status check_config(const fe_config* c) {
 // ------------------------------------------------------------------------------------------
 // Workspace layout
 // ------------------------------------------------------------------------------------------
+// Wide bf16 models (d >= 512) run their projections and FFNs as tiled products over LDS-staged
+// operands (gemm_tiled.hip), with LayerNorms as separate launches: there a row tile of the
+// fused kernels would stream whole weight matrices through its compute unit.
+constexpr int kWideD = 512;
+bool wide(const fe_model* m) { return m->bf16 && m->cfg.d >= kWideD; }
+
 struct Ws {
   size_t status;                                        // int32 [2][B]: items, context
   size_t lin_st;                                        // linear models: fp32 [B][H][dh+1][dh], one module's state
   size_t c_kvp;                                         // linear models: act [n][2][B][T][d] item-layer keys/values
-  size_t c_xin, c_x, c_qkv, c_o, c_h;                   // context stage
-  size_t i_g0, i_g, i_g1, i_qkv, i_o, i_q, i_h;         // item stage
-  size_t s_x, s_qkv, s_o, s_h, s_c;                     // sequence + cross stages
+  size_t c_xin, c_x, c_qkv, c_o, c_h, c_ln;             // context stage
+  size_t i_g0, i_g, i_g1, i_qkv, i_o, i_q, i_h, i_ln;   // item stage
+  size_t s_x, s_qkv, s_o, s_h, s_c, s_ln;               // sequence + cross stages
+  // *_ln: wide bf16 models only, bf16 [rows][d] LayerNorm outputs feeding the tiled products
   size_t total;
 };
 
@@ -322,6 +329,7 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     w.c_qkv = b.take(R * 3 * d * e);
     w.c_o = b.take(R * d * e);
     w.c_h = b.take(R * F * e);
+    if (wide(m)) w.c_ln = b.take(R * d * 2);
     end = std::max(end, b.at);
   }
   {  // items
@@ -335,6 +343,7 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     w.i_o = b.take(R * d * e);
     w.i_q = b.take(R * d * e);
     w.i_h = b.take(R * F * e);
+    if (wide(m)) w.i_ln = b.take(R * d * 2);
     end = std::max(end, b.at);
   }
   {  // sequences (the cross module reuses these buffers; its rows B*K are fewer)
@@ -345,6 +354,7 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     w.s_o = b.take(R * d * e);
     w.s_h = b.take(R * F * e);
     w.s_c = b.take(B * K * d * 4);
+    if (wide(m)) w.s_ln = b.take(R * d * 2);
     end = std::max(end, b.at);
   }
   w.total = (end + 255) & ~size_t(255);
@@ -423,17 +433,20 @@ GemmArgs gemm(const void* A, int lda, bool a_f32, int R, int K, int N, const voi
 }
 
 // One projection launch: packed-weight bf16 kernel or generic fp32 kernel.
-fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s);
-// X += FFN(LN(X)) on fp32 models: two generic launches through Hf.
+// lnbuf: bf16 [R][K] scratch for the LayerNorm of wide models (unused otherwise).
+fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s, void* lnbuf = nullptr);
+// X += FFN(LN(X)) on fp32 and wide bf16 models: LN, up-projection + ReLU into Hf, down-projection
+// with the residual.
 fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const float* lnb, const void* w1,
                   const float* b1, const void* w2, const float* b2, void* Hf, const int32_t* nvalid, int rpb,
-                  hipStream_t s);
+                  hipStream_t s, void* lnbuf = nullptr);
 
 struct Bufs {
   float* X;      // fp32 residual stream [rows][d]
   void* qkv;     // act [rows][3d]
   void* O;       // act [rows][d]
   void* Hf;      // act [rows][F]
+  void* ln;      // wide bf16 models: bf16 [rows][d] LayerNorm output (else unused)
 };
 
 // One pre-LN encoder block over nb batches of `per` rows; attention stays inside a batch.
@@ -458,7 +471,7 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     // LN1 and q|k|v, the per-head state of the batch's keys and values, then every query row
     GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
     g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
-    fe_status st0 = run_proj(m, g, s);
+    fe_status st0 = run_proj(m, g, s, b.ln);
     if (st0 != FE_OK) return st0;
     const int H = m->cfg.n_heads, dh = d / H;
     const char* qkv = static_cast<const char*>(b.qkv);
@@ -472,7 +485,7 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   } else {
     GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, w.wqkv, w.bqkv, b.qkv, 3 * d, false, EPI_STORE);
     g.ln_g = w.ln1g; g.ln_b = w.ln1b; g.nvalid = nvalid; g.rows_per_batch = per;
-    fe_status st0 = run_proj(m, g, s);
+    fe_status st0 = run_proj(m, g, s, b.ln);
     if (st0 != FE_OK) return st0;
     AttnArgs a{};
     a.Q = b.qkv; a.q_bs = (long long)per * 3 * d; a.q_rs = 3 * d;
@@ -484,7 +497,7 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     a.scale = scale;
     FE_LAUNCH(F_ATTN, s, launch_attention(a, bf, s));
   }
-  if (bf) {
+  if (bf && !wide(m)) {
     // output projection, residual, LN2 and FFN in one kernel
     PostArgs p{b.O, xin, xin_f32, b.X, R, per, nvalid, d, F, 0, w.wo, w.bo, w.ln2g, w.ln2b,
                w.w1, w.b1, w.w2, w.b2, nullptr, nullptr, nullptr};
@@ -504,9 +517,9 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
   }
   GemmArgs g = gemm(b.O, d, false, R, d, d, w.wo, w.bo, b.X, d, true, EPI_RESID);
   g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = nvalid; g.rows_per_batch = per;
-  fe_status st = run_proj(m, g, s);
+  fe_status st = run_proj(m, g, s, b.ln);
   if (st != FE_OK) return st;
-  return run_ffn(m, b.X, R, w.ln2g, w.ln2b, w.w1, w.b1, w.w2, w.b2, b.Hf, nvalid, per, s);
+  return run_ffn(m, b.X, R, w.ln2g, w.ln2b, w.w1, w.b1, w.w2, w.b2, b.Hf, nvalid, per, s, b.ln);
 }
 
 // Whole modules of short groups run as one kernel on bf16 models.
@@ -541,7 +554,23 @@ fe_status seq_encode(const fe_model* m, int B, int K, int L, const void* seq, fl
   return FE_OK;
 }
 
-fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s) {
+// The LayerNorm of a wide model's product input, into lnbuf (bf16), then the tiled product.
+fe_status run_wide(const fe_model* m, GemmArgs g, void* lnbuf, hipStream_t s) {
+  if (g.ln_g) {
+    if (!lnbuf) return fail(FE_EHIP, "internal: no LayerNorm buffer for a wide projection");
+    FE_LAUNCH(F_LN, s, launch_layernorm_masked(g.A, g.a_f32, g.lda, g.R, g.K, g.ln_g, g.ln_b, lnbuf, 0, g.K, g.nvalid,
+                                               g.rows_per_batch, true, s));
+    g.A = lnbuf;
+    g.a_f32 = 0;
+    g.lda = g.K;
+    g.ln_g = g.ln_b = nullptr;
+  }
+  FE_LAUNCH(F_GEMM, s, launch_gemm_tiled(g, s));
+  return FE_OK;
+}
+
+fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s, void* lnbuf) {
+  if (wide(m)) return run_wide(m, g, lnbuf, s);
   if (m->bf16) FE_LAUNCH(F_GEMM, s, launch_proj(g, s));
   else FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
   return FE_OK;
@@ -549,13 +578,19 @@ fe_status run_proj(const fe_model* m, const GemmArgs& g, hipStream_t s) {
 
 fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const float* lnb, const void* w1,
                   const float* b1, const void* w2, const float* b2, void* Hf, const int32_t* nvalid, int rpb,
-                  hipStream_t s) {
+                  hipStream_t s, void* lnbuf) {
   const int d = m->cfg.d, F = m->cfg.ffn_dim;
   GemmArgs g = gemm(X, d, true, R, d, F, w1, b1, Hf, F, false, EPI_RELU);
   g.ln_g = lng; g.ln_b = lnb; g.nvalid = nvalid; g.rows_per_batch = rpb;
-  FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
+  if (wide(m)) {
+    fe_status st = run_wide(m, g, lnbuf, s);
+    if (st != FE_OK) return st;
+  } else {
+    FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
+  }
   g = gemm(Hf, F, false, R, F, d, w2, b2, X, d, true, EPI_RESID);
   g.res = X; g.ldr = d; g.res_f32 = true; g.nvalid = nvalid; g.rows_per_batch = rpb;
+  if (wide(m)) return run_wide(m, g, lnbuf, s);
   FE_LAUNCH(F_GEMM, s, launch_gemm(g, false, s));
   return FE_OK;
 }
@@ -727,7 +762,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
                               FE_DEV_BAD_TOKEN, bf, s));
     src = at<char>(ws, w.c_xin);
   }
-  Bufs b{at<float>(ws, w.c_x), at<char>(ws, w.c_qkv), at<char>(ws, w.c_o), at<char>(ws, w.c_h)};
+  Bufs b{at<float>(ws, w.c_x), at<char>(ws, w.c_qkv), at<char>(ws, w.c_o), at<char>(ws, w.c_h), at<char>(ws, w.c_ln)};
   // linear models: the item layers' keys and values go to the workspace first, and kv receives
   // their per-head state
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
@@ -744,11 +779,12 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
                     clear_late ? status_ctx : nullptr, B};
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       const bool last = l + 1 == m->cfg.n_layers;
-      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s, bf && last ? &kvo : nullptr, lin_st);
+      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s,
+                     bf && !wide(m) && last ? &kvo : nullptr, lin_st);
       if (st != FE_OK) return st;
     }
   }
-  if (!bf || whole) {
+  if (!bf || whole || wide(m)) {
     // key/value projections of all item layers, with the context module's final LayerNorm fused
     // into their prologue unless the module kernel already applied it
     GemmArgs g = gemm(b.X, d, true, R, d, 2 * m->cfg.n_layers * d, m->wkv, m->bkv, kvp, d, false, EPI_STORE);
@@ -761,7 +797,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
       g.zero = status_ctx;
       g.zero_n = B;
     }
-    st = run_proj(m, g, s);
+    st = run_proj(m, g, s, b.ln);
     if (st != FE_OK) return st;
   }
   if (lin) {
@@ -814,6 +850,8 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
   void* O = at<char>(ws, w.i_o);
   void* Qc = at<char>(ws, w.i_q);
   void* Hf = at<char>(ws, w.i_h);
+  void* lnb = wide(m) ? at<char>(ws, w.i_ln) : nullptr;
+  const bool fused_tail = bf && !wide(m);     // k_post tails (else separate products)
   const int dh = d / m->cfg.n_heads;
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const ItemW& iw = m->item[l];
@@ -826,7 +864,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     } else {
       GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, iw.wqkv, iw.bqkv, qkv, 3 * d, false, EPI_STORE);
       g.ln_g = iw.ln1g; g.ln_b = iw.ln1b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-      st = run_proj(m, g, s);
+      st = run_proj(m, g, s, lnb);
       if (st != FE_OK) return st;
       AttnArgs a{};
       a.Q = qkv; a.q_bs = (long long)Ucap * 3 * d; a.q_rs = 3 * d;
@@ -854,7 +892,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }
-    if (bf) {
+    if (fused_tail) {
       // x1 = x + O Wo + bo -> G, and the cross-attention queries q = LN2(x1) Wq + bq -> Qc
       PostArgs p{O, xin, xin_f32, G, R, Ucap, n_uniq, d, F, 1, iw.wo, iw.bo, iw.ln2g, iw.ln2b,
                  nullptr, nullptr, nullptr, nullptr, iw.wq, iw.bq, Qc};
@@ -862,12 +900,12 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     } else {
       GemmArgs g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
       g.res = xin; g.ldr = d; g.res_f32 = xin_f32; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-      st = run_proj(m, g, s);
+      st = run_proj(m, g, s, lnb);
       if (st != FE_OK) return st;
       // cross-attention: the distinct elements are the queries, the context cache the keys/values
       g = gemm(G, d, true, R, d, d, iw.wq, iw.bq, Qc, d, false, EPI_STORE);
       g.ln_g = iw.ln2g; g.ln_b = iw.ln2b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-      st = run_proj(m, g, s);
+      st = run_proj(m, g, s, lnb);
       if (st != FE_OK) return st;
     }
     if (lin) {
@@ -885,7 +923,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       c.scale = 1.0f / sqrtf((float)dh);
       FE_LAUNCH(F_ATTN, s, launch_attention(c, bf, s));
     }
-    if (bf) {
+    if (fused_tail) {
       // the last layer also applies the module's final LayerNorm and writes H directly
       const bool last = l + 1 == m->cfg.n_layers;
       PostArgs p{O, G, 1, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
@@ -896,12 +934,12 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     }
     GemmArgs g = gemm(O, d, false, R, d, d, iw.wo2, iw.bo2, G, d, true, EPI_RESID);
     g.res = G; g.ldr = d; g.res_f32 = true; g.nvalid = n_uniq; g.rows_per_batch = Ucap;
-    st = run_proj(m, g, s);
+    st = run_proj(m, g, s, lnb);
     if (st != FE_OK) return st;
-    st = run_ffn(m, G, R, iw.ln3g, iw.ln3b, iw.w1, iw.b1, iw.w2, iw.b2, Hf, n_uniq, Ucap, s);
+    st = run_ffn(m, G, R, iw.ln3g, iw.ln3b, iw.w1, iw.b1, iw.w2, iw.b2, Hf, n_uniq, Ucap, s, lnb);
     if (st != FE_OK) return st;
   }
-  if (!bf)
+  if (!fused_tail)
     FE_LAUNCH(F_LN, s, launch_layernorm_masked(G, 1, d, R, d, m->item_lnf_g, m->item_lnf_b, H, 0, d, n_uniq, Ucap, bf, s));
   return FE_OK;
 }
@@ -928,14 +966,14 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool bf = m->bf16;
   const int d = m->cfg.d;
-  Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h)};
+  Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h), at<char>(ws, w.s_ln)};
   float* c = at<float>(ws, w.s_c);
   st = seq_encode(m, B, K, L, seq, c, b, s);
   if (st != FE_OK) return st;
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
   if (!lin && module_fits(m, K))
     return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
-  Bufs bc{c, b.qkv, b.O, b.Hf};
+  Bufs bc{c, b.qkv, b.O, b.Hf, b.ln};
   float* lin_st = lin ? at<float>(ws, w.lin_st) : nullptr;
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin_st);
@@ -953,7 +991,7 @@ fe_status fe_encode_sequences(const fe_model* m, int B, int K, int L, const void
   if (!aligned16(seq) || !aligned16(C) || !aligned16(ws)) return fail(FE_EINVAL, "pointers must be 16-byte aligned");
   const Ws w = layout(m, B, 1, 1, K, L);
   if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
-  Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h)};
+  Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h), at<char>(ws, w.s_ln)};
   return seq_encode(m, B, K, L, seq, C, b, static_cast<hipStream_t>(stream));
 }
 

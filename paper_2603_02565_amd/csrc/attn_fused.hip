@@ -43,6 +43,15 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
   if (a.nvalid) n = min(n, a.nvalid[b]);
   if (n <= 0) return;                                // uniform over the workgroup
   const int nrb = (n + 31) / 32;                     // 32-row blocks that hold valid rows
+  // the weight fragments of this wave's first projection block (step 2), requested now so that
+  // their latency hides behind LN1
+  const bf16x8* Wqkv = static_cast<const bf16x8*>(a.wqkv);
+  bf16x8 wfirst[KS];
+  if (wave < 3 * nrb) {
+    const int cbg = (wave % 3) * a.n_heads + h;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) wfirst[ks] = Wqkv[((long long)cbg * KS + ks) * 64 + lane];
+  }
 
   // ---- 1. LN1 of rows 0 .. 32*nrb - 1 (rows >= n are zero) -------------------------------
   if (tid < D / 4) {
@@ -106,13 +115,12 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
 
   // ---- 2. q, k, v of head h: block i = 3*rb + j (j = 0 q, 1 k, 2 v) on wave i % 16 ---------
   {
-    const bf16x8* W = static_cast<const bf16x8*>(a.wqkv);
     for (int i = wave; i < 3 * nrb; i += NT / 64) {
       const int rb = i / 3, j = i % 3;
       const int cbg = j * a.n_heads + h;             // global 32-column block of the projection
       bf16x8 wf[KS], af[KS];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) wf[ks] = W[((long long)cbg * KS + ks) * 64 + lane];
+      for (int ks = 0; ks < KS; ++ks) wf[ks] = i == wave ? wfirst[ks] : Wqkv[((long long)cbg * KS + ks) * 64 + lane];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) af[ks] = a_frag(As, LDA, rb * 32, ks * 16, lane);
       f32x16 acc = {};
@@ -297,6 +305,15 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
   if (n <= 0) return;                                // uniform over the workgroup
   const int nrb = (n + 31) / 32;
   const int nk = a.T, nkb = (nk + 31) / 32;
+  // Wo fragments of this wave's column block, requested first: their latency hides behind the
+  // staging below
+  const int cb = wave & 3, rb0 = wave >> 2;
+  bf16x8 wf[KS];
+  {
+    const bf16x8* W = static_cast<const bf16x8*>(a.wo);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) wf[ks] = W[((long long)cb * KS + ks) * 64 + lane];
+  }
   if (tid < D) {   // the block's vectors, read after the first barrier
     const int v = tid / (D / 4), o = (tid % (D / 4)) * 4;
     const float* src = v == 0 ? a.bo : v == 1 ? a.ln2g : v == 2 ? a.ln2b : a.bq;
@@ -328,7 +345,6 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
   }
   // ---- residual rows: wave w holds column block cb = w % 4 of row blocks w/4 and w/4 + 4, in
   //      the transposed accumulator layout (row rb*32 + lane%32, columns cb*32 + 8q + 4(lane/32) + e)
-  const int cb = wave & 3, rb0 = wave >> 2;
   const int colq = cb * 32 + 4 * (lane >> 5);       // + 8q
   f32x16 x[2];
 #pragma unroll
@@ -365,10 +381,6 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
 
   // ---- x1 = x + O Wo + bo ------------------------------------------------------------------
   {
-    const bf16x8* W = static_cast<const bf16x8*>(a.wo);
-    bf16x8 wf[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) wf[ks] = W[((long long)cb * KS + ks) * 64 + lane];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int rb = rb0 + 4 * i;
@@ -386,6 +398,13 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
         x[i][4 * q + 3] += acc[4 * q + 3] + bb.w;
       }
     }
+  }
+  // Wq fragments of head h for the query step, requested before LN2
+  bf16x8 wqf[KS];
+  if (wave < nrb) {
+    const bf16x8* W = static_cast<const bf16x8*>(a.wq);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) wqf[ks] = W[((long long)h * KS + ks) * 64 + lane];
   }
   // the head-0 workgroup writes x1 of the valid rows as the new residual stream
   if (h == 0) {
@@ -447,13 +466,11 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
 
   // ---- q of head h = LN2(x1) Wq + bq: row block `wave` ------------------------------------
   if (wave < nrb) {
-    const bf16x8* W = static_cast<const bf16x8*>(a.wq);
     const int rb = wave, row = rb * 32 + (lane & 31);
     f32x16 acc = {};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(W[((long long)h * KS + ks) * 64 + lane],
-                                                    a_frag(As, LDA, rb * 32, ks * 16, lane), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wqf[ks], a_frag(As, LDA, rb * 32, ks * 16, lane), acc, 0, 0, 0);
     const float* bias = s_vec + 3 * D + h * DH;
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {

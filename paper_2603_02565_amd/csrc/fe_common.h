@@ -187,6 +187,10 @@ hipError_t launch_module_small(ModuleArgs a, hipStream_t s);
 hipError_t launch_post(const PostArgs& a, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s);   // fp32 models
 hipError_t launch_proj(const GemmArgs& a, hipStream_t s);                    // bf16 models, K = d
+// bf16 models with d >= 256: 128 x 128 tiles, LDS-staged operands; A bf16 without LayerNorm
+// (ln_g == nullptr), K a multiple of 64, N of 128.
+bool gemm_tiled_fits(int K, int N);
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, bool bf16_model, hipStream_t s);
 hipError_t launch_layernorm(const void* X, int x_f32, long long x_rs, int R, int d, const float* g,
                             const float* b, void* Y, int y_f32, long long y_rs, bool bf16_model,

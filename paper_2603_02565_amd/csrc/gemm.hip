@@ -158,6 +158,62 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
+// Row r of a wide model (d = 512 NC): each lane holds 8 consecutive values of every 512-column
+// chunk (16- or 32-byte loads and stores), all indices compile-time.
+template <typename T, int NC>
+FE_DEV void ln_row_wide(const void* X, int x_f32, long long x_rs, int r, const float* g, const float* b, void* Y,
+                        int y_f32, long long y_rs, bool valid, int lane) {
+  constexpr int D = 512 * NC;
+  float v[8 * NC];
+  float sum = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int k = c * 512 + lane * 8;
+    if (x_f32 || sizeof(T) == 4) {
+      const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(X) + (size_t)r * x_rs + k);
+      const float4 t0 = src[0], t1 = src[1];
+      v[8 * c] = t0.x; v[8 * c + 1] = t0.y; v[8 * c + 2] = t0.z; v[8 * c + 3] = t0.w;
+      v[8 * c + 4] = t1.x; v[8 * c + 5] = t1.y; v[8 * c + 6] = t1.z; v[8 * c + 7] = t1.w;
+    } else {
+      const bf16x8 t = *reinterpret_cast<const bf16x8*>(static_cast<const bf16*>(X) + (size_t)r * x_rs + k);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[8 * c + j] = (float)t[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sum += v[8 * c + j];
+  }
+  const float mean = wave_sum(sum) * (1.f / D);
+  float sq = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8 * NC; ++t) { const float dl = v[t] - mean; sq += dl * dl; }
+  const float rstd = rsqrtf(wave_sum(sq) * (1.f / D) + 1e-5f);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int k = c * 512 + lane * 8;
+    const float4 g0 = *reinterpret_cast<const float4*>(g + k), g1 = *reinterpret_cast<const float4*>(g + k + 4);
+    const float4 b0 = *reinterpret_cast<const float4*>(b + k), b1 = *reinterpret_cast<const float4*>(b + k + 4);
+    const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+    const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+    float y[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) y[j] = valid ? (v[8 * c + j] - mean) * rstd * gg[j] + bb[j] : 0.f;
+    if (y_f32) {
+      float4* dst = reinterpret_cast<float4*>(static_cast<float*>(Y) + (size_t)r * y_rs + k);
+      dst[0] = make_float4(y[0], y[1], y[2], y[3]);
+      dst[1] = make_float4(y[4], y[5], y[6], y[7]);
+    } else if constexpr (sizeof(T) == 2) {
+      bf16x8 o;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = (bf16)y[j];
+      *reinterpret_cast<bf16x8*>(static_cast<bf16*>(Y) + (size_t)r * y_rs + k) = o;
+    } else {
+      float4* dst = reinterpret_cast<float4*>(static_cast<float*>(Y) + (size_t)r * y_rs + k);
+      dst[0] = make_float4(y[0], y[1], y[2], y[3]);
+      dst[1] = make_float4(y[4], y[5], y[6], y[7]);
+    }
+  }
+}
+
 // One wave per row: Y = LN(X), padding rows (per nvalid) written as zeros.
 template <typename T>
 __global__ __launch_bounds__(256) void k_layernorm(const void* X, int x_f32, long long x_rs, int R, int d,
@@ -167,6 +223,14 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* X, int x_f32, lon
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= R) return;
   const bool valid = !nvalid || (r % rpb) < nvalid[r / rpb];
+  if (d == 512) {
+    ln_row_wide<T, 1>(X, x_f32, x_rs, r, g, b, Y, y_f32, y_rs, valid, lane);
+    return;
+  }
+  if (d == 1024) {
+    ln_row_wide<T, 2>(X, x_f32, x_rs, r, g, b, Y, y_f32, y_rs, valid, lane);
+    return;
+  }
   float vals[16];
   int nv = 0;
   float sum = 0.f;
@@ -185,10 +249,15 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* X, int x_f32, lon
   const float rstd = rsqrtf(wave_sum(sq) / (float)d + 1e-5f);
   nv = 0;
   for (int k = lane * 4; k < d; k += 256, ++nv) {
-    for (int j = 0; j < 4; ++j) {
-      const float y = valid ? (vals[nv * 4 + j] - mean) * rstd * g[k + j] + b[k + j] : 0.f;
-      if (y_f32) static_cast<float*>(Y)[(size_t)r * y_rs + k + j] = y;
-      else static_cast<T*>(Y)[(size_t)r * y_rs + k + j] = from_f32<T>(y);
+    float y[4];
+    for (int j = 0; j < 4; ++j) y[j] = valid ? (vals[nv * 4 + j] - mean) * rstd * g[k + j] + b[k + j] : 0.f;
+    if (y_f32) {
+      *reinterpret_cast<float4*>(static_cast<float*>(Y) + (size_t)r * y_rs + k) = make_float4(y[0], y[1], y[2], y[3]);
+    } else {
+      T o[4];
+      for (int j = 0; j < 4; ++j) o[j] = from_f32<T>(y[j]);
+      if constexpr (sizeof(T) == 2) *reinterpret_cast<bf16x4*>(static_cast<T*>(Y) + (size_t)r * y_rs + k) = *reinterpret_cast<const bf16x4*>(o);
+      else *reinterpret_cast<float4*>(static_cast<T*>(Y) + (size_t)r * y_rs + k) = *reinterpret_cast<const float4*>(o);
     }
   }
 }

@@ -435,7 +435,7 @@ struct ModuleSmem {
 // n_layers encoder blocks and the final LayerNorm over a tile of whole groups; one launch per
 // module.  Per block: LN1 -> As; q|k|v -> LDS; attention per (group, head) -> As; x += O Wo + bo;
 // LN2 -> As; x += FFN.  The fp32 residual x never leaves registers; the result leaves as fp32.
-template <int TM, int D, int DH, int NKB, bool CLS, int G>
+template <int TM, int D, int DH, int NKB, bool CLS, int G, int NCH = 0>
 __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleArgs a) {
   static_assert(G == 1 || !CLS, "the compacted last block runs on one wave group");
   using L = ModuleSmem<TM, D>;
@@ -493,7 +493,7 @@ __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleA
     go.start(w.wo);
     lds_barrier();
     group_attention<D, DH, NKB, false, 4 * G>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
-    FfnStream<TMG, D> ffn;
+    FfnStream<TMG, D, NCH, NCH ? 3 : 2> ffn;
     ffn.start(w.w1, w.w2, a.F);
     lds_barrier();
     go.run(Ag, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TMG, D>(x, jj, rb, acc, vec + V::O); });
@@ -773,15 +773,15 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   }
 }
 
-template <int TM, int D, int DH, bool CLS, int G>
+template <int TM, int D, int DH, bool CLS, int G, int NCH = 0>
 hipError_t launch_module_c(const ModuleArgs& a, hipStream_t s) {
   const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
   const dim3 grid(tiles), block(WG * G);
   switch ((a.S + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1, CLS, G>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2, CLS, G>), grid, block, 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3, CLS, G>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4, CLS, G>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((k_module_small<TM, D, DH, 1, CLS, G, NCH>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_module_small<TM, D, DH, 2, CLS, G, NCH>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_module_small<TM, D, DH, 3, CLS, G, NCH>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_module_small<TM, D, DH, 4, CLS, G, NCH>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -796,6 +796,9 @@ hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
   if (a.first_row_only) return launch_module_c<TM, D, DH, true, 1>(a, s);
   if constexpr (D == 128) {   // at d = 256 two groups per compute unit would spill registers
     const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
+    // two wave groups leave room in the register budget for a three-stage FFN weight stream
+    // when the FFN width is fixed at 4d
+    if (tiles <= 128 && a.F == 4 * D) return launch_module_c<TM, D, DH, false, 2, 4>(a, s);
     if (tiles <= 128) return launch_module_c<TM, D, DH, false, 2>(a, s);
   }
   return launch_module_c<TM, D, DH, false, 1>(a, s);
