@@ -93,7 +93,7 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
     q += __shfl_xor(q, 1, 64);
     q += __shfl_xor(q, 2, 64);
     const float rstd = rsqrtf(q * (1.f / D) + 1e-5f), nm = -mean * rstd;
-    __syncthreads();                                 // s_g, s_b visible
+    lds_barrier();                                   // s_g, s_b visible
     if (r < 32 * nrb) {
       // element index of v[i]: fp32 rows hold float4 (i/4)*TPR + part, bf16 rows bf16x8 (i/8)*TPR + part
 #pragma unroll
@@ -111,7 +111,7 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- 2. q, k, v of head h: block i = 3*rb + j (j = 0 q, 1 k, 2 v) on wave i % 16 ---------
   {
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- 3. attention: query tile `wave`, every key in LDS ----------------------------------
   const int q0 = wave * 16;
@@ -377,7 +377,7 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) Vt[(d0 + i) * VLD + key] = v[i];
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- x1 = x + O Wo + bo ------------------------------------------------------------------
   {
@@ -438,7 +438,7 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
       s_stat[cb * NR + rb * 32 + lane] =
           make_float2(0.5f * (ma + mb), __uint_as_float(pq[0]) + __uint_as_float(pq[1]) + dm * dm * 8.f);
   }
-  __syncthreads();                                   // also retires every read of As (O)
+  lds_barrier();                                     // also retires every read of As (O)
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int rb = rb0 + 4 * i, row = rb * 32 + (lane & 31);
@@ -462,7 +462,7 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
       *reinterpret_cast<bf16x4*>(&As[row * LDA + c]) = o;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- q of head h = LN2(x1) Wq + bq: row block `wave` ------------------------------------
   if (wave < nrb) {
@@ -484,7 +484,7 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
       *reinterpret_cast<bf16x4*>(&Qs[row * QLD + c]) = o;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- attention over the context keys ----------------------------------------------------
   tile_attention<D, DH, NR>(Qs, Ks, Vt, n, nk, a.scale * kLog2e,

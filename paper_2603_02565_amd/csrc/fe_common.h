@@ -52,6 +52,23 @@ FE_DEV int xcd_tile(int i, int n) {
 FE_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 FE_DEV void vmem_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// OR of `pred` over the workgroup of NW waves with an LDS-only barrier: unlike
+// __syncthreads_or it neither reads the dispatch packet nor waits for outstanding vector-memory
+// loads, so prefetches issued before it stay in flight.  LDS writes made before it are visible to
+// the whole workgroup after it.
+template <int NW>
+FE_DEV bool block_any(int pred) {
+  static_assert(NW >= 1 && NW <= 16, "at most 16 waves");
+  __shared__ int s_wany[NW];
+  const bool w = __any(pred);
+  if ((threadIdx.x & 63) == 0) s_wany[threadIdx.x >> 6] = w;
+  lds_barrier();
+  int r = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) r |= s_wany[i];
+  return r != 0;
+}
+
 FE_DEV float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

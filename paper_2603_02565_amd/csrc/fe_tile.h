@@ -105,7 +105,7 @@ FE_DEV bool mark_rows(int row0, int R, const int32_t* nvalid, int rpb, int* s_va
     if (v && nvalid) v = (r % rpb) < nvalid[r / rpb];
     s_valid[threadIdx.x] = v;
   }
-  return __syncthreads_or(v);
+  return block_any<WG / 64>(v);
 }
 
 

@@ -31,12 +31,12 @@ __global__ __launch_bounds__(WG, 2) void k_proj(GemmArgs a) {
   if (a.zero && blockIdx.x == 0 && blockIdx.y == 0)
     for (int i = threadIdx.x; i < a.zero_n; i += WG) a.zero[i] = 0;
 
-  ColGemm<TM, D, NCB> gq;
-  gq.start(static_cast<const bf16x8*>(a.Wt) + (long long)cb0 * KS * 64);
   copy_ln_params<D>(a.ln_g, a.ln_b, s_g, s_b);
   if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
+  ColGemm<TM, D, NCB> gq;
+  gq.start(static_cast<const bf16x8*>(a.Wt) + (long long)cb0 * KS * 64);
   stage_rows<TM, D>(a.A, a.a_f32, a.lda, row0, s_valid, a.ln_g ? s_g : nullptr, s_b, As);
-  __syncthreads();
+  lds_barrier();
   bf16* C = static_cast<bf16*>(a.C);
   bf16* st = Cs + wave * 32 * 40;
   gq.run(As, LD, [&](int, int cb, int rb, const f32x16& acc) {

@@ -462,13 +462,15 @@ __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleA
   const long long row0 = (long long)g0 * a.S;
   const int nrows = ng * a.S;
 
+  if (nrows <= 0) return;                              // uniform; the grid has no empty tiles
+  if (threadIdx.x < TM) s_valid[threadIdx.x] = (int)threadIdx.x < nrows;
+  lds_barrier();                                       // LDS only: nothing outstanding is waited for
   // layer 0's vectors: DMA into LDS, published by the statistics barrier of the first LN1
   vecs_dma<D>(a.layer[0], s_vec[0]);
-  ColGemm<TMG, D, 3 * D / 32> gq;
-  gq.start(a.layer[0].wqkv);
-  if (!mark_rows<TM>(0, nrows, nullptr, 1, s_valid)) return;
   Resid<TMG, D> x;
   resid_load<TMG, D>(x, a.Xin, a.xin_f32, row0 + gr * TMG, validg);
+  ColGemm<TMG, D, 3 * D / 32> gq;
+  gq.start(a.layer[0].wqkv);
   vmem_wait();
 
   using V = Vecs<D>;
@@ -693,12 +695,12 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
 
   if (a.zero && blockIdx.x == 0)
     for (int e = threadIdx.x; e < a.zero_n; e += WG) a.zero[e] = 0;
-  ColGemm<TM, D, D / 32> go;
-  go.start(a.wo);
   if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) {
     if (TAIL == 0 && a.Hout) zero_rows_bf16<TM, D>(static_cast<bf16*>(a.Hout), row0, a.R, nullptr);
     return;
   }
+  ColGemm<TM, D, D / 32> go;
+  go.start(a.wo);
   stage_rows<TM, D>(a.O, false, D, row0, s_valid, nullptr, nullptr, As);
   Resid<TM, D> x;
   resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
