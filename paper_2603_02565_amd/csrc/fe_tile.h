@@ -168,6 +168,9 @@ struct ColGemm {
       for (int kk = 0; kk < KB; ++kk)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) af[kk][rb] = a_frag(As, lda, rb * 32, (sk * KB + kk) * 16, lane);
+      // every LDS read of the stage is issued before its first product, so the reads overlap
+      // each other and the products wait only for the ones they consume
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int kk = 0; kk < KB; ++kk)
 #pragma unroll

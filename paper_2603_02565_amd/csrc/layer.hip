@@ -386,6 +386,7 @@ struct FfnStream {
         for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(As, LD, rb * 32, (t * 8 + h * 4 + k) * 16, lane);
+        __builtin_amdgcn_sched_barrier(0);   // all reads of the group before its products
 #pragma unroll
         for (int k = 0; k < 4; ++k)
 #pragma unroll
@@ -415,6 +416,7 @@ struct FfnStream {
         for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(Hc, HLD, rb * 32, (h * 4 + k) * 16, lane);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
 #pragma unroll
