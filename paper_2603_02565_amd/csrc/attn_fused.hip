@@ -123,6 +123,7 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
       for (int ks = 0; ks < KS; ++ks) wf[ks] = i == wave ? wfirst[ks] : Wqkv[((long long)cbg * KS + ks) * 64 + lane];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) af[ks] = a_frag(As, LDA, rb * 32, ks * 16, lane);
+      __builtin_amdgcn_sched_barrier(0);   // every operand read issued before the first product
       f32x16 acc = {};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks], af[ks], acc, 0, 0, 0);
@@ -385,10 +386,13 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
     for (int i = 0; i < 2; ++i) {
       const int rb = rb0 + 4 * i;
       if (rb >= nrb) continue;                       // uniform over the wave
+      bf16x8 af[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) af[ks] = a_frag(As, LDA, rb * 32, ks * 16, lane);
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 acc = {};
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks], a_frag(As, LDA, rb * 32, ks * 16, lane), acc, 0, 0, 0);
+      for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks], af[ks], acc, 0, 0, 0);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float4 bb = *reinterpret_cast<const float4*>(&s_vec[colq + 8 * q]);
@@ -467,10 +471,13 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
   // ---- q of head h = LN2(x1) Wq + bq: row block `wave` ------------------------------------
   if (wave < nrb) {
     const int rb = wave, row = rb * 32 + (lane & 31);
+    bf16x8 af[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) af[ks] = a_frag(As, LDA, rb * 32, ks * 16, lane);
+    __builtin_amdgcn_sched_barrier(0);
     f32x16 acc = {};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wqf[ks], a_frag(As, LDA, rb * 32, ks * 16, lane), acc, 0, 0, 0);
+    for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wqf[ks], af[ks], acc, 0, 0, 0);
     const float* bias = s_vec + 3 * D + h * DH;
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {
