@@ -13,6 +13,8 @@
 //   cross-sequence sets) whose attention ran in the chunked attention kernel; it reads the
 //   attention output O and the residual stream from global memory.  Its second variant replaces
 //   the FFN by the item layers' cross-attention query projection q = LN2(x1) Wq + bq.
+#include <type_traits>
+
 #include "fe_common.h"
 #include "fe_tile.h"
 
@@ -427,6 +429,120 @@ struct FfnStream {
   }
 };
 
+// The same product for a compile-time chunk count (F = 128*NCH), software-pipelined over the
+// chunks: between two barriers a wave forms the first-layer block of chunk s and the
+// second-layer blocks of chunk s - 1 (two independent MFMA chains), then chunk s's bias + ReLU
+// epilogue into hidden buffer s & 1, which the next step reads.  Buffer s & 1 was last read in
+// step s - 1 (as chunk s - 2), which ended with a barrier.  Weight stages are consumed, and
+// streamed through the DEPTH-slot register ring, in the order
+//   W1(0); W1(1) W2(0); W1(2) W2(1); ...; W1(NCH-1) W2(NCH-2); W2(NCH-1).
+// Same interface and the same ordering duties for the caller as FfnStream.
+template <int TM, int D, int NCH, int DEPTH>
+struct FfnPipe {
+  static constexpr int RB = TM / 32, KS = D / 16, OCB = D / 128, F = NCH * HC;
+  static constexpr int S1 = KS / 8, NS = S1 + OCB, NST = NCH * NS;
+  static_assert(KS % 8 == 0 && NCH >= 1 && DEPTH >= 2, "unsupported shape");
+  bf16x8 buf[DEPTH][8];
+  const bf16x8 *W1l, *W2l;
+  static constexpr int g_w1(int c, int t) { return c == 0 ? t : S1 + (c - 1) * NS + t; }
+  static constexpr int g_w2(int c, int j) { return S1 + c * NS + (c + 1 < NCH ? S1 : 0) + j; }
+  FE_DEV void load(int g) {   // stage g of the consumption order into ring slot g % DEPTH
+    bool w1;
+    int c, t;
+    if (g < S1) {
+      w1 = true; c = 0; t = g;
+    } else {
+      const int r = g - S1, st = r / NS + 1, o = r % NS;
+      if (st < NCH) {
+        w1 = o < S1; c = w1 ? st : st - 1; t = w1 ? o : o - S1;
+      } else {
+        w1 = false; c = NCH - 1; t = r - (NCH - 1) * NS;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      buf[g % DEPTH][k] = w1 ? W1l[((long long)c * 4 * KS + t * 8 + k) * 64] : W2l[((long long)4 * t * (F / 16) + c * 8 + k) * 64];
+  }
+  FE_DEV void fetch(int g) {   // consuming stage g: request stage g + DEPTH - 1
+    if (g + DEPTH - 1 < NST) load(g + DEPTH - 1);
+  }
+  FE_DEV void start(const void* w1p, const void* w2p, int) {
+    const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3), lane = threadIdx.x & 63;
+    W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
+    W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (F / 16) * 64 + lane;
+#pragma unroll
+    for (int g = 0; g < DEPTH - 1; ++g)
+      if (g < NST) load(g);
+  }
+  // acc[rb] += the 8 k-steps of ring slot `slot` against the tile At (row stride ld) at k-steps k0..
+  FE_DEV void steps(const bf16* At, int ld, int k0, int slot, f32x16 (&acc)[RB], int lane) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      bf16x8 af[4][RB];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(At, ld, rb * 32, (k0 + h * 4 + k) * 16, lane);
+      __builtin_amdgcn_sched_barrier(0);   // all reads of the group before its products
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot][h * 4 + k], af[k][rb], acc[rb], 0, 0, 0);
+    }
+  }
+  template <class Acc>
+  FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x) {
+    constexpr int LD = D + APAD;
+    const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
+    f32x16 acc_h[RB];
+#pragma unroll
+    for (int s = 0; s <= NCH; ++s) {
+      float4 bias1[4];
+      if (s < NCH) {
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq)
+          bias1[qq] = *reinterpret_cast<const float4*>(&b1[(s * 4 + wave) * 32 + qq * 8 + (lane >> 5) * 4]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) acc_h[rb] = f32x16{};
+#pragma unroll
+        for (int t = 0; t < S1; ++t) {
+          fetch(g_w1(s, t));
+          steps(As, LD, t * 8, g_w1(s, t) % DEPTH, acc_h, lane);
+        }
+      }
+      if (s > 0) {
+        const bf16* Hp = Hs + ((s - 1) & 1) * TM * HLD;
+#pragma unroll
+        for (int j = 0; j < OCB; ++j) {
+          fetch(g_w2(s - 1, j));
+          f32x16 (&xo)[RB] = x.v[j];
+          steps(Hp, HLD, 0, g_w2(s - 1, j) % DEPTH, xo, lane);
+        }
+      }
+      if (s < NCH) {
+        bf16* Hc = Hs + (s & 1) * TM * HLD;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) {
+            const float* bb = reinterpret_cast<const float*>(&bias1[qq]);
+            bf16x4 hv;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) hv[e] = (bf16)fmaxf(acc_h[rb][4 * qq + e] + bb[e], 0.f);
+            *reinterpret_cast<bf16x4*>(&Hc[(rb * 32 + (lane & 31)) * HLD + wave * 32 + qq * 8 + (lane >> 5) * 4]) = hv;
+          }
+        lds_barrier();
+      }
+    }
+  }
+};
+
+// FFN weight stream of a tile: pipelined over a compile-time chunk count (NCH > 0), else the
+// runtime-width stream.
+template <int TM, int D, int NCH>
+using FfnOf = typename std::conditional<(NCH > 0), FfnPipe<TM, D, (NCH > 0 ? NCH : 1), 3>, FfnStream<TM, D, 0, 2>>::type;
+
 template <int TM, int D>
 struct ModuleSmem {
   static constexpr int LDA = D + APAD, LDQ = 3 * D + APAD;
@@ -497,7 +613,7 @@ __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleA
     go.start(w.wo);
     lds_barrier();
     group_attention<D, DH, NKB, false, 4 * G>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
-    FfnStream<TMG, D, NCH, NCH ? 3 : 2> ffn;
+    FfnOf<TMG, D, NCH> ffn;
     ffn.start(w.w1, w.w2, a.F);
     lds_barrier();
     go.run(Ag, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TMG, D>(x, jj, rb, acc, vec + V::O); });
@@ -706,7 +822,7 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   stage_rows<TM, D>(a.O, false, D, row0, s_valid, nullptr, nullptr, As);
   Resid<TM, D> x;
   resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
-  FfnStream<TM, D, NCH, NCH ? 3 : 2> ffn;
+  FfnOf<TM, D, NCH> ffn;
   if constexpr (TAIL == 0) ffn.start(a.w1, a.w2, a.F);
   lds_barrier();
   go.run(As, LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, a.bo); });
