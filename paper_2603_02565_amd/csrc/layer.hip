@@ -474,21 +474,30 @@ struct FfnPipe {
     for (int g = 0; g < DEPTH - 1; ++g)
       if (g < NST) load(g);
   }
-  // acc[rb] += the 8 k-steps of ring slot `slot` against the tile At (row stride ld) at k-steps k0..
+  // acc[rb] += the 8 k-steps of ring slot `slot` against the tile At (row stride ld) at k-steps
+  // k0..: pairs of k-steps, the LDS reads of pair p + 1 issued before the products of pair p, so
+  // the reads stay in flight behind the matrix work
   FE_DEV void steps(const bf16* At, int ld, int k0, int slot, f32x16 (&acc)[RB], int lane) {
+    bf16x8 af[2][2][RB];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      bf16x8 af[4][RB];
+    for (int k = 0; k < 2; ++k)
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
+      for (int rb = 0; rb < RB; ++rb) af[0][k][rb] = a_frag(At, ld, rb * 32, (k0 + k) * 16, lane);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) af[k][rb] = a_frag(At, ld, rb * 32, (k0 + h * 4 + k) * 16, lane);
-      __builtin_amdgcn_sched_barrier(0);   // all reads of the group before its products
+    for (int p = 0; p < 4; ++p) {
+      if (p + 1 < 4) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) af[(p + 1) & 1][k][rb] = a_frag(At, ld, rb * 32, (k0 + 2 * p + 2 + k) * 16, lane);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
-          acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot][h * 4 + k], af[k][rb], acc[rb], 0, 0, 0);
+          acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot][2 * p + k], af[p & 1][k][rb], acc[rb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   template <class Acc>
