@@ -442,11 +442,12 @@ fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const fl
                   hipStream_t s, void* lnbuf = nullptr);
 
 struct Bufs {
-  float* X;      // fp32 residual stream [rows][d]
+  float* X;      // residual stream [rows][d]: fp32, or bf16 when xbf
   void* qkv;     // act [rows][3d]
   void* O;       // act [rows][d]
   void* Hf;      // act [rows][F]
   void* ln;      // wide bf16 models: bf16 [rows][d] LayerNorm output (else unused)
+  bool xbf = false;   // X holds bf16 (the fused tails of bf16 models write it so between kernels)
 };
 
 // One pre-LN encoder block over nb batches of `per` rows; attention stays inside a batch.
@@ -501,6 +502,7 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     // output projection, residual, LN2 and FFN in one kernel
     PostArgs p{b.O, xin, xin_f32, b.X, R, per, nvalid, d, F, 0, w.wo, w.bo, w.ln2g, w.ln2b,
                w.w1, w.b1, w.w2, w.b2, nullptr, nullptr, nullptr};
+    p.xout_bf16 = b.xbf;
     if (kvo) {
       p.Xout = nullptr;   // nothing reads the module's residual after its key/value projections
       p.lnfg = kvo->lnf_g;
@@ -769,6 +771,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
   float* lin_st = lin ? at<float>(ws, w.lin_st) : nullptr;
   void* kvp = lin ? at<char>(ws, w.c_kvp) : kv;
   const bool whole = !lin && module_fits(m, T);
+  b.xbf = bf && !wide(m) && !whole;   // block by block through the fused tails: bf16 between kernels
   if (whole) {
     st = run_module(m, m->ctx, B, T, src, false, m->ctx_lnf_g, m->ctx_lnf_b, b.X, false, s);
     if (st != FE_OK) return st;
@@ -779,7 +782,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
                     clear_late ? status_ctx : nullptr, B};
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       const bool last = l + 1 == m->cfg.n_layers;
-      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0, b, nullptr, s,
+      st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0 && !b.xbf, b, nullptr, s,
                      bf && !wide(m) && last ? &kvo : nullptr, lin_st);
       if (st != FE_OK) return st;
     }
@@ -852,11 +855,12 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
   void* Hf = at<char>(ws, w.i_h);
   void* lnb = wide(m) ? at<char>(ws, w.i_ln) : nullptr;
   const bool fused_tail = bf && !wide(m);     // k_post tails (else separate products)
+  const bool rbf = fused_tail;                // G and G1 hold the residual stream in bf16
   const int dh = d / m->cfg.n_heads;
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const ItemW& iw = m->item[l];
     const void* xin = l == 0 ? G0 : static_cast<const void*>(G);
-    const bool xin_f32 = l > 0;
+    const bool xin_f32 = l > 0 && !rbf;
     if (bf && self_attention_fits(d, m->cfg.n_heads, Ucap)) {
       SelfAttnArgs sa{xin, xin_f32, B, Ucap, n_uniq, iw.ln1g, iw.ln1b, iw.wqkv, iw.bqkv, O, m->cfg.n_heads,
                       1.0f / sqrtf((float)dh)};
@@ -884,11 +888,13 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       // per (request, head); its output goes to Qc (every head's workgroup reads all of O)
       CrossAttnArgs ca{O, xin, xin_f32, G1, B, Ucap, n_uniq, iw.wo, iw.bo, iw.ln2g, iw.ln2b, iw.wq, iw.bq,
                        Kc, Vc, T, Qc, m->cfg.n_heads, 1.0f / sqrtf((float)dh)};
+      ca.xout_bf16 = rbf;
       FE_LAUNCH(F_ATTN, s, launch_cross_attention(ca, d, s));
       const bool last = l + 1 == m->cfg.n_layers;
-      PostArgs p{Qc, G1, 1, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
+      PostArgs p{Qc, G1, !rbf, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
                  iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr,
                  last ? m->item_lnf_g : nullptr, last ? m->item_lnf_b : nullptr, last ? H : nullptr};
+      p.xout_bf16 = rbf;
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }
@@ -896,6 +902,7 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
       // x1 = x + O Wo + bo -> G, and the cross-attention queries q = LN2(x1) Wq + bq -> Qc
       PostArgs p{O, xin, xin_f32, G, R, Ucap, n_uniq, d, F, 1, iw.wo, iw.bo, iw.ln2g, iw.ln2b,
                  nullptr, nullptr, nullptr, nullptr, iw.wq, iw.bq, Qc};
+      p.xout_bf16 = rbf;
       FE_LAUNCH(F_POST, s, launch_post(p, s));
     } else {
       GemmArgs g = gemm(O, d, false, R, d, d, iw.wo, iw.bo, G, d, true, EPI_RESID);
@@ -926,9 +933,10 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     if (fused_tail) {
       // the last layer also applies the module's final LayerNorm and writes H directly
       const bool last = l + 1 == m->cfg.n_layers;
-      PostArgs p{O, G, 1, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
+      PostArgs p{O, G, !rbf, last ? nullptr : G, R, Ucap, n_uniq, d, F, 0, iw.wo2, iw.bo2, iw.ln3g, iw.ln3b,
                  iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr,
                  last ? m->item_lnf_g : nullptr, last ? m->item_lnf_b : nullptr, last ? H : nullptr};
+      p.xout_bf16 = rbf;
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }

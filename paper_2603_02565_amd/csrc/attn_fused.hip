@@ -416,10 +416,18 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
     for (int i = 0; i < 2; ++i) {
       const int rb = rb0 + 4 * i, row = rb * 32 + (lane & 31);
       if (rb >= nrb || row >= n) continue;
-      float* y = a.Xout + (rbase + row) * D + colq;
+      const long long o = (rbase + row) * D + colq;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(y + 8 * q) = make_float4(x[i][4 * q], x[i][4 * q + 1], x[i][4 * q + 2], x[i][4 * q + 3]);
+      for (int q = 0; q < 4; ++q) {
+        if (a.xout_bf16) {
+          bf16x4 hv;
+          hv[0] = (bf16)x[i][4 * q]; hv[1] = (bf16)x[i][4 * q + 1]; hv[2] = (bf16)x[i][4 * q + 2]; hv[3] = (bf16)x[i][4 * q + 3];
+          *reinterpret_cast<bf16x4*>(static_cast<bf16*>(a.Xout) + o + 8 * q) = hv;
+        } else {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.Xout) + o + 8 * q) =
+              make_float4(x[i][4 * q], x[i][4 * q + 1], x[i][4 * q + 2], x[i][4 * q + 3]);
+        }
+      }
     }
   }
   // ---- LN2(x1) -> As: per-row statistics of the wave's 32 columns (two lanes share a row),

@@ -145,12 +145,13 @@ hipError_t launch_self_attention(const SelfAttnArgs& a, int d, hipStream_t s);
 // O (act, all heads of the self-attention) and O2 must differ, and so must Xin and Xout: every
 // head's workgroup reads the whole rows of O and Xin.
 struct CrossAttnArgs {
-  const void* O; const void* Xin; int xin_f32; float* Xout;
+  const void* O; const void* Xin; int xin_f32; void* Xout;
   int B, per; const int32_t* nvalid;
   const void* wo; const float* bo; const float *ln2g, *ln2b; const void* wq; const float* bq;
   const void* Kc; const void* Vc; int T;
   void* O2;
   int n_heads; float scale;
+  int xout_bf16;                        // Xout is bf16 (else fp32)
 };
 bool cross_attention_fits(int d, int n_heads, int per, int T);
 hipError_t launch_cross_attention(const CrossAttnArgs& a, int d, hipStream_t s);
@@ -161,9 +162,10 @@ hipError_t launch_cross_attention(const CrossAttnArgs& a, int d, hipStream_t s);
 //           (Xout may then be nullptr); with kv != nullptr the key/value projections of the
 //           same LayerNorm (see the fields below);
 //   tail 1: Xout = x1 and Qout = LN2(x1) Wq + bq (bf16).
+// Xout is fp32, or bf16 with xout_bf16 (the residual stream between kernels).
 // Rows with (r % rows_per_batch) >= nvalid[r / rows_per_batch] are padding.
 struct PostArgs {
-  const void* O; const void* Xin; int xin_f32; float* Xout;
+  const void* O; const void* Xin; int xin_f32; void* Xout;
   int R, rows_per_batch; const int32_t* nvalid;
   int D, F, tail;
   const void* wo; const float* bo; const float *ln2g, *ln2b;
@@ -175,6 +177,7 @@ struct PostArgs {
   //   (LayerNorm with lnfg, lnfb; Wkv [D][2 * kv_layers * D] in packed fragment order, bf16 out)
   const void* wkv; const float* bkv; void* kv; int kv_layers;
   int32_t* zero; int zero_n;            // zero[0 .. zero_n) is cleared (or nullptr)
+  int xout_bf16;                        // Xout is bf16 (else fp32)
 };
 
 // Device pointers of one pre-LN encoder block (matrices of bf16 models in packed fragment order).

@@ -772,21 +772,27 @@ __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleA
   }
 }
 
-// Residual rows of x to Xout (fp32, row stride D) for valid tile rows.
+// Residual rows of x to Xout (row stride D; fp32, or bf16 with out_bf16) for valid tile rows.
 template <int TM, int D>
-FE_DEV void resid_store(const Resid<TM, D>& x, float* Xout, long long row0, const int* s_valid) {
+FE_DEV void resid_store(const Resid<TM, D>& x, void* Xout, bool out_bf16, long long row0, const int* s_valid) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int rb = 0; rb < TM / 32; ++rb) {
     const int r = rb * 32 + (lane & 31);
     if (!s_valid[r]) continue;
-    float* y = Xout + (row0 + r) * D;
 #pragma unroll
     for (int j = 0; j < D / 128; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const f32x16& v = x.v[j][rb];
-        *reinterpret_cast<float4*>(&y[resid_col(j, q)]) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+        const long long o = (row0 + r) * D + resid_col(j, q);
+        if (out_bf16) {
+          bf16x4 h;
+          h[0] = (bf16)v[4 * q]; h[1] = (bf16)v[4 * q + 1]; h[2] = (bf16)v[4 * q + 2]; h[3] = (bf16)v[4 * q + 3];
+          *reinterpret_cast<bf16x4*>(static_cast<bf16*>(Xout) + o) = h;
+        } else {
+          *reinterpret_cast<float4*>(static_cast<float*>(Xout) + o) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+        }
       }
   }
 }
@@ -803,7 +809,7 @@ FE_DEV void zero_rows_bf16(bf16* Y, long long row0, long long R, const int* s_va
 
 // The tail of a block whose attention ran in a separate kernel (long groups), bf16 models:
 //   x1 = Xin + O Wo + bo (residual in registers), then
-//   TAIL 0: x2 = x1 + FFN(LN2(x1)) -> Xout (fp32); when Hout is set (last item layer) also
+//   TAIL 0: x2 = x1 + FFN(LN2(x1)) -> Xout (fp32 or bf16); when Hout is set (last item layer) also
 //           Hout = LNf(x2) in bf16, with zero rows for padding rows;
 //   TAIL 1: Xout = x1, and the item layers' cross-attention queries Qout = LN2(x1) Wq + bq (bf16).
 // NCH > 0 fixes the FFN width at 128*NCH, which lets its weight stream run three stages deep
@@ -846,7 +852,7 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
     for (int j = 0; j < D / 128; ++j)
 #pragma unroll
       for (int rb = 0; rb < TM / 32; ++rb) resid_add<TM, D>(x, j, rb, f32x16{}, a.b2);
-    if (a.Xout) resid_store<TM, D>(x, a.Xout, row0, s_valid);
+    if (a.Xout) resid_store<TM, D>(x, a.Xout, a.xout_bf16, row0, s_valid);
     if (a.Hout) {
       // final LayerNorm of the module into bf16 H; padding rows of the tile become zeros
       float nm[TM / 32], rstd[TM / 32];
@@ -893,7 +899,7 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
       }
     }
   } else {
-    resid_store<TM, D>(x, a.Xout, row0, s_valid);
+    resid_store<TM, D>(x, a.Xout, a.xout_bf16, row0, s_valid);
     bf16* st = reinterpret_cast<bf16*>(big) + wave * 32 * 40;
     bf16* Q = static_cast<bf16*>(a.Qout) + (long long)row0 * D;
     gq.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) {
