@@ -882,20 +882,32 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
     }
     if (a.kv) {
       // last context block: the module's final LayerNorm feeds the key/value projections of
-      // every item layer (one slab of 2D columns per layer: keys, then values)
-      float nm[TM / 32], rstd[TM / 32];
-      resid_stats<TM, D>(x, s_stat, nm, rstd);    // also retires the FFN's reads of As and big
-      resid_norm_to_lds<TM, D>(x, nm, rstd, a.lnfg, a.lnfb, As);
-      lds_barrier();
+      // every item layer (one slab of 2D columns per layer: keys, then values; the slabs are
+      // consecutive column blocks of Wkv).  Two item layers run as one weight stream over all
+      // 4D columns, requested before the LayerNorm statistics.
       bf16* st = reinterpret_cast<bf16*>(big) + wave * 32 * 40;
-      for (int l = 0; l < a.kv_layers; ++l) {
-        ColGemm<TM, D, 2 * D / 32> gkv;
-        gkv.start(static_cast<const bf16x8*>(a.wkv) + (long long)l * (2 * D / 32) * (D / 16) * 64);
-        gkv.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) {
-          const int half = cb / (D / 32), c0 = (cb % (D / 32)) * 32;   // 0: keys, 1: values
-          bf16* out = static_cast<bf16*>(a.kv) + (long long)(2 * l + half) * a.R * D + (long long)row0 * D + c0;
-          store_block_bf16(acc, a.bkv + (2 * l + half) * D + c0, st, out, D, rb, s_valid);
-        });
+      auto kv_store = [&](int cb, int rb, const f32x16& acc) {   // cb: column block over all layers
+        const int slab = cb / (D / 32), c0 = (cb % (D / 32)) * 32;   // slab 2l: keys, 2l + 1: values
+        bf16* out = static_cast<bf16*>(a.kv) + (long long)slab * a.R * D + (long long)row0 * D + c0;
+        store_block_bf16(acc, a.bkv + slab * D + c0, st, out, D, rb, s_valid);
+      };
+      float nm[TM / 32], rstd[TM / 32];
+      if (a.kv_layers == 2) {
+        ColGemm<TM, D, 4 * D / 32> gkv;
+        gkv.start(a.wkv);
+        resid_stats<TM, D>(x, s_stat, nm, rstd);    // also retires the FFN's reads of As and big
+        resid_norm_to_lds<TM, D>(x, nm, rstd, a.lnfg, a.lnfb, As);
+        lds_barrier();
+        gkv.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) { kv_store(cb, rb, acc); });
+      } else {
+        resid_stats<TM, D>(x, s_stat, nm, rstd);
+        resid_norm_to_lds<TM, D>(x, nm, rstd, a.lnfg, a.lnfb, As);
+        lds_barrier();
+        for (int l = 0; l < a.kv_layers; ++l) {
+          ColGemm<TM, D, 2 * D / 32> gkv;
+          gkv.start(static_cast<const bf16x8*>(a.wkv) + (long long)l * (2 * D / 32) * (D / 16) * 64);
+          gkv.run(As, LDA, [&](int, int cb, int rb, const f32x16& acc) { kv_store(l * (2 * D / 32) + cb, rb, acc); });
+        }
       }
     }
   } else {
@@ -968,12 +980,12 @@ hipError_t launch_module_small(ModuleArgs a, hipStream_t s) {
   }
 }
 
+// d >= 512 models take the tiled products instead of the fused tails
 hipError_t launch_post(const PostArgs& a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
   switch (a.D) {
     case 128: return launch_post_t<64, 128>(a, s);
     case 256: return launch_post_t<64, 256>(a, s);
-    case 512: return launch_post_t<32, 512>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
