@@ -304,68 +304,53 @@ FE_DEV void vecs_dma(const EncW& w, float* dst) {
   }
 }
 
-// x += W2 ReLU(As W1 + b1) + b2 for the tile in As (LN2 output), hidden width F in chunks of
-// HC = 128, accumulating straight into the register-resident residual (its blocks are the
-// down-projection's output blocks).  Wave w computes hidden columns 32w..32w+31 of a chunk and
-// output blocks w + 4j.  The weight fragments of a chunk form one stream -- the KS k-steps of
-// W1 column block 4c + w, then for every output block j the 8 k-steps 8c.. of W2 column block
-// w + 4j -- consumed in stages of 8 fragments (NS = 2*KS/8 per chunk, an even count) through a
-// ring of DEPTH register stages, each stage requested DEPTH - 1 stages ahead.  With NCH = 0 the
-// chunk count F/HC is a runtime value and DEPTH is 2 (ring slot = stage parity); with NCH > 0
-// the F = 128*NCH chunks are unrolled, so every ring slot is a compile-time index for any DEPTH.
-// Hidden chunks alternate between two LDS buffers in Hs (2 x TM x HLD): chunk c is written to
-// buffer c&1 and one barrier per chunk separates its writers from its readers; buffer c&1 is
-// rewritten (chunk c+2) only after every wave passed the barrier of chunk c+1, i.e. finished
-// reading chunk c.  The caller orders the first writes to Hs after its earlier readers and the
-// next writes to As or Hs after this call.
-template <int TM, int D, int NCH = 0, int DEPTH = 2>
+// x += W2 ReLU(As W1 + b1) + b2 for the tile in As (LN2 output), hidden width F (a runtime
+// multiple of HC = 128) in chunks of HC, accumulating straight into the register-resident residual
+// (its blocks are the down-projection's output blocks).  Wave w computes hidden columns
+// 32w..32w+31 of a chunk and output blocks w + 4j.  The weight fragments of a chunk form one
+// stream -- the KS k-steps of W1 column block 4c + w, then for every output block j the 8 k-steps
+// 8c.. of W2 column block w + 4j -- consumed in stages of 8 fragments (NS = 2*KS/8 per chunk, an
+// even count) through a two-slot register ring (slot = stage parity), each stage requested one
+// stage ahead.  Hidden chunks alternate between two LDS buffers in Hs (2 x TM x HLD): chunk c is
+// written to buffer c&1 and one barrier per chunk separates its writers from its readers; buffer
+// c&1 is rewritten (chunk c+2) only after every wave passed the barrier of chunk c+1, i.e.
+// finished reading chunk c.  The caller orders the first writes to Hs after its earlier readers
+// and the next writes to As or Hs after this call.
+template <int TM, int D>
 struct FfnStream {
   static constexpr int RB = TM / 32, KS = D / 16, OCB = D / 128;
   static constexpr int S1 = KS / 8, NS = S1 + OCB;         // W1 stages, stages per chunk
   static_assert(KS % 8 == 0 && NS % 2 == 0, "unsupported width");
-  static_assert(NCH > 0 || DEPTH == 2, "a runtime chunk count needs the two-stage ring");
-  bf16x8 buf[DEPTH][8];
+  bf16x8 buf[2][8];
   const bf16x8 *W1l, *W2l;
   int F;
-  static constexpr int slot(int c, int t) { return NCH ? (c * NS + t) % DEPTH : t % 2; }
-  FE_DEV void load(int c, int t) {      // stage t of chunk c into its ring slot (compile-time t, slot)
+  FE_DEV void load(int c, int t) {      // stage t of chunk c into ring slot t & 1 (compile-time t)
     if (t < S1) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) buf[slot(c, t)][k] = W1l[((long long)c * 4 * KS + t * 8 + k) * 64];
+      for (int k = 0; k < 8; ++k) buf[t & 1][k] = W1l[((long long)c * 4 * KS + t * 8 + k) * 64];
     } else {
       const int j = t - S1;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) buf[slot(c, t)][k] = W2l[((long long)4 * j * (F / 16) + c * 8 + k) * 64];
+      for (int k = 0; k < 8; ++k) buf[t & 1][k] = W2l[((long long)4 * j * (F / 16) + c * 8 + k) * 64];
     }
   }
-  // request the stage DEPTH - 1 positions after stage t of chunk c, if there is one
+  // request the stage after stage t of chunk c, if there is one
   FE_DEV void prefetch(int c, int t, int nchunks) {
-    if constexpr (NCH == 0) {
-      if (t + 1 < NS) load(c, t + 1);
-      else if (c + 1 < nchunks) load(c + 1, 0);
-    } else {
-      const int g = c * NS + t + DEPTH - 1;
-      if (g < NCH * NS) load(g / NS, g % NS);
-    }
+    if (t + 1 < NS) load(c, t + 1);
+    else if (c + 1 < nchunks) load(c + 1, 0);
   }
   FE_DEV void start(const void* w1p, const void* w2p, int f) {
     const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3), lane = threadIdx.x & 63;
     F = f;
     W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
     W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (f / 16) * 64 + lane;
-#pragma unroll
-    for (int g = 0; g < DEPTH - 1; ++g) load(g / NS, g % NS);
+    load(0, 0);
   }
   template <class Acc>
   FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x) {
     const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
-    if constexpr (NCH > 0) {
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) chunk(c, NCH, As, Hs, b1, x, lane, wave);
-    } else {
-      const int nchunks = F / HC;
-      for (int c = 0; c < nchunks; ++c) chunk(c, nchunks, As, Hs, b1, x, lane, wave);
-    }
+    const int nchunks = F / HC;
+    for (int c = 0; c < nchunks; ++c) chunk(c, nchunks, As, Hs, b1, x, lane, wave);
   }
   template <class Acc>
   FE_DEV void chunk(int c, int nchunks, const bf16* As, bf16* Hs, const float* b1, Acc& x, int lane, int wave) {
@@ -393,7 +378,7 @@ struct FfnStream {
         for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot(c, t)][h * 4 + k], af[k][rb], acc_h[rb], 0, 0, 0);
+            acc_h[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][h * 4 + k], af[k][rb], acc_h[rb], 0, 0, 0);
       }
     }
 #pragma unroll
@@ -423,7 +408,7 @@ struct FfnStream {
         for (int k = 0; k < 4; ++k)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            x.v[j][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[slot(c, t)][h * 4 + k], af[k][rb], x.v[j][rb], 0, 0, 0);
+            x.v[j][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][h * 4 + k], af[k][rb], x.v[j][rb], 0, 0, 0);
       }
     }
   }
@@ -550,7 +535,7 @@ struct FfnPipe {
 // FFN weight stream of a tile: pipelined over a compile-time chunk count (NCH > 0), else the
 // runtime-width stream.
 template <int TM, int D, int NCH>
-using FfnOf = typename std::conditional<(NCH > 0), FfnPipe<TM, D, (NCH > 0 ? NCH : 1), 3>, FfnStream<TM, D, 0, 2>>::type;
+using FfnOf = typename std::conditional<(NCH > 0), FfnPipe<TM, D, (NCH > 0 ? NCH : 1), 3>, FfnStream<TM, D>>::type;
 
 template <int TM, int D>
 struct ModuleSmem {
@@ -812,8 +797,8 @@ FE_DEV void zero_rows_bf16(bf16* Y, long long row0, long long R, const int* s_va
 //   TAIL 0: x2 = x1 + FFN(LN2(x1)) -> Xout (fp32 or bf16); when Hout is set (last item layer) also
 //           Hout = LNf(x2) in bf16, with zero rows for padding rows;
 //   TAIL 1: Xout = x1, and the item layers' cross-attention queries Qout = LN2(x1) Wq + bq (bf16).
-// NCH > 0 fixes the FFN width at 128*NCH, which lets its weight stream run three stages deep
-// (used at D = 128, where the third stage still fits the register budget).
+// NCH > 0 fixes the FFN width at 128*NCH and takes the software-pipelined stream with a
+// three-stage weight ring (used at D = 128, where it fits the register budget).
 template <int TM, int D, int TAIL, int NCH>
 __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   constexpr int LDA = D + APAD;
@@ -943,8 +928,8 @@ hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
   if (a.first_row_only) return launch_module_c<TM, D, DH, true, 1>(a, s);
   if constexpr (D == 128) {   // at d = 256 two groups per compute unit would spill registers
     const int tiles = (a.n_groups + a.gpt - 1) / a.gpt;
-    // two wave groups leave room in the register budget for a three-stage FFN weight stream
-    // when the FFN width is fixed at 4d
+    // two wave groups leave room in the register budget for the pipelined FFN stream (three-stage
+    // weight ring) when the FFN width is fixed at 4d
     if (tiles <= 128 && a.F == 4 * D) return launch_module_c<TM, D, DH, false, 2, 4>(a, s);
     if (tiles <= 128) return launch_module_c<TM, D, DH, false, 2>(a, s);
   }

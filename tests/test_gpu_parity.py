@@ -108,6 +108,19 @@ def test_cfg4_text_hypotheses():
 
 # ------------------------------------------------------------------------- stage-isolated parity
 
+@pytest.mark.parametrize("cid,ffn", [(1, 256), (1, 768), (3, 512)])
+def test_ffn_width_other_than_4d(cid, ffn):
+    """F != 4d: the row-tile tails and module kernels stream the FFN with a runtime chunk count
+    (F = 4d takes the compile-time, software-pipelined stream)."""
+    kw = dict(B=2, K=20) if cid == 1 else dict(B=1, K=12, T=300, M=120)
+    c = gen.config(cid, ffn=ffn, **kw)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in range(c.B):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+    assert np.all(out["status"] == 0)
+
+
 def test_assemble_bit_exact_on_oracle_inputs():
     """fe_assemble on H and slot given by the oracle: the gather is exact; the position add rounds once."""
     c = gen.config(1, B=4)
