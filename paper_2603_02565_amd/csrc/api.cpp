@@ -840,7 +840,12 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
   const void* table = pool ? pool : m->emb;
   const long long table_bs = pool ? (long long)M * d : 0;
   void* G0 = at<char>(ws, w.i_g0);
-  if (dedup_gather_fits(Ucap, d, bf)) {
+  // the first item layer's self-attention kernel builds the distinct set and gathers the rows
+  // itself when it covers the set (its bitmap lives in the LN1 tile: M <= 278528)
+  const bool set_in_attention = bf && self_attention_fits(d, m->cfg.n_heads, Ucap) && (M + 31) / 32 <= 8704;
+  if (set_in_attention) {
+    // nothing to launch here
+  } else if (dedup_gather_fits(Ucap, d, bf)) {
     FE_LAUNCH(F_DEDUP, s, launch_dedup_gather(lists, B, KL, M, Ucap, uniq, n_uniq, slot, status_items, table, table_bs, d,
                                               G0, bf, s));
   } else {
@@ -864,7 +869,13 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
     if (bf && self_attention_fits(d, m->cfg.n_heads, Ucap)) {
       SelfAttnArgs sa{xin, xin_f32, B, Ucap, n_uniq, iw.ln1g, iw.ln1b, iw.wqkv, iw.bqkv, O, m->cfg.n_heads,
                       1.0f / sqrtf((float)dh)};
-      FE_LAUNCH(F_ATTN, s, launch_self_attention(sa, d, s));
+      if (l == 0 && set_in_attention) {
+        sa.lists = lists; sa.KL = KL; sa.M = M;
+        sa.table = table; sa.table_bs = table_bs;
+        sa.uniq = uniq; sa.n_uniq = n_uniq; sa.slot = slot; sa.status = status_items;
+        sa.Xrows = G0;
+      }
+      FE_LAUNCH(F_ATTN, s, launch_self_attention(sa, d, s));   // the distinct set rides in the first launch
     } else {
       GemmArgs g = gemm(xin, d, xin_f32, R, d, 3 * d, iw.wqkv, iw.bqkv, qkv, 3 * d, false, EPI_STORE);
       g.ln_g = iw.ln1g; g.ln_b = iw.ln1b; g.nvalid = n_uniq; g.rows_per_batch = Ucap;

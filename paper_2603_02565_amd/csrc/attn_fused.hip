@@ -17,7 +17,9 @@
 //   3. attention of those queries over the request's context keys/values (the key/value cache).
 // No q|k|v or query tensor reaches global memory, and the projections need no launches of their own.
 #include "fe_common.h"
+#include "fe_dedup.h"
 #include "fe_tile.h"
+#include "flasheval.h"
 
 namespace {
 
@@ -26,7 +28,7 @@ using fe_tile::a_frag;
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int D, int DH>
+template <int D, int DH, bool DEDUP>
 __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
   constexpr int NT = 1024, NR = 256, LDA = D + APAD, QLD = DH + 8, VLD = NR + 8;
   constexpr int KS = D / 16, NB = DH / 16, NB32 = NR / 32;
@@ -36,12 +38,35 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 Ks[NR * QLD];
   __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VLD];
   __shared__ __attribute__((aligned(16))) float s_g[D], s_b[D];
+  __shared__ int32_t s_uniq[DEDUP ? NR : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = xcd_tile(blockIdx.x, gridDim.x), h = bh % a.n_heads, b = bh / a.n_heads;
   int n = a.per;
-  if (a.nvalid) n = min(n, a.nvalid[b]);
-  if (n <= 0) return;                                // uniform over the workgroup
+  if constexpr (DEDUP) {
+    // the request's distinct set; its bitmap and word prefix sums live in As until LN1 overwrites it
+    uint32_t* bits = reinterpret_cast<uint32_t*>(As);
+    const int W = (a.M + 31) >> 5;
+    const bool lead = h == 0;
+    int bad = 0;
+    const int U = fe_dedup::distinct_set<NT>(a.lists + (long long)b * a.KL, a.KL, a.M, a.per,
+                                             lead ? a.uniq + (long long)b * a.per : nullptr,
+                                             lead ? a.slot + (long long)b * a.KL : nullptr, &bad, bits, bits + W, s_uniq);
+    if (lead && tid == 0) {
+      a.n_uniq[b] = U;
+      a.status[b] = bad ? FE_DEV_BAD_INDEX : 0;
+    }
+    n = min(n, U);
+    if (n <= 0) {                                    // no valid entry: zero rows only
+      if (lead)
+        for (int e = tid; e < a.per * (D / 8); e += NT)
+          reinterpret_cast<bf16x8*>(a.Xrows)[(long long)b * a.per * (D / 8) + e] = bf16x8{};
+      return;                                        // uniform over the workgroup
+    }
+  } else {
+    if (a.nvalid) n = min(n, a.nvalid[b]);
+    if (n <= 0) return;                              // uniform over the workgroup
+  }
   const int nrb = (n + 31) / 32;                     // 32-row blocks that hold valid rows
   // the weight fragments of this wave's first projection block (step 2), requested now so that
   // their latency hides behind LN1
@@ -65,7 +90,19 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
     const bool valid = r < n;
     const long long grow = (long long)b * a.per + (valid ? r : 0);
     float v[NV];
-    if (a.x_f32) {
+    if constexpr (DEDUP) {
+      // element rows from the table; the head-0 workgroup also writes them (zero rows from n on)
+      const bf16x8* src = reinterpret_cast<const bf16x8*>(static_cast<const bf16*>(a.table) + b * a.table_bs +
+                                                          (long long)s_uniq[valid ? r : 0] * D);
+      bf16x8* dst = reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.Xrows) + ((long long)b * a.per + r) * D);
+#pragma unroll
+      for (int i = 0; i < NV / 8; ++i) {
+        const bf16x8 t = src[i * TPR + part];
+        if (h == 0 && r < a.per) dst[i * TPR + part] = valid ? t : bf16x8{};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[8 * i + e] = (float)t[e];
+      }
+    } else if (a.x_f32) {
       const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(a.X) + grow * D);
 #pragma unroll
       for (int i = 0; i < NV / 4; ++i) {
@@ -98,7 +135,7 @@ __global__ __launch_bounds__(1024) void k_self_attention(SelfAttnArgs a) {
       // element index of v[i]: fp32 rows hold float4 (i/4)*TPR + part, bf16 rows bf16x8 (i/8)*TPR + part
 #pragma unroll
       for (int i = 0; i < NV; i += 4) {
-        const int k = a.x_f32 ? ((i / 4) * TPR + part) * 4 : ((i / 8) * TPR + part) * 8 + (i % 8);
+        const int k = (!DEDUP && a.x_f32) ? ((i / 4) * TPR + part) * 4 : ((i / 8) * TPR + part) * 8 + (i % 8);
         const float4 gg = *reinterpret_cast<const float4*>(&s_g[k]);
         const float4 bb = *reinterpret_cast<const float4*>(&s_b[k]);
         bf16x4 o;
@@ -513,7 +550,15 @@ bool self_attention_fits(int d, int n_heads, int per) { return d == 128 && d / n
 hipError_t launch_self_attention(const SelfAttnArgs& a, int d, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;
   if (!self_attention_fits(d, a.n_heads, a.per)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((k_self_attention<128, 32>), dim3((unsigned)(a.B * a.n_heads)), dim3(1024), 0, s, a);
+  if (a.lists) {
+    // the bitmap and its prefix sums live in the 256 x 136 bf16 LN1 tile
+    if (a.KL < 1 || a.M < 1 || a.per != min(a.M, a.KL) || 2 * ((a.M + 31) / 32) > 256 * 136 / 2 || !a.table ||
+        !a.uniq || !a.n_uniq || !a.slot || !a.status || !a.Xrows)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_self_attention<128, 32, true>), dim3((unsigned)(a.B * a.n_heads)), dim3(1024), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_self_attention<128, 32, false>), dim3((unsigned)(a.B * a.n_heads)), dim3(1024), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -133,6 +133,16 @@ struct SelfAttnArgs {
   const void* wqkv; const float* bqkv;
   void* O;
   int n_heads; float scale;
+  // With lists != nullptr (the first item layer) the kernel also builds the distinct set of each
+  // request from its KL list entries over elements 0..M-1 and reads its rows from `table`
+  // (request b's element id at table + b*table_bs + id*D, activation type) instead of X; nvalid
+  // and X are then unused.  The head-0 workgroup of request b writes uniq[b][0..per) (ascending,
+  // -1 padded), n_uniq[b], slot[b][0..KL), status[b] and the gathered rows Xrows[b][0..per)
+  // (zero rows from n_uniq[b] on); per = U_cap = min(M, KL).
+  const int32_t* lists; int KL, M;
+  const void* table; long long table_bs;
+  int32_t *uniq, *n_uniq, *slot, *status;
+  void* Xrows;
 };
 bool self_attention_fits(int d, int n_heads, int per);
 hipError_t launch_self_attention(const SelfAttnArgs& a, int d, hipStream_t s);

@@ -3,6 +3,7 @@
 // assembly with positions added after the gather (Section 4.3), and the score head with the
 // argmax of eq. (1).
 #include "fe_common.h"
+#include "fe_dedup.h"
 #include "flasheval.h"
 
 #include <climits>
@@ -10,87 +11,27 @@
 namespace {
 
 // ------------------------------------------------------------------------------------------
-// U(z): one workgroup per request.  A bitmap of M bits in LDS marks the elements that occur;
-// an exclusive scan of per-word popcounts gives every element its rank, so uniq comes out in
-// ascending order and slot = rank(element) is exact and deterministic.
+// U(z): one workgroup per request (fe_dedup.h).
 // ------------------------------------------------------------------------------------------
-
-// Exclusive prefix sum of one value per thread over the 256-thread workgroup (wave scans on
-// lane shuffles, then the four wave totals through LDS); *total receives the sum of all values.
-FE_DEV uint32_t block_exclusive_scan(uint32_t x, uint32_t* s_wave, uint32_t* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t inc = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t t = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += t;
-  }
-  if (lane == 63) s_wave[wave] = inc;
-  __syncthreads();
-  uint32_t before = 0;
-  for (int w = 0; w < wave; ++w) before += s_wave[w];
-  *total = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
-  return before + inc - x;
-}
 
 // The distinct set of request b = xcd_tile(blockIdx.x, B) (XCD-contiguous requests, so the
 // kernels after it, mapped the same way, read slot and the element rows from their own L2):
-// writes uniq (ascending, padded with -1 up to U_cap),
-// n_uniq, slot and the status word, and, when s_uniq != nullptr, the distinct ids into LDS
-// s_uniq[0 .. U).  bits and pre are LDS arrays of (M + 31) / 32 words.  Returns U; the ids in
-// s_uniq are visible to the whole workgroup when it returns.
+// writes uniq (ascending, padded with -1 up to U_cap), n_uniq, slot and the status word, and,
+// when s_uniq != nullptr, the distinct ids into LDS s_uniq[0 .. U).  bits and pre are LDS arrays
+// of (M + 31) / 32 words.  Returns U; the ids in s_uniq are visible to the whole workgroup when
+// it returns.
 FE_DEV int dedup_request(const int32_t* __restrict__ lists, int KL, int M, int U_cap, int32_t* __restrict__ uniq,
                          int32_t* __restrict__ n_uniq, int32_t* __restrict__ slot, int32_t* __restrict__ status,
                          uint32_t* bits, uint32_t* pre, int32_t* s_uniq) {
-  __shared__ uint32_t s_wave[4];
-  const int W = (M + 31) >> 5;
-  const int b = xcd_tile(blockIdx.x, gridDim.x), tid = threadIdx.x;
-  const int32_t* lb = lists + (long long)b * KL;
-
-  for (int i = tid; i < W; i += 256) bits[i] = 0u;
-  __syncthreads();
+  const int b = xcd_tile(blockIdx.x, gridDim.x);
   int bad = 0;
-  for (int i = tid; i < KL; i += 256) {
-    const int v = lb[i];
-    if (v >= 0 && v < M) atomicOr(&bits[v >> 5], 1u << (v & 31));
-    else bad = 1;
-  }
-  bad = __syncthreads_or(bad);
-
-  // per-thread contiguous chunk of words, then a block-wide exclusive scan of the chunk sums
-  const int chunk = (W + 255) / 256;
-  const int w0 = min(W, tid * chunk), w1 = min(W, w0 + chunk);
-  uint32_t local = 0;
-  for (int w = w0; w < w1; ++w) local += __popc(bits[w]);
-  uint32_t total;
-  uint32_t run = block_exclusive_scan(local, s_wave, &total);
-  int32_t* ub = uniq + (long long)b * U_cap;
-  for (int w = w0; w < w1; ++w) {
-    pre[w] = run;
-    uint32_t m = bits[w];
-    while (m) {
-      const int t = __ffs(m) - 1;
-      const int id = (w << 5) + t;
-      ub[run] = id;
-      if (s_uniq) s_uniq[run] = id;
-      ++run;
-      m &= m - 1;
-    }
-  }
-  for (int i = (int)total + tid; i < U_cap; i += 256) ub[i] = -1;
-  __syncthreads();
-  int32_t* sb = slot + (long long)b * KL;
-  for (int i = tid; i < KL; i += 256) {
-    const int v = lb[i];
-    int s = -1;
-    if (v >= 0 && v < M) s = (int)(pre[v >> 5] + __popc(bits[v >> 5] & ((1u << (v & 31)) - 1u)));
-    sb[i] = s;
-  }
-  if (tid == 0) {
-    n_uniq[b] = (int32_t)total;
+  const int U = fe_dedup::distinct_set<256>(lists + (long long)b * KL, KL, M, U_cap, uniq + (long long)b * U_cap,
+                                            slot + (long long)b * KL, &bad, bits, pre, s_uniq);
+  if (threadIdx.x == 0) {
+    n_uniq[b] = (int32_t)U;
     status[b] = bad ? FE_DEV_BAD_INDEX : 0;
   }
-  return (int)total;
+  return U;
 }
 
 __global__ __launch_bounds__(256) void k_dedup(const int32_t* __restrict__ lists, int KL, int M, int U_cap,
