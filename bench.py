@@ -117,8 +117,13 @@ def family_flops(c, U, fam_names):
         add("linear", n * lin_apply(rows_item))
     else:
         add("attention", sum(n * 4.0 * u * T * d for u in U))
-    add("attention" if selfattn(min(c.M, K * c.L)) else "gemm", n * 6.0 * d * d * rows_item)
-    add("post" if fused else "gemm", n * (6.0 * d * d + 4.0 * d * F) * rows_item)
+    ucap = min(c.M, K * c.L)
+    add("attention" if selfattn(ucap) else "gemm", n * 6.0 * d * d * rows_item)
+    # output + query projections of the item self-attention: inside the fused cross-attention
+    # kernel when it applies (softmax, groups and context of at most 256 rows), else in the tail
+    cross_fused = selfattn(ucap) and not lin and T <= 256
+    add("attention" if cross_fused else ("post" if fused else "gemm"), n * 4.0 * d * d * rows_item)
+    add("post" if fused else "gemm", n * (2.0 * d * d + 4.0 * d * F) * rows_item)
     return out
 
 
@@ -218,15 +223,26 @@ def cpu_cached(c, W, I, seconds: float):
                       f"request) in {dt:.1f} s"}
 
 
-# sources that define the module kernel, its launch shapes and the arguments it is given
-TRAFFIC_SOURCES = ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp")
+# Sources that define each profiled family's kernels (and api.cpp, which sets their arguments):
+# a traffic profile is used only while all of them are unchanged.
+TRAFFIC_SOURCES = {
+    "layer": ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp"),
+    "post": ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp"),
+    "attention": ("attn_fused.hip", "attention.hip", "fe_dedup.h", "fe_tile.h", "fe_common.h", "api.cpp"),
+}
+# kernel-name prefixes of each family (as rocprofv3 reports them)
+TRAFFIC_KERNELS = {
+    "layer": ("k_module_small",),
+    "post": ("k_post",),
+    "attention": ("k_self_attention", "k_cross_attention", "k_attention"),
+}
 
 
-def sources_digest() -> str:
-    """sha256 over the sources of the module kernel (identifies the kernel a traffic profile saw)."""
+def sources_digest(family: str) -> str:
+    """sha256 over the sources of `family`'s kernels (identifies the kernels a traffic profile saw)."""
     import hashlib
     h = hashlib.sha256()
-    for f in TRAFFIC_SOURCES:
+    for f in TRAFFIC_SOURCES[family]:
         with open(os.path.join(ROOT, "paper_2603_02565_amd", "csrc", f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
@@ -236,8 +252,8 @@ def measured_traffic(family: str):
     """HBM bytes per launch of `family` from profiles/traffic.json, if it was taken on these sources.
 
     The file holds FETCH_SIZE and WRITE_SIZE (rocprofv3 --pmc, one pass each) per dispatch of the
-    family's kernel, each scaled by the factor the same counter shows for a plain copy of known
-    size; it is ignored (null) once the kernel sources have changed.
+    family's kernels, each scaled by the factor the same counter shows for a plain copy of known
+    size; a family's entry is ignored (null) once its kernels' sources have changed.
     """
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
@@ -245,9 +261,10 @@ def measured_traffic(family: str):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("family") != family or t.get("sources_sha256") != sources_digest():
+    entry = t.get("families", {}).get(family)
+    if family not in TRAFFIC_SOURCES or not entry or entry.get("sources_sha256") != sources_digest(family):
         return None
-    return t.get("bytes_per_launch")
+    return entry.get("bytes_per_launch")
 
 
 MATRIX_FAMILIES = ("gemm", "ffn", "attention", "layer", "post")
