@@ -227,15 +227,25 @@ def cpu_cached(c, W, I, seconds: float):
 # a traffic profile is used only while all of them are unchanged.
 TRAFFIC_SOURCES = {
     "layer": ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp"),
+    "seq_module": ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp"),
     "post": ("layer.hip", "fe_tile.h", "fe_common.h", "api.cpp"),
     "attention": ("attn_fused.hip", "attention.hip", "fe_dedup.h", "fe_tile.h", "fe_common.h", "api.cpp"),
 }
 # kernel-name prefixes of each family (as rocprofv3 reports them)
 TRAFFIC_KERNELS = {
     "layer": ("k_module_small",),
+    "seq_module": ("k_module_small",),        # its [CLS]-only instantiations (template flag `true`)
     "post": ("k_post",),
     "attention": ("k_self_attention", "k_cross_attention", "k_attention"),
 }
+
+
+def traffic_kernel(family: str, name: str) -> bool:
+    """Whether rocprofv3 kernel `name` belongs to `family`."""
+    n = name.replace("void (anonymous namespace)::", "")
+    if not any(n.startswith(p) for p in TRAFFIC_KERNELS[family]):
+        return False
+    return family != "seq_module" or ", true," in n
 
 
 def sources_digest(family: str) -> str:
@@ -484,13 +494,39 @@ def main() -> int:
 
     # ---- kernel-timing region: the same steps with HIP events around every launch
     fam = {}
+    launches = []
     if not args.no_trace:
         fe.fe_trace_enable(True)
         for _ in range(args.steps):
             step()
         torch.cuda.synchronize()
-        fam = fe.fe_trace_read()
+        launches = fe.fe_trace_read_launches()
         fe.fe_trace_enable(False)
+        for f, t in launches:
+            ms_n = fam.get(f, (0.0, 0))
+            fam[f] = (ms_n[0] + t, ms_n[1] + 1)
+    # the pass's launch sequence (identical every step) and the mean time of each of its launches
+    per_pass = len(launches) // args.steps if launches else 0
+    seq_fams = [f for f, _ in launches[:per_pass]]
+    pos_ms = [float(np.mean([launches[i * per_pass + j][1] for i in range(args.steps)])) for j in range(per_pass)] \
+        if per_pass and len(launches) == per_pass * args.steps and \
+        all([f for f, _ in launches[i * per_pass:(i + 1) * per_pass]] == seq_fams for i in range(args.steps)) else []
+    # the SeqEnc module: the one "layer" launch right after the assembly (whole sequence encoder in
+    # one kernel); timed on its own as back-to-back fe_encode_sequences calls between two events
+    seq_pos = None
+    if pos_ms and "assemble" in seq_fams:
+        a = len(seq_fams) - 1 - seq_fams[::-1].index("assemble")
+        if a + 1 < len(seq_fams) and seq_fams[a + 1] == "layer":
+            seq_pos = a + 1
+    seqenc_us = None
+    if seq_pos is not None:
+        C_out = torch.empty((c.B, c.K, c.d), dtype=torch.float32, device="cuda")
+
+        def seq_only():
+            fe.fe_encode_sequences(ev.handle, c.B, c.K, c.L, bufs["seq"], C_out, bufs["ws"])
+
+        seqenc_us = time_pass(seq_only, stream, max(50, args.steps), 5) * 1e3
+        del C_out
 
     out = {
         "metric": METRIC, "value": round(lists_per_s, 1), "unit": "lists/s", "n_gpus": 1,
@@ -527,7 +563,20 @@ def main() -> int:
         dom = max((k for k in stages if k != "linear"), key=lambda k: stages[k]["ms_per_step"])
         dom_ms, dom_n = fam[dom]
         avg_s = dom_ms / dom_n / 1e3
-        if flops.get(dom, 0.0) > 0:
+        longest = int(np.argmax(pos_ms)) if pos_ms else None
+        if longest is not None and longest == seq_pos and seqenc_us is not None:
+            # the dominant kernel is the SeqEnc module: its own flops over its own back-to-back time
+            S = c.L + 1
+            sf = sum(module_parts(c.d, c.ffn, c.n_layers, c.B * c.K * S, c.B * c.K, S, True))
+            ach = sf / (seqenc_us / 1e6) / 1e12
+            out["roofline"] = {"kernel": "k_module_small (SeqEnc module)", "bound": "mfma", "achieved": round(ach, 2),
+                               "peak": round(peak, 1), "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                               "traffic": measured_traffic("seq_module"), "avg_launch_us": round(seqenc_us, 3),
+                               "launches_per_step": 1, "flops_per_launch": int(sf),
+                               "share_of_pass": round(pos_ms[longest] / sum(pos_ms), 4),
+                               "timing": "mean of back-to-back fe_encode_sequences calls (one launch each) "
+                                         "between two HIP events on the pass's stream"}
+        elif flops.get(dom, 0.0) > 0:
             per_launch = flops[dom] / (dom_n / args.steps)
             ach = per_launch / avg_s / 1e12
             out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1),

@@ -38,6 +38,14 @@ fe_status fe_trace_enable(int on);
  */
 fe_status fe_trace_read(double* total_ms, int64_t* launches);
 
+/*
+ * Synchronise every recorded event and write the launches in the order they were enqueued:
+ * family[i] and ms[i] (kernel time) for i < *count (host arrays of `capacity` entries).  If more
+ * than `capacity` launches are recorded, *count receives their number, nothing else is written,
+ * the records are kept and FE_EINVAL is returned.  Records are consumed otherwise.
+ */
+fe_status fe_trace_read_launches(int32_t* family, double* ms, int64_t capacity, int64_t* count);
+
 /* Name of family i ("" if out of range). */
 const char* fe_trace_family(int i);
 

@@ -637,6 +637,28 @@ fe_status fe_trace_read(double* total_ms, int64_t* launches) {
   return st;
 }
 
+fe_status fe_trace_read_launches(int32_t* family, double* ms, int64_t capacity, int64_t* count) {
+  if (!count || (capacity > 0 && (!family || !ms))) return fail(FE_EINVAL, "NULL output array");
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  *count = (int64_t)g_trace.size();
+  if ((int64_t)g_trace.size() > capacity)
+    return fail(FE_EINVAL, "%zu launches recorded, capacity %lld", g_trace.size(), (long long)capacity);
+  fe_status st = FE_OK;
+  for (size_t i = 0; i < g_trace.size(); ++i) {
+    const TraceRec& r = g_trace[i];
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess && st == FE_OK) st = fail(FE_EHIP, "trace event: %s", hipGetErrorString(e));
+    family[i] = r.fam;
+    ms[i] = t;
+    g_event_pool.push_back(r.a);
+    g_event_pool.push_back(r.b);
+  }
+  g_trace.clear();
+  return st;
+}
+
 const char* fe_trace_family(int i) { return (i >= 0 && i < FE_TRACE_FAMILIES) ? kFamName[i] : ""; }
 
 fe_status fe_param_count(const fe_config* cfg, size_t* n_floats) {

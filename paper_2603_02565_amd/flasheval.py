@@ -24,7 +24,7 @@ FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_kv_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
             "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
-            "fe_trace_family")
+            "fe_trace_read_launches", "fe_trace_family")
 FE_TRACE_FAMILIES = 12
 
 
@@ -73,6 +73,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_evaluate_naive": (S, [P, I, I, I, I, I, P, P, P, P, P, P, P, P, Z, P]),
         "fe_trace_enable": (S, [I]),
         "fe_trace_read": (S, [P, P]),
+        "fe_trace_read_launches": (S, [P, P, ctypes.c_int64, P]),
         "fe_trace_family": (ctypes.c_char_p, [I]),
     }
     for name, (res, args) in sig.items():
@@ -231,6 +232,17 @@ def fe_evaluate_naive(model: int, B: int, T: int, M: int, K: int, L: int, x, ctx
 
 def fe_trace_enable(on: bool) -> None:
     _check(load_library().fe_trace_enable(1 if on else 0), "fe_trace_enable")
+
+
+def fe_trace_read_launches(capacity: int = 1 << 16) -> List[Tuple[str, float]]:
+    """Recorded launches in enqueue order: (family name, kernel ms) each; consumes the records."""
+    lib = load_library()
+    fam = np.zeros(capacity, dtype=np.int32)
+    ms = np.zeros(capacity, dtype=np.float64)
+    n = ctypes.c_int64(0)
+    _check(lib.fe_trace_read_launches(fam.ctypes.data, ms.ctypes.data, capacity, ctypes.byref(n)),
+           "fe_trace_read_launches")
+    return [(lib.fe_trace_family(int(fam[i])).decode(), float(ms[i])) for i in range(n.value)]
 
 
 def fe_trace_read() -> Dict[str, Tuple[float, int]]:

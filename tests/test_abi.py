@@ -87,3 +87,9 @@ def test_trace_toggle_without_launches():
     assert set(out) == {"gemm", "attention", "layernorm", "dedup", "gather", "assemble", "score_select", "fill", "ffn",
                         "layer", "post", "linear"}
     assert all(v == (0.0, 0) for v in out.values())
+
+
+def test_trace_launch_records_without_launches():
+    fe.fe_trace_enable(True)
+    assert fe.fe_trace_read_launches() == []
+    fe.fe_trace_enable(False)

@@ -308,3 +308,34 @@ def test_graph_replay_matches_eager():
             assert np.array_equal(got[k], eager[k]), k
     del graph
     ev.close()
+
+
+def test_trace_launch_records_match_family_totals():
+    """Per-launch trace records (what the bench uses to find the longest kernel of the pass) agree
+    with the per-family totals, and the pass ends with assembly, the sequence-encoder module, the
+    cross-sequence module and the head."""
+    from collections import Counter
+    c = gen.config(1, B=2, K=8)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = make_evaluator(c, W)
+    ev.allocate(c.B, c.T, c.M, c.K, c.L)
+    d = upload(c, I)
+
+    def run():
+        ev.run(x=d["x"], pool=d["pool"], lists=d["lists"])
+        torch.cuda.synchronize()
+
+    run()
+    fe.fe_trace_enable(True)
+    run()
+    seq = fe.fe_trace_read_launches()
+    run()
+    tot = fe.fe_trace_read()
+    fe.fe_trace_enable(False)
+    counts = Counter(f for f, _ in seq)
+    assert all(tot[f][1] == counts.get(f, 0) for f in tot)
+    assert all(t > 0 for _, t in seq)
+    fams = [f for f, _ in seq]
+    a = len(fams) - 1 - fams[::-1].index("assemble")
+    assert fams[a + 1:] == ["layer", "layer", "score_select"]
+    ev.close()
