@@ -121,6 +121,17 @@ def test_ffn_width_other_than_4d(cid, ffn):
     assert np.all(out["status"] == 0)
 
 
+@pytest.mark.parametrize("d,H,n", [(128, 2, 1), (128, 4, 3), (128, 2, 8), (256, 4, 2), (256, 8, 1)])
+def test_model_shapes(d, H, n):
+    """Head widths 32 and 64, one to eight layers, d = 128 and 256 on the bf16 path: other kernel
+    instantiations (head width 64 takes the chunked attention instead of the fused per-head kernels)."""
+    c = gen.config(1, B=2, K=12, L=6, T=80, M=60, d=d, n_heads=H, n_layers=n, ffn=4 * d)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    for b in range(c.B):
+        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+
+
 def test_assemble_bit_exact_on_oracle_inputs():
     """fe_assemble on H and slot given by the oracle: the gather is exact; the position add rounds once."""
     c = gen.config(1, B=4)
