@@ -29,7 +29,8 @@ constexpr int HLD = HC + APAD;
 // Attention inside groups of S consecutive tile rows (S <= 16*NKB), reading q|k|v from the
 // LDS tile QKVs (row stride ldq; query columns 0..D-1, keys D..2D-1, values 2D..3D-1) and
 // writing the per-head outputs into Os (row stride lds); with FIRST_TILE only the first 16
-// queries of each group are computed.  One wave per (group, head, 16-query
+// queries of each group are computed and only the first query's output is written, to row g of
+// Os for group g (the compact [CLS] rows).  One wave per (group, head, 16-query
 // tile), two such units in flight per wave: the NKB score blocks are formed first as
 // independent MFMA chains, then one softmax over the whole group, then P V.
 template <int D, int DH, int NKB, bool FIRST_TILE = false, int WAVES = 4>
@@ -39,7 +40,7 @@ FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng
   const int g4 = lane >> 4, c16 = lane & 15;
   const int units = ng * UPG;
   for (int u0 = wave * NU; u0 < units; u0 += WAVES * NU) {
-    int base[NU], hcol[NU], q[NU];
+    int base[NU], hcol[NU], q[NU], grpx[NU];
     bool live[NU];
     bf16x8 qf[NU][DH / 32];
     f32x4 sc[NU][NKB];
@@ -48,6 +49,7 @@ FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng
       const int u = min(u0 + x, units - 1);
       live[x] = u0 + x < units;
       const int grp = u / UPG, rem = u % UPG;
+      grpx[x] = grp;
       hcol[x] = (rem / QT) * DH;
       base[x] = grp * S;
       q[x] = (rem % QT) * 16 + c16;
@@ -121,11 +123,12 @@ FE_DEV void group_attention(const bf16* QKVs, int ldq, bf16* Os, int lds, int ng
       }
 #pragma unroll
       for (int x = 0; x < NU; ++x) {
-        if (!live[x] || q[x] >= S) continue;
+        if (!live[x] || q[x] >= S || (FIRST_TILE && q[x] != 0)) continue;
         bf16x4 w;
 #pragma unroll
         for (int j = 0; j < 4; ++j) w[j] = (bf16)(o[x][j] * inv[x]);
-        *reinterpret_cast<bf16x4*>(&Os[(base[x] + q[x]) * lds + hcol[x] + i * 16 + g4 * 4]) = w;
+        const int orow = FIRST_TILE ? grpx[x] : base[x] + q[x];
+        *reinterpret_cast<bf16x4*>(&Os[orow * lds + hcol[x] + i * 16 + g4 * 4]) = w;
       }
     }
   }
@@ -625,8 +628,9 @@ __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleA
     // Last block when only each group's first row is wanted (the [CLS] rows of the sequence
     // encoder): keys and values still come from every row, but the attention runs for the first
     // query tile of each group only, and the output projection, LN2, FFN and the final LayerNorm
-    // run on the first rows alone, compacted into one 32-row block.
-    constexpr int LDC = D + 4;
+    // run on the first rows alone, compacted into one 32-row block: the attention writes group
+    // g's first-row output to row g of As (free once q|k|v are formed), and each wave moves the
+    // residual of row g*S to lane g by lane shuffles (same wave, same columns).
     const int last = a.n_layers - 1;
     const EncW& w = a.layer[last];
     const float* vec = s_vec[last & 1];
@@ -642,50 +646,34 @@ __global__ __launch_bounds__(WG * G, G == 1 ? 2 : 1) void k_module_small(ModuleA
     });
     ColGemm<32, D, D / 32> go;
     go.start(w.wo);
-    lds_barrier();
+    lds_barrier();                                   // q|k|v written, every read of As (LN1) retired
     group_attention<D, DH, NKB, true>(QKVs, L::LDQ, As, L::LDA, ng, a.S, a.scale * kLog2e);
-    lds_barrier();
-    // compaction: attention rows g*S of As -> Ac row g (bf16), residual rows g*S -> Xc row g
-    bf16* Ac = reinterpret_cast<bf16*>(big);
-    float* Xc = reinterpret_cast<float*>(big + 32 * L::LDA * 2);
-    for (int e = threadIdx.x; e < 32 * D / 8; e += WG) {
-      const int r = e / (D / 8), c = (e % (D / 8)) * 8;
-      const bf16x8 v = r < ng ? *reinterpret_cast<const bf16x8*>(&As[r * a.S * L::LDA + c]) : bf16x8{};
-      *reinterpret_cast<bf16x8*>(&Ac[r * L::LDA + c]) = v;
-    }
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int r = rb * 32 + (lane & 31);
-      if (!s_valid[r] || r % a.S) continue;
-      float* dst = Xc + (r / a.S) * LDC;
-#pragma unroll
-      for (int j = 0; j < D / 128; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x16& v = x.v[j][rb];
-          *reinterpret_cast<float4*>(&dst[resid_col(j, q)]) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
-        }
-    }
-    lds_barrier();
     Resid<32, D> xc;
     {
-      const int r = lane & 31;
+      // lane l of the compact block holds row g = l % 32 (columns of half l / 32), taken from the
+      // lane and row block that hold tile row g*S
+      const int g = lane & 31, src_row = g * a.S;
+      const int src = (src_row & 31) + (lane & 32), src_rb = src_row >> 5;
 #pragma unroll
       for (int j = 0; j < D / 128; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 t = r < ng ? *reinterpret_cast<const float4*>(&Xc[r * LDC + resid_col(j, q)]) : make_float4(0.f, 0.f, 0.f, 0.f);
-          xc.v[j][0][4 * q] = t.x;
-          xc.v[j][0][4 * q + 1] = t.y;
-          xc.v[j][0][4 * q + 2] = t.z;
-          xc.v[j][0][4 * q + 3] = t.w;
+        for (int i = 0; i < 16; ++i) {
+          float v = 0.f;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const float t = __shfl(x.v[j][rb][i], src, 64);
+            if (rb == src_rb) v = t;
+          }
+          xc.v[j][0][i] = g < ng ? v : 0.f;
         }
     }
     FfnStream<32, D> ffn;
     ffn.start(w.w1, w.w2, a.F);
-    go.run(Ac, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<32, D>(xc, jj, rb, acc, vec + V::O); });
-    // LN2 of the compact rows -> As rows 0..31; its statistics barrier retires the reads of Ac,
-    // so the FFN's hidden buffers may reuse the compaction area
+    lds_barrier();                                   // the compact attention rows are visible
+    go.run(As, L::LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<32, D>(xc, jj, rb, acc, vec + V::O); });
+    // LN2 of the compact rows -> As rows 0..31; its statistics barrier retires the output
+    // projection's reads of As, and every wave is past the attention, so the FFN's hidden
+    // buffers may take the q|k|v area
     resid_ln_to_lds<32, D>(xc, vec + V::G2, vec + V::B2, s_stat, As);
     lds_barrier();
     ffn.run(As, Hs, w.b1, xc);
