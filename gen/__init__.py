@@ -306,3 +306,11 @@ def make_inputs(cfg: Config) -> Dict[str, Optional[np.ndarray]]:
     else:
         raise ValueError(cfg.list_kind)
     return {"x": x, "ctx_ids": ctx_ids, "pool": pool, "lists": lists}
+
+
+def make_relevance(cfg: Config, p: float = 0.2, seed_offset: int = 40_000) -> np.ndarray:
+    """Synthetic item-level feedback for training: a[b][m] in {0, 1}, Bernoulli(p) per request
+    and element (int32 [B][M]; M = vocab for token-id items).  The labels built from it are the
+    consumer's business."""
+    rng = np.random.default_rng(seed_offset + cfg.cid + 97 * cfg.list_seed)
+    return (rng.random((cfg.B, cfg.M)) < p).astype(np.int32)
