@@ -599,6 +599,12 @@ fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const fl
 
 }  // namespace
 
+// Records the error text of a call implemented in another file of the library (the training step).
+fe_status fe_report(fe_status st, const char* msg) {
+  g_err = msg;
+  return st;
+}
+
 // ==========================================================================================
 // Exported functions
 // ==========================================================================================

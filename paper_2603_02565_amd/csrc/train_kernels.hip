@@ -1,0 +1,446 @@
+// fp32 kernels of the training step (Section 4.5): the forward with saved activations and its
+// backward.  Plain, general kernels: a batched strided product, row-wise LayerNorm and softmax
+// with their backward passes, elementwise steps, row gathers and their scatter-add backward, and
+// the losses with the label construction of Appendix B.1.
+#include "fe_common.h"
+#include "train_kernels.h"
+
+#include <algorithm>
+
+namespace {
+
+// ------------------------------------------------------------------------------------------
+// C[z] = alpha * op(A[z]) op(B[z]) + beta * C[z] (+ bias[j]); element (i, k) of A[z] at
+// A + z1*a_b1 + z2*a_b2 + i*a_rs + k*a_cs (likewise B with (k, j), C with (i, j) and unit column
+// stride), z = z1*nb2 + z2.  64 x 64 output tile per workgroup of 256 threads (4 x 4 each), k in
+// steps of 16 through LDS.
+// ------------------------------------------------------------------------------------------
+constexpr int GT = 64, GK = 16;
+
+__global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
+  __shared__ float As[GK][GT + 1], Bs[GK][GT + 1];
+  const int zz = z0 + blockIdx.z, z = zz % nz, kc = zz / nz;
+  const int z1 = z / g.nb2, z2 = z % g.nb2;
+  const int kbeg = g.ksplit > 0 ? kc * g.ksplit : 0;
+  const int kend = g.ksplit > 0 ? min(g.K, kbeg + g.ksplit) : g.K;
+  const float* A = g.A + z1 * g.a_b1 + z2 * g.a_b2;
+  const float* B = g.B + z1 * g.b_b1 + z2 * g.b_b2;
+  float* C = g.C + z1 * g.c_b1 + z2 * g.c_b2;
+  const int i0 = blockIdx.y * GT, j0 = blockIdx.x * GT;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  float acc[4][4] = {};
+  for (int k0 = kbeg; k0 < kend; k0 += GK) {
+    for (int e = threadIdx.x; e < GK * GT; e += 256) {
+      const int kk = e / GT, mm = e % GT;
+      const int i = i0 + mm, k = k0 + kk;
+      As[kk][mm] = (i < g.M && k < kend) ? A[i * g.a_rs + k * g.a_cs] : 0.f;
+      const int j = j0 + mm;
+      Bs[kk][mm] = (j < g.N && k < kend) ? B[k * g.b_rs + j * g.b_cs] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < GK; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) { a[u] = As[kk][ty * 4 + u]; b[u] = Bs[kk][tx * 4 + u]; }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(a[u], b[v], acc[u][v]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = i0 + ty * 4 + u;
+    if (i >= g.M) continue;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int j = j0 + tx * 4 + v;
+      if (j >= g.N) continue;
+      float r = g.alpha * acc[u][v];
+      float* c = C + i * g.c_rs + j;
+      if (g.ksplit > 0) {
+        atomicAdd(c, r);
+        continue;
+      }
+      if (g.bias) r += g.bias[j];
+      *c = g.beta != 0.f ? r + g.beta * *c : r;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// LayerNorm over rows of d values (biased variance, eps 1e-5): one wave per row.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_ln_fwd(const float* X, long long x_rs, int rows, int d, const float* g,
+                                                const float* b, float* Y, long long y_rs, float* mean, float* rstd) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* x = X + row * x_rs;
+  float s = 0.f;
+  for (int j = lane; j < d; j += 64) s += x[j];
+  const float mu = wave_sum(s) / d;
+  float q = 0.f;
+  for (int j = lane; j < d; j += 64) { const float t = x[j] - mu; q += t * t; }
+  const float rs = rsqrtf(wave_sum(q) / d + 1e-5f);
+  float* y = Y + row * y_rs;
+  for (int j = lane; j < d; j += 64) y[j] = (x[j] - mu) * rs * g[j] + b[j];
+  if (lane == 0) { mean[row] = mu; rstd[row] = rs; }
+}
+
+// dX += rstd (dxh - mean(dxh) - xh mean(dxh xh)) with dxh = dY g and xh the normalised input;
+// dg += sum_rows dY xh, db += sum_rows dY (per-workgroup partial sums, then atomics).
+__global__ __launch_bounds__(256) void k_ln_bwd(const float* X, long long x_rs, int rows, int d, const float* g,
+                                                const float* mean, const float* rstd, const float* dY, long long dy_rs,
+                                                float* dX, long long dx_rs, float* dg, float* db) {
+  extern __shared__ float part[];   // [4 waves][2][d]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float* pg = part + wave * 2 * d;
+  float* pb = pg + d;
+  for (int j = lane; j < d; j += 64) { pg[j] = 0.f; pb[j] = 0.f; }
+  for (int row = blockIdx.x * 4 * TRAIN_LN_ROWS + wave; row < min(rows, (blockIdx.x + 1) * 4 * TRAIN_LN_ROWS); row += 4) {
+    const float* x = X + row * x_rs;
+    const float* dy = dY + row * dy_rs;
+    const float mu = mean[row], rs = rstd[row];
+    float s1 = 0.f, s2 = 0.f;
+    for (int j = lane; j < d; j += 64) {
+      const float xh = (x[j] - mu) * rs, dxh = dy[j] * g[j];
+      s1 += dxh;
+      s2 += dxh * xh;
+      pg[j] += dy[j] * xh;
+      pb[j] += dy[j];
+    }
+    s1 = wave_sum(s1) / d;
+    s2 = wave_sum(s2) / d;
+    float* dx = dX + row * dx_rs;
+    for (int j = lane; j < d; j += 64) {
+      const float xh = (x[j] - mu) * rs;
+      dx[j] += rs * (dy[j] * g[j] - s1 - xh * s2);
+    }
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < d; j += 256) {
+    float sg = 0.f, sb = 0.f;
+    for (int w = 0; w < 4; ++w) { sg += part[w * 2 * d + j]; sb += part[w * 2 * d + d + j]; }
+    atomicAdd(&dg[j], sg);
+    atomicAdd(&db[j], sb);
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Softmax over the keys of every score row: P = softmax(scale S) on keys j < klen(z1), 0 beyond;
+// query rows i >= qlen(z1) are all zero.  Row r of batch z = z1*nb2 + z2 is S + z*nq*nk + r*nk.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_softmax_fwd(const float* S, float* P, int nbatch, int nb2, int nq, int nk,
+                                                     float scale, const int32_t* qlen, const int32_t* klen) {
+  const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= (long long)nbatch * nq) return;
+  const int z = (int)(row / nq), i = (int)(row % nq), z1 = z / nb2;
+  const int kl = klen ? min(nk, klen[z1]) : nk;
+  const bool live = (qlen ? i < qlen[z1] : true) && kl > 0;
+  const float* s = S + row * nk;
+  float* p = P + row * nk;
+  float mx = -INFINITY;
+  for (int j = lane; j < kl; j += 64) mx = fmaxf(mx, s[j] * scale);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int j = lane; j < kl; j += 64) sum += expf(s[j] * scale - mx);
+  sum = wave_sum(sum);
+  const float inv = live ? 1.f / sum : 0.f;
+  for (int j = lane; j < nk; j += 64) p[j] = (live && j < kl) ? expf(s[j] * scale - mx) * inv : 0.f;
+}
+
+// dS = scale P (dP - sum_j P_j dP_j), in place over dP.
+__global__ __launch_bounds__(256) void k_softmax_bwd(const float* P, float* dP, long long rows, int nk, float scale) {
+  const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* p = P + row * nk;
+  float* dp = dP + row * nk;
+  float s = 0.f;
+  for (int j = lane; j < nk; j += 64) s += p[j] * dp[j];
+  s = wave_sum(s);
+  for (int j = lane; j < nk; j += 64) dp[j] = scale * p[j] * (dp[j] - s);
+}
+
+// ------------------------------------------------------------------------------------------
+// Elementwise steps over n values.
+// ------------------------------------------------------------------------------------------
+__global__ void k_add(const float* a, const float* b, float* y, long long n) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = a[i] + b[i];
+}
+__global__ void k_copy(const float* x, float* y, long long n) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = x[i];
+}
+__global__ void k_acc(float* y, const float* x, long long n) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] += x[i];
+}
+__global__ void k_relu(const float* x, float* y, long long n) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = fmaxf(x[i], 0.f);
+}
+__global__ void k_relu_bwd(const float* x, const float* dy, float* dx, long long n) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dx[i] = x[i] > 0.f ? dy[i] : 0.f;
+}
+__global__ void k_fill(float* y, long long n, float v) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = v;
+}
+// db[j] += sum over rows of dY[r][j] (row stride rs): one thread per column, rows split over
+// blockIdx.y chunks of TRAIN_COL_ROWS, one atomic per chunk and column.
+__global__ void k_colsum(const float* dY, long long rs, int rows, int cols, float* db) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= cols) return;
+  const int r0 = blockIdx.y * TRAIN_COL_ROWS, r1 = min(rows, r0 + TRAIN_COL_ROWS);
+  float s = 0.f;
+  for (int r = r0; r < r1; ++r) s += dY[r * rs + j];
+  atomicAdd(&db[j], s);
+}
+
+// Y[b][r] = row idx[b][r] of table T + b*t_bs for r < n (n = nvalid ? nvalid[b] : rows); rows past
+// n and ids outside [0, n_table) give zero rows.
+__global__ void k_gather(const float* T, long long t_bs, int n_table, const int32_t* idx, int idx_bs,
+                         const int32_t* nvalid, int rows, int d, float* Y) {
+  const int b = blockIdx.y, r = blockIdx.x;
+  const int n = nvalid ? nvalid[b] : rows;
+  float* y = Y + ((long long)b * rows + r) * d;
+  const int id = r < n ? idx[(long long)b * idx_bs + r] : -1;
+  if (id < 0 || id >= n_table) {
+    for (int j = threadIdx.x; j < d; j += blockDim.x) y[j] = 0.f;
+    return;
+  }
+  const float* t = T + b * t_bs + (long long)id * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) y[j] = t[j];
+}
+// the gather's backward: dT row idx[b][r] += dY[b][r] for the rows the gather read
+__global__ void k_scatter_add(const float* dY, const int32_t* idx, int idx_bs, const int32_t* nvalid, int rows,
+                              int d, float* dT, long long t_bs, int n_table) {
+  const int b = blockIdx.y, r = blockIdx.x;
+  const int n = nvalid ? nvalid[b] : rows;
+  if (r >= n) return;
+  const int id = idx[(long long)b * idx_bs + r];
+  if (id < 0 || id >= n_table) return;
+  const float* dy = dY + ((long long)b * rows + r) * d;
+  float* t = dT + b * t_bs + (long long)id * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) atomicAdd(&t[j], dy[j]);
+}
+
+// seq[b][k][0] = cls + pos[0]; seq[b][k][j+1] = H[b][slot[b][k][j]] + pos[j+1] (Section 4.3)
+__global__ void k_assemble_f32(const float* H, int U_cap, const int32_t* slot, int K, int L, int d, const float* cls,
+                               const float* pos, float* seq) {
+  const int b = blockIdx.z, k = blockIdx.y, j = blockIdx.x;   // j = 0..L
+  float* o = seq + (((long long)b * K + k) * (L + 1) + j) * d;
+  const int sl = j == 0 ? 0 : slot[((long long)b * K + k) * L + j - 1];
+  const float* src = j == 0 ? cls : H + ((long long)b * U_cap + sl) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) o[e] = (sl >= 0 ? src[e] : 0.f) + pos[(long long)j * d + e];
+}
+// the assembly's backward: dH[b][slot] += dseq rows, dpos[j] += dseq[.][.][j], dcls += dseq[.][.][0]
+__global__ void k_assemble_bwd(const float* dseq, int U_cap, const int32_t* slot, int K, int L, int d, float* dH,
+                               float* dcls, float* dpos) {
+  const int b = blockIdx.z, k = blockIdx.y, j = blockIdx.x;
+  const float* g = dseq + (((long long)b * K + k) * (L + 1) + j) * d;
+  const int sl = j == 0 ? 0 : slot[((long long)b * K + k) * L + j - 1];
+  float* dst = j == 0 ? dcls : dH + ((long long)b * U_cap + sl) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) {
+    if (sl >= 0) atomicAdd(&dst[e], g[e]);
+    atomicAdd(&dpos[(long long)j * d + e], g[e]);
+  }
+}
+
+// Loss of request b (Section 4.5) with its labels (Appendix B.1): r_k = sum_j relevant[b][l_kj],
+// y = min argmax r_k; MSE target r_k, BCE target r_k / L.  Adds loss_b / B to *loss and writes
+// dscores[b][k] = (1/B) dloss_b / ds_k.  One workgroup per request, K <= 1024.
+__global__ __launch_bounds__(256) void k_loss(const float* s, const int32_t* lists, const int32_t* relevant, int M,
+                                              int B, int K, int L, int kind, float* loss, float* ds) {
+  __shared__ int sr[1024];
+  __shared__ float red[256];
+  __shared__ int sy;
+  const int b = blockIdx.x;
+  const float* sb = s + (long long)b * K;
+  for (int k = threadIdx.x; k < K; k += 256) {
+    int r = 0;
+    for (int j = 0; j < L; ++j) {
+      const int e = lists[((long long)b * K + k) * L + j];
+      r += (e >= 0 && e < M) ? relevant[(long long)b * M + e] : 0;
+    }
+    sr[k] = r;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int y = 0;
+    for (int k = 1; k < K; ++k) if (sr[k] > sr[y]) y = k;
+    sy = y;
+  }
+  __syncthreads();
+  // CE needs max and sum of exp over the K scores
+  float mx = -INFINITY;
+  for (int k = threadIdx.x; k < K; k += 256) mx = fmaxf(mx, sb[k]);
+  red[threadIdx.x] = mx;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + o]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float part = 0.f;
+  for (int k = threadIdx.x; k < K; k += 256) part += expf(sb[k] - mx);
+  red[threadIdx.x] = part;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  const float sumexp = red[0];
+  __syncthreads();
+  float lpart = 0.f;
+  for (int k = threadIdx.x; k < K; k += 256) {
+    const float sk = sb[k];
+    float l = 0.f, g = 0.f;
+    if (kind == TRAIN_MSE) {
+      const float t = (float)sr[k];
+      l = (sk - t) * (sk - t) / K;
+      g = 2.f * (sk - t) / K;
+    } else if (kind == TRAIN_BCE) {
+      const float t = (float)sr[k] / L;
+      // t softplus(-s) + (1 - t) softplus(s), softplus(v) = max(v, 0) + log1p(exp(-|v|))
+      const float sp_pos = fmaxf(sk, 0.f) + log1pf(expf(-fabsf(sk)));
+      const float sp_neg = fmaxf(-sk, 0.f) + log1pf(expf(-fabsf(sk)));
+      l = (t * sp_neg + (1.f - t) * sp_pos) / K;
+      g = (1.f / (1.f + expf(-sk)) - t) / K;
+    } else {
+      const float p = expf(sk - mx) / sumexp;
+      g = p - (k == sy ? 1.f : 0.f);
+      if (k == sy) l = -(sk - mx - logf(sumexp));
+    }
+    lpart += l;
+    ds[(long long)b * K + k] = g / B;
+  }
+  red[threadIdx.x] = lpart;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) atomicAdd(loss, red[0] / B);
+}
+
+inline unsigned blocks(long long n) { return (unsigned)((n + 255) / 256); }
+
+}  // namespace
+
+hipError_t t_gemm(const TGemm& g, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0 || g.nbatch <= 0) return hipSuccess;
+  if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.ksplit % GK)) return hipErrorInvalidValue;
+  const int nk = g.ksplit > 0 ? (g.K + g.ksplit - 1) / g.ksplit : 1;
+  const long long total = (long long)g.nbatch * nk;
+  const dim3 grid((unsigned)((g.N + GT - 1) / GT), (unsigned)((g.M + GT - 1) / GT), 1);
+  for (long long z0 = 0; z0 < total; z0 += 65535) {
+    dim3 gz = grid;
+    gz.z = (unsigned)std::min<long long>(65535, total - z0);
+    hipLaunchKernelGGL(k_gemm, gz, dim3(256), 0, s, g, (int)z0, g.nbatch);
+  }
+  return hipGetLastError();
+}
+
+hipError_t t_ln_fwd(const float* X, long long x_rs, int rows, int d, const float* g, const float* b, float* Y,
+                    long long y_rs, float* mean, float* rstd, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_ln_fwd, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, X, x_rs, rows, d, g, b, Y, y_rs, mean,
+                     rstd);
+  return hipGetLastError();
+}
+
+hipError_t t_ln_bwd(const float* X, long long x_rs, int rows, int d, const float* g, const float* mean,
+                    const float* rstd, const float* dY, long long dy_rs, float* dX, long long dx_rs, float* dg,
+                    float* db, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const unsigned nb = (unsigned)((rows + 4 * TRAIN_LN_ROWS - 1) / (4 * TRAIN_LN_ROWS));
+  hipLaunchKernelGGL(k_ln_bwd, dim3(nb), dim3(256), 8 * d * sizeof(float), s, X, x_rs, rows, d, g, mean, rstd, dY, dy_rs,
+                     dX, dx_rs, dg, db);
+  return hipGetLastError();
+}
+
+hipError_t t_softmax_fwd(const float* S, float* P, int nbatch, int nb2, int nq, int nk, float scale,
+                         const int32_t* qlen, const int32_t* klen, hipStream_t s) {
+  const long long rows = (long long)nbatch * nq;
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_softmax_fwd, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, S, P, nbatch, nb2, nq, nk, scale,
+                     qlen, klen);
+  return hipGetLastError();
+}
+
+hipError_t t_softmax_bwd(const float* P, float* dP, long long rows, int nk, float scale, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_softmax_bwd, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, P, dP, rows, nk, scale);
+  return hipGetLastError();
+}
+
+hipError_t t_add(const float* a, const float* b, float* y, long long n, hipStream_t s) {
+  if (n > 0) hipLaunchKernelGGL(k_add, dim3(blocks(n)), dim3(256), 0, s, a, b, y, n);
+  return hipGetLastError();
+}
+hipError_t t_copy(const float* x, float* y, long long n, hipStream_t s) {
+  if (n > 0) hipLaunchKernelGGL(k_copy, dim3(blocks(n)), dim3(256), 0, s, x, y, n);
+  return hipGetLastError();
+}
+hipError_t t_acc(float* y, const float* x, long long n, hipStream_t s) {
+  if (n > 0) hipLaunchKernelGGL(k_acc, dim3(blocks(n)), dim3(256), 0, s, y, x, n);
+  return hipGetLastError();
+}
+hipError_t t_relu(const float* x, float* y, long long n, hipStream_t s) {
+  if (n > 0) hipLaunchKernelGGL(k_relu, dim3(blocks(n)), dim3(256), 0, s, x, y, n);
+  return hipGetLastError();
+}
+hipError_t t_relu_bwd(const float* x, const float* dy, float* dx, long long n, hipStream_t s) {
+  if (n > 0) hipLaunchKernelGGL(k_relu_bwd, dim3(blocks(n)), dim3(256), 0, s, x, dy, dx, n);
+  return hipGetLastError();
+}
+hipError_t t_fill(float* y, long long n, float v, hipStream_t s) {
+  if (n > 0) hipLaunchKernelGGL(k_fill, dim3(blocks(n)), dim3(256), 0, s, y, n, v);
+  return hipGetLastError();
+}
+hipError_t t_colsum(const float* dY, long long rs, int rows, int cols, float* db, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_colsum, dim3((unsigned)((cols + 255) / 256), (unsigned)((rows + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
+                     dim3(256), 0, s, dY, rs, rows, cols, db);
+  return hipGetLastError();
+}
+hipError_t t_gather(const float* T, long long t_bs, int n_table, const int32_t* idx, int idx_bs, const int32_t* nvalid,
+                    int B, int rows, int d, float* Y, hipStream_t s) {
+  if (B <= 0 || rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather, dim3((unsigned)rows, (unsigned)B), dim3(128), 0, s, T, t_bs, n_table, idx, idx_bs, nvalid,
+                     rows, d, Y);
+  return hipGetLastError();
+}
+hipError_t t_scatter_add(const float* dY, const int32_t* idx, int idx_bs, const int32_t* nvalid, int B, int rows, int d,
+                         float* dT, long long t_bs, int n_table, hipStream_t s) {
+  if (B <= 0 || rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_scatter_add, dim3((unsigned)rows, (unsigned)B), dim3(128), 0, s, dY, idx, idx_bs, nvalid, rows, d,
+                     dT, t_bs, n_table);
+  return hipGetLastError();
+}
+hipError_t t_assemble(const float* H, int B, int U_cap, const int32_t* slot, int K, int L, int d, const float* cls,
+                      const float* pos, float* seq, hipStream_t s) {
+  hipLaunchKernelGGL(k_assemble_f32, dim3((unsigned)(L + 1), (unsigned)K, (unsigned)B), dim3(128), 0, s, H, U_cap, slot, K,
+                     L, d, cls, pos, seq);
+  return hipGetLastError();
+}
+hipError_t t_assemble_bwd(const float* dseq, int B, int U_cap, const int32_t* slot, int K, int L, int d, float* dH,
+                          float* dcls, float* dpos, hipStream_t s) {
+  hipLaunchKernelGGL(k_assemble_bwd, dim3((unsigned)(L + 1), (unsigned)K, (unsigned)B), dim3(128), 0, s, dseq, U_cap,
+                     slot, K, L, d, dH, dcls, dpos);
+  return hipGetLastError();
+}
+hipError_t t_loss(const float* scores, const int32_t* lists, const int32_t* relevant, int M, int B, int K, int L, int kind,
+                  float* loss, float* dscores, hipStream_t s) {
+  if (K > 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_loss, dim3((unsigned)B), dim3(256), 0, s, scores, lists, relevant, M, B, K, L, kind, loss, dscores);
+  return hipGetLastError();
+}

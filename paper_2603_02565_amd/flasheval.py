@@ -20,11 +20,13 @@ FE_OK, FE_EINVAL, FE_EUNSUPPORTED, FE_ENOMEM, FE_EHIP = range(5)
 FE_F32, FE_BF16 = 0, 1
 FE_ATTN_SOFTMAX, FE_ATTN_LINEAR = 0, 1
 FE_DEV_BAD_INDEX, FE_DEV_BAD_TOKEN = 1, 2
+FE_LOSS_MSE, FE_LOSS_BCE, FE_LOSS_CE = 0, 1, 2
+LOSS_KIND = {"mse": FE_LOSS_MSE, "bce": FE_LOSS_BCE, "ce": FE_LOSS_CE}
 
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_kv_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
             "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
-            "fe_trace_read_launches", "fe_trace_family")
+            "fe_trace_read_launches", "fe_trace_family", "fe_train_workspace_size", "fe_train_grads")
 FE_TRACE_FAMILIES = 12
 
 
@@ -75,6 +77,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_trace_read": (S, [P, P]),
         "fe_trace_read_launches": (S, [P, P, ctypes.c_int64, P]),
         "fe_trace_family": (ctypes.c_char_p, [I]),
+        "fe_train_workspace_size": (S, [cfgp, I, I, I, I, I, ctypes.POINTER(Z)]),
+        "fe_train_grads": (S, [cfgp, P, I, I, I, I, I, P, P, P, P, P, I, P, P, P, P, Z, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -228,6 +232,21 @@ def fe_evaluate_naive(model: int, B: int, T: int, M: int, K: int, L: int, x, ctx
     _check(load_library().fe_evaluate_naive(model, B, T, M, K, L, _ptr(x), _ptr(ctx_ids), _ptr(pool), _ptr(lists),
                                             _ptr(Cp), _ptr(scores), _ptr(best), _ptr(ws),
                                             ws.numel() * ws.element_size(), _stream(stream)), "fe_evaluate_naive")
+
+
+def fe_train_workspace_size(cfg: fe_config, B: int, T: int, M: int, K: int, L: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().fe_train_workspace_size(ctypes.byref(cfg), B, T, M, K, L, ctypes.byref(n)),
+           "fe_train_workspace_size")
+    return n.value
+
+
+def fe_train_grads(cfg: fe_config, params, B: int, T: int, M: int, K: int, L: int, x, ctx_ids, pool, lists, relevant,
+                   loss_kind: int, loss, scores, grads, ws, stream=None) -> None:
+    _check(load_library().fe_train_grads(ctypes.byref(cfg), _ptr(params), B, T, M, K, L, _ptr(x), _ptr(ctx_ids),
+                                         _ptr(pool), _ptr(lists), _ptr(relevant), loss_kind, _ptr(loss), _ptr(scores),
+                                         _ptr(grads), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "fe_train_grads")
 
 
 def fe_trace_enable(on: bool) -> None:

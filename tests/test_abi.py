@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _declared():
     names = set()
-    for h in ("flasheval.h", "flasheval_trace.h"):
+    for h in sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h")):
         with open(os.path.join(ROOT, "include", h)) as f:
             text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
         names |= set(re.findall(r"\b(fe_[a-z_]+)\s*\(", text))
@@ -93,3 +93,34 @@ def test_trace_launch_records_without_launches():
     fe.fe_trace_enable(True)
     assert fe.fe_trace_read_launches() == []
     fe.fe_trace_enable(False)
+
+
+def _train_cfg(c, **kw):
+    f = fe.fe_config(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, fe.FE_F32, fe.FE_ATTN_SOFTMAX)
+    for k, v in kw.items():
+        setattr(f, k, v)
+    return f
+
+
+def test_train_workspace_grows_with_the_batch():
+    c = gen.config(1)
+    small = fe.fe_train_workspace_size(_train_cfg(c), 2, 64, 200, 50, 10)
+    big = fe.fe_train_workspace_size(_train_cfg(c), 4, 64, 200, 50, 10)
+    longer = fe.fe_train_workspace_size(_train_cfg(c), 2, 128, 200, 50, 10)
+    assert 0 < small < big and small < longer and small % 256 == 0
+
+
+@pytest.mark.parametrize("kw,dims,status", [
+    (dict(dtype=fe.FE_BF16), (2, 64, 200, 50, 10), fe.FE_EUNSUPPORTED),           # fp32 models only
+    (dict(attention=fe.FE_ATTN_LINEAR), (2, 64, 200, 50, 10), fe.FE_EUNSUPPORTED),
+    ({}, (2, 64, 200, 1025, 10), fe.FE_EUNSUPPORTED),                              # K > 1024
+    ({}, (2, 64, 200, 50, 11), fe.FE_EINVAL),                                      # L > max_L
+    ({}, (0, 64, 200, 50, 10), fe.FE_EINVAL),
+    (dict(vocab=40), (2, 64, 200, 50, 10), fe.FE_EINVAL),                          # token ids need M = vocab
+])
+def test_train_validation(kw, dims, status):
+    c = gen.config(1)
+    with pytest.raises(fe.FeError) as e:
+        fe.fe_train_workspace_size(_train_cfg(c, **kw), *dims)
+    assert e.value.status == status
+    assert fe.load_library().fe_last_error().decode()

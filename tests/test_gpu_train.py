@@ -1,0 +1,137 @@
+"""Parity of the GPU training step (include/flasheval_train.h, Section 4.5) with the float64
+training reference: the batch loss, the forward's scores and the gradient of every parameter,
+on the same seeded weights, inputs and item-level feedback.
+
+Tolerance (fp32 step against float64): scores within 1e-4 of their largest magnitude, as in the
+forward parity tests; the loss within 1e-4 relative; every gradient tensor within 2e-3 of the
+largest entry of its own reference gradient or of 1e-3 x the largest reference gradient entry of
+the whole model, whichever is larger.  fp32 rounding accumulates through the backward of
+4 n_layers blocks and sums over up to B T rows; the floor holds a tensor whose gradient vanishes
+in exact arithmetic (the head bias under the listwise CE loss, whose gradient is the sum of
+softmax(s) - e_y = 0) to the model-wide scale instead of to its own rounding noise."""
+import numpy as np
+import pytest
+import torch
+
+import gen
+from oracle import train
+from paper_2603_02565_amd import flasheval as fe
+
+pytestmark = pytest.mark.gpu
+
+GRAD_RTOL = 2e-3
+GRAD_FLOOR = 1e-3
+
+
+def fe_cfg(c):
+    return fe.fe_config(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, fe.FE_F32, fe.FE_ATTN_SOFTMAX)
+
+
+def run_train(c, W, I, a, kind):
+    dev = torch.device("cuda:0")
+    cfg = fe_cfg(c)
+    names = fe.param_names(c.n_layers, c.vocab)
+    P = torch.from_numpy(fe.pack_params(W, c.n_layers, c.vocab)).to(dev)
+    B, T, M, K, L = c.B, c.T, c.M, c.K, c.L
+    f32 = lambda v: None if v is None else torch.from_numpy(np.ascontiguousarray(v, np.float32)).to(dev)
+    i32 = lambda v: None if v is None else torch.from_numpy(np.ascontiguousarray(v, np.int32)).to(dev)
+    x, pool = (None, None) if c.vocab else (f32(I["x"]), f32(I["pool"]))
+    ids = i32(I["ctx_ids"]) if c.vocab else None
+    lists, rel = i32(I["lists"]), i32(a)
+    ws = torch.empty(fe.fe_train_workspace_size(cfg, B, T, M, K, L), dtype=torch.uint8, device=dev)
+    G = torch.full_like(P, float("nan"))
+    loss = torch.full((1,), float("nan"), device=dev)
+    scores = torch.full((B * K,), float("nan"), device=dev)
+    fe.fe_train_grads(cfg, P, B, T, M, K, L, x, ids, pool, lists, rel, fe.LOSS_KIND[kind], loss, scores, G, ws)
+    torch.cuda.synchronize()
+    flat = G.cpu().numpy()
+    grads, o = {}, 0
+    for n in names:
+        k = int(np.prod(W[n].shape))
+        grads[n] = flat[o:o + k].reshape(W[n].shape)
+        o += k
+    assert o == flat.size
+    return float(loss.item()), grads, scores.cpu().numpy().reshape(B, K)
+
+
+def check(c, W, I, a, kind):
+    loss, g, s = run_train(c, W, I, a, kind)
+    Wd = {k: np.asarray(v, np.float64) for k, v in W.items()}
+    rloss, rg, rs = train.train_grads(c, Wd, I, a, kind)
+    assert abs(loss - rloss) <= 1e-4 * max(1.0, abs(rloss)), (loss, rloss)
+    stol = 1e-4 * max(1.0, float(np.max(np.abs(rs))))
+    assert np.max(np.abs(s - rs)) <= stol, "scores"
+    top = max(float(np.max(np.abs(v))) for v in rg.values())
+    worst = []
+    for n, ref in rg.items():
+        assert np.all(np.isfinite(g[n])), n
+        scale = max(float(np.max(np.abs(ref))), GRAD_FLOOR * top)
+        err = float(np.max(np.abs(g[n] - ref))) / scale
+        worst.append((err, n))
+        assert err <= GRAD_RTOL, (n, err)
+    worst.sort(reverse=True)
+    print(f"{c.label} {kind}: loss {loss:.6g} (ref {rloss:.6g}); worst gradient errors {worst[:3]}")
+
+
+def _relevance(c):
+    a = gen.make_relevance(c)
+    a[:, : max(1, c.M // 8)] = 1      # some positives in every request, so the labels are not all ties
+    return a
+
+
+@pytest.mark.parametrize("kind", train.LOSSES)
+def test_tiny(kind):
+    c = gen.config(0)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), kind)
+
+
+@pytest.mark.parametrize("kind", train.LOSSES)
+def test_recsys_shape(kind):
+    """RecSys-base model shape (d 128, 4 heads, 2 layers, FFN 512) in fp32, three requests with
+    zipf lists: each request has its own number of distinct items (masked item-set rows)."""
+    c = gen.config(1, B=3, T=20, K=6, L=4, M=25, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), kind)
+
+
+def test_several_tiles():
+    """Context, item set and list count past one 64-row tile with ragged tails (T 150, U up to
+    100 of M 100, K 70)."""
+    c = gen.config(1, B=2, T=150, K=70, L=3, M=100, n_layers=1, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "ce")
+
+
+def test_token_ids():
+    """Token-id context and items: the embedding table's gradient gathers from both."""
+    c = gen.config(4, B=2, K=3, L=5, T=9, vocab=40, M=40, n_layers=1, d=64, n_heads=1, ffn=128, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "mse")
+
+
+def test_head_width_64():
+    c = gen.config(1, B=2, T=12, K=5, L=4, M=18, d=128, n_heads=2, n_layers=1, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "bce")
+
+
+def test_full_recsys_batch():
+    """The RecSys-base batch (B 64, T 256, K 50, L 10, M 200) in fp32: scores of sampled requests
+    against the oracle's forward, and the two results that are closed forms in the scores and the
+    labels: the batch MSE loss and the head bias gradient (1/B) sum_b (2/K) sum_k (s_k - r_k)."""
+    import oracle
+    c = gen.config(1, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    a = _relevance(c)
+    loss, g, s = run_train(c, W, I, a, "mse")
+    for b in (0, 37, 63):
+        ref = oracle.evaluate_cached(c, W, I, requests=[b])[b]["scores"]
+        assert np.max(np.abs(s[b] - ref)) <= 1e-4 * max(1.0, float(np.max(np.abs(ref)))), b
+    r, _ = train.sequence_labels(I["lists"], a)
+    sd = s.astype(np.float64)
+    want = float(np.mean(np.mean((sd - r) ** 2, 1)))
+    assert abs(loss - want) <= 1e-5 * max(1.0, abs(want))
+    want_b = float(np.mean(np.sum(2 * (sd - r) / c.K, 1)))
+    assert abs(float(g["head.b"][0]) - want_b) <= 1e-4 * max(1.0, abs(want_b))
+    assert all(np.all(np.isfinite(v)) for v in g.values())
