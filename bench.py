@@ -155,6 +155,26 @@ def naive_flops(c, U):
     return B * K * ctx + K * L * sum(items) + seq + cross
 
 
+def train_flops(c, U):
+    """Algorithmic flops of one training step (forward + backward) over the valid rows: every
+    product of the forward once, and twice more in the backward (input and weight gradients of a
+    projection; dP, dV, dQ, dK of an attention).  U: distinct elements per request."""
+    d, F, H, n, dh = c.d, c.ffn, c.n_heads, c.n_layers, c.d // c.n_heads
+    B, T, K, S = c.B, c.T, c.K, c.L + 1
+    Usum = float(sum(U))
+
+    def enc(rows, att):                      # one encoder block: projections, FFN, attention
+        return 2 * rows * (4 * d * d + 2 * d * F) + att
+    fwd = n * enc(B * T, 4 * B * H * T * T * dh)
+    fwd += n * 2 * (2 * B * T * d * d)                                  # context keys and values per item layer
+    fwd += n * (2 * Usum * (6 * d * d + 2 * d * F)
+                + 4 * H * dh * sum(u * u + u * T for u in U))          # item-set layers
+    fwd += n * enc(B * K * S, 4 * B * K * H * S * S * dh)              # SeqEnc
+    fwd += n * enc(B * K, 4 * B * H * K * K * dh)                      # cross-sequence module
+    fwd += 2 * B * K * d
+    return 3 * fwd
+
+
 def cpu_baseline(c, W, I, seconds: float):
     """The float64 oracle, in its candidate-factorised order, on this host for a bounded time.
 
@@ -348,6 +368,8 @@ def main() -> int:
     ap.add_argument("--no-naive", action="store_true",
                     help="skip timing the candidate-factorised evaluator (no reuse) on the GPU")
     ap.add_argument("--naive-steps", type=int, default=5)
+    ap.add_argument("--no-train", action="store_true", help="skip the fp32 training-step timing")
+    ap.add_argument("--train-steps", type=int, default=10)
     ap.add_argument("--no-variants", action="store_true",
                     help="skip timing the pass without cross-sequence interaction (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -646,6 +668,34 @@ def main() -> int:
             "what": "context encoded once per list, distinct-element set once per element occurrence, "
                     "each list assembled from its own encodings (fe_evaluate_naive)"}
         ev.naive_buffers = None
+        torch.cuda.empty_cache()
+    if not args.no_train and c.attention == "softmax" and c.K <= 1024:
+        # one training step (Section 4.5) on the same batch: fp32 model, listwise CE loss
+        cfg = fe.fe_config(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, fe.FE_F32, fe.FE_ATTN_SOFTMAX)
+        Pt = torch.from_numpy(fe.pack_params(W, c.n_layers, c.vocab)).to(dev)
+        Gt = torch.empty_like(Pt)
+        xt = None if I["x"] is None else torch.from_numpy(I["x"]).to(dev).float()
+        pt = None if I["pool"] is None else torch.from_numpy(I["pool"]).to(dev).float()
+        rel = torch.from_numpy(gen.make_relevance(c)).to(dev)
+        loss_t = torch.empty(1, device=dev)
+        wst = torch.empty(fe.fe_train_workspace_size(cfg, c.B, c.T, c.M, c.K, c.L), dtype=torch.uint8, device=dev)
+
+        def train_step():
+            fe.fe_train_grads(cfg, Pt, c.B, c.T, c.M, c.K, c.L, xt, ids, pt, lists, rel, fe.FE_LOSS_CE, loss_t, None,
+                              Gt, wst)
+
+        tr_ms = time_pass(train_step, stream, args.train_steps, 2)
+        tf = train_flops(c, U)
+        out["train"] = {
+            "ms_per_step": round(tr_ms, 3), "steps_per_s": round(1e3 / tr_ms, 2),
+            "lists_per_s": round(c.B * c.K / (tr_ms / 1e3), 1), "loss": round(float(loss_t.item()), 6),
+            "dtype": "f32", "loss_kind": "ce", "steps": args.train_steps,
+            "gflops_per_step": round(tf / 1e9, 2), "tflops": round(tf / (tr_ms / 1e3) / 1e12, 2),
+            "frac_of_fp32_peak": round(tf / (tr_ms / 1e3) / 1e12 / PEAK_FP32_TFLOPS, 4),
+            "workspace_GiB": round(wst.numel() / 2**30, 3),
+            "what": "fe_train_grads: forward with saved activations, listwise CE loss, backward of every "
+                    "parameter, on this batch in fp32"}
+        del Pt, Gt, wst
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(c, W, I, args.cpu_seconds)

@@ -277,7 +277,7 @@ hipError_t linear_dw(const float* X, long long x_rs, int R, int din, const float
   const long long tiles = (long long)((din + 63) / 64) * ((dout + 63) / 64);
   long long chunks = std::max(1LL, 2048 / tiles);
   long long ks = std::max(256LL, (R + chunks - 1) / chunks);
-  g.ksplit = (int)((ks + 15) / 16 * 16);
+  g.ksplit = (int)((ks + 31) / 32 * 32);
   TRY(t_gemm(g, s));
   if (db) TRY(t_colsum(dY, dy_rs, R, dout, db, s));
   return hipSuccess;

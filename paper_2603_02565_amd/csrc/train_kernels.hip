@@ -12,13 +12,26 @@ namespace {
 // ------------------------------------------------------------------------------------------
 // C[z] = alpha * op(A[z]) op(B[z]) + beta * C[z] (+ bias[j]); element (i, k) of A[z] at
 // A + z1*a_b1 + z2*a_b2 + i*a_rs + k*a_cs (likewise B with (k, j), C with (i, j) and unit column
-// stride), z = z1*nb2 + z2.  64 x 64 output tile per workgroup of 256 threads (4 x 4 each), k in
-// steps of 16 through LDS.
+// stride), z = z1*nb2 + z2.
+//
+// fp32 matrix cores: a workgroup of four waves owns a (32 WM) x (32 WN) output tile, each wave one
+// 32 x 32 block accumulated by v_mfma_f32_32x32x2_f32 (lane l feeds A[l%32][l/32] and
+// B[l/32][l%32] of a 32x32x2 step and holds D[8q + 4(l/32) + e][l%32] in accumulator 4q + e).
+// k advances in steps of 32 through LDS, the next step's operands loaded into registers while
+// the current step's products run.  AK / BK: the operand's k index is its contiguous one,
+// so consecutive lanes load along k (else along i or j), which keeps the global loads coalesced
+// for both orientations.
 // ------------------------------------------------------------------------------------------
-constexpr int GT = 64, GK = 16;
+constexpr int GK = 32;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+template <int WM, int WN, bool AK, bool BK>
 __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
-  __shared__ float As[GK][GT + 1], Bs[GK][GT + 1];
+  static_assert(WM * WN == 4, "four waves");
+  constexpr int TM = 32 * WM, TN = 32 * WN, PA = TM + 4, PB = TN + 4;
+  constexpr int NA = GK * TM / 256, NB = GK * TN / 256;   // elements per thread per k-step
+  __shared__ float As[GK][PA];
+  __shared__ float Bs[GK][PB];
   const int zz = z0 + blockIdx.z, z = zz % nz, kc = zz / nz;
   const int z1 = z / g.nb2, z2 = z % g.nb2;
   const int kbeg = g.ksplit > 0 ? kc * g.ksplit : 0;
@@ -26,39 +39,60 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
   const float* A = g.A + z1 * g.a_b1 + z2 * g.a_b2;
   const float* B = g.B + z1 * g.b_b1 + z2 * g.b_b2;
   float* C = g.C + z1 * g.c_b1 + z2 * g.c_b2;
-  const int i0 = blockIdx.y * GT, j0 = blockIdx.x * GT;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  float acc[4][4] = {};
-  for (int k0 = kbeg; k0 < kend; k0 += GK) {
-    for (int e = threadIdx.x; e < GK * GT; e += 256) {
-      const int kk = e / GT, mm = e % GT;
+  const int i0 = blockIdx.y * TM, j0 = blockIdx.x * TN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wi = (wave / WN) * 32, wj = (wave % WN) * 32;
+  const int lr = lane & 31, lk = lane >> 5;
+  float ra[NA], rb[NB];
+  // the operands of k-step k0 into registers (zero outside the matrices and past kend)
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int t = 0; t < NA; ++t) {
+      const int e = threadIdx.x + 256 * t;
+      const int kk = AK ? e % GK : e / TM, mm = AK ? e / GK : e % TM;
       const int i = i0 + mm, k = k0 + kk;
-      As[kk][mm] = (i < g.M && k < kend) ? A[i * g.a_rs + k * g.a_cs] : 0.f;
-      const int j = j0 + mm;
-      Bs[kk][mm] = (j < g.N && k < kend) ? B[k * g.b_rs + j * g.b_cs] : 0.f;
+      ra[t] = (i < g.M && k < kend) ? A[i * g.a_rs + k * g.a_cs] : 0.f;
     }
+#pragma unroll
+    for (int t = 0; t < NB; ++t) {
+      const int e = threadIdx.x + 256 * t;
+      const int kk = BK ? e % GK : e / TN, nn = BK ? e / GK : e % TN;
+      const int j = j0 + nn, k = k0 + kk;
+      rb[t] = (j < g.N && k < kend) ? B[k * g.b_rs + j * g.b_cs] : 0.f;
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int t = 0; t < NA; ++t) {
+      const int e = threadIdx.x + 256 * t;
+      As[AK ? e % GK : e / TM][AK ? e / GK : e % TM] = ra[t];
+    }
+#pragma unroll
+    for (int t = 0; t < NB; ++t) {
+      const int e = threadIdx.x + 256 * t;
+      Bs[BK ? e % GK : e / TN][BK ? e / GK : e % TN] = rb[t];
+    }
+  };
+  f32x16 acc = {};
+  load(kbeg);
+  for (int k0 = kbeg; k0 < kend; k0 += GK) {
+    store();
     __syncthreads();
+    if (k0 + GK < kend) load(k0 + GK);   // the next step's loads are in flight during this step's products
 #pragma unroll
-    for (int kk = 0; kk < GK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) { a[u] = As[kk][ty * 4 + u]; b[u] = Bs[kk][tx * 4 + u]; }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(a[u], b[v], acc[u][v]);
-    }
+    for (int t = 0; t < GK / 2; ++t)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[2 * t + lk][wi + lr], Bs[2 * t + lk][wj + lr], acc, 0, 0, 0);
     __syncthreads();
   }
+  const int j = j0 + wj + lr;
+  if (j >= g.N) return;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int i = i0 + ty * 4 + u;
-    if (i >= g.M) continue;
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int j = j0 + tx * 4 + v;
-      if (j >= g.N) continue;
-      float r = g.alpha * acc[u][v];
+    for (int e = 0; e < 4; ++e) {
+      const int i = i0 + wi + 8 * q + 4 * lk + e;
+      if (i >= g.M) continue;
+      float r = g.alpha * acc[4 * q + e];
       float* c = C + i * g.c_rs + j;
       if (g.ksplit > 0) {
         atomicAdd(c, r);
@@ -67,7 +101,6 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
       if (g.bias) r += g.bias[j];
       *c = g.beta != 0.f ? r + g.beta * *c : r;
     }
-  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -192,15 +225,19 @@ __global__ void k_fill(float* y, long long n, float v) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) y[i] = v;
 }
-// db[j] += sum over rows of dY[r][j] (row stride rs): one thread per column, rows split over
-// blockIdx.y chunks of TRAIN_COL_ROWS, one atomic per chunk and column.
-__global__ void k_colsum(const float* dY, long long rs, int rows, int cols, float* db) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= cols) return;
+// db[j] += sum over rows of dY[r][j] (row stride rs): a workgroup takes 64 columns x
+// TRAIN_COL_ROWS rows, its four waves every fourth row, then one atomic per column.
+__global__ __launch_bounds__(256) void k_colsum(const float* dY, long long rs, int rows, int cols, float* db) {
+  __shared__ float part[4][64];
+  const int j = blockIdx.x * 64 + (threadIdx.x & 63), w = threadIdx.x >> 6;
   const int r0 = blockIdx.y * TRAIN_COL_ROWS, r1 = min(rows, r0 + TRAIN_COL_ROWS);
   float s = 0.f;
-  for (int r = r0; r < r1; ++r) s += dY[r * rs + j];
-  atomicAdd(&db[j], s);
+  if (j < cols)
+    for (int r = r0 + w; r < r1; r += 4) s += dY[r * rs + j];
+  part[w][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (w == 0 && j < cols) atomicAdd(&db[j], part[0][threadIdx.x] + part[1][threadIdx.x] + part[2][threadIdx.x] +
+                                               part[3][threadIdx.x]);
 }
 
 // Y[b][r] = row idx[b][r] of table T + b*t_bs for r < n (n = nvalid ? nvalid[b] : rows); rows past
@@ -335,17 +372,33 @@ inline unsigned blocks(long long n) { return (unsigned)((n + 255) / 256); }
 
 }  // namespace
 
+template <int WM, int WN, bool AK, bool BK>
+void gemm_launch(const TGemm& g, long long total, hipStream_t s) {
+  constexpr int TM = 32 * WM, TN = 32 * WN;
+  const dim3 grid((unsigned)((g.N + TN - 1) / TN), (unsigned)((g.M + TM - 1) / TM), 1);
+  for (long long z0 = 0; z0 < total; z0 += 65535) {
+    dim3 gz = grid;
+    gz.z = (unsigned)std::min<long long>(65535, total - z0);
+    hipLaunchKernelGGL((k_gemm<WM, WN, AK, BK>), gz, dim3(256), 0, s, g, (int)z0, g.nbatch);
+  }
+}
+
+template <int WM, int WN>
+void gemm_orient(const TGemm& g, long long total, hipStream_t s) {
+  const bool ak = g.a_cs == 1 && g.a_rs != 1, bk = g.b_rs == 1 && g.b_cs != 1;
+  if (ak && bk) gemm_launch<WM, WN, true, true>(g, total, s);
+  else if (ak) gemm_launch<WM, WN, true, false>(g, total, s);
+  else if (bk) gemm_launch<WM, WN, false, true>(g, total, s);
+  else gemm_launch<WM, WN, false, false>(g, total, s);
+}
+
 hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.nbatch <= 0) return hipSuccess;
   if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.ksplit % GK)) return hipErrorInvalidValue;
   const int nk = g.ksplit > 0 ? (g.K + g.ksplit - 1) / g.ksplit : 1;
   const long long total = (long long)g.nbatch * nk;
-  const dim3 grid((unsigned)((g.N + GT - 1) / GT), (unsigned)((g.M + GT - 1) / GT), 1);
-  for (long long z0 = 0; z0 < total; z0 += 65535) {
-    dim3 gz = grid;
-    gz.z = (unsigned)std::min<long long>(65535, total - z0);
-    hipLaunchKernelGGL(k_gemm, gz, dim3(256), 0, s, g, (int)z0, g.nbatch);
-  }
+  if (g.N <= 32) gemm_orient<4, 1>(g, total, s);   // 128 x 32 tiles (one head's width)
+  else gemm_orient<2, 2>(g, total, s);             // 64 x 64 tiles
   return hipGetLastError();
 }
 
@@ -408,7 +461,7 @@ hipError_t t_fill(float* y, long long n, float v, hipStream_t s) {
 }
 hipError_t t_colsum(const float* dY, long long rs, int rows, int cols, float* db, hipStream_t s) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_colsum, dim3((unsigned)((cols + 255) / 256), (unsigned)((rows + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
+  hipLaunchKernelGGL(k_colsum, dim3((unsigned)((cols + 63) / 64), (unsigned)((rows + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
                      dim3(256), 0, s, dY, rs, rows, cols, db);
   return hipGetLastError();
 }
