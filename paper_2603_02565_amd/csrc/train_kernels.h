@@ -9,8 +9,7 @@
 fe_status fe_report(fe_status st, const char* msg);
 
 enum { TRAIN_MSE = 0, TRAIN_BCE = 1, TRAIN_CE = 2 };
-constexpr int TRAIN_LN_ROWS = 16;    // rows per wave in one LayerNorm-backward workgroup
-constexpr int TRAIN_COL_ROWS = 64;   // rows per workgroup of a column sum
+constexpr int TRAIN_COL_ROWS = 64;   // rows per workgroup of a column reduction
 
 // C[z] = alpha * A[z] B[z] + beta * C[z] + bias (bias[j] over columns, may be null), z < nbatch,
 // z = z1 * nb2 + z2.  Element (i, k) of A[z] is A[z1*a_b1 + z2*a_b2 + i*a_rs + k*a_cs]; B (k, j)

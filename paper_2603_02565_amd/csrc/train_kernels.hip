@@ -103,6 +103,64 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
     }
 }
 
+// Batched products with M, N <= 32 (attention inside short sequences): each wave owns one batch
+// item's 32 x 32 tile, four items per workgroup, same k-steps and prefetch as k_gemm.
+template <bool AK, bool BK>
+__global__ __launch_bounds__(256) void k_gemm_small(TGemm g, int z0) {
+  constexpr int P = 36, N1 = GK * 32 / 64;   // elements per lane per operand per k-step
+  __shared__ float As[4][GK][P];
+  __shared__ float Bs[4][GK][P];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int z = z0 + blockIdx.x * 4 + wave;
+  const bool live = z < g.nbatch;
+  const int z1 = live ? z / g.nb2 : 0, z2 = live ? z % g.nb2 : 0;
+  const float* A = g.A + z1 * g.a_b1 + z2 * g.a_b2;
+  const float* B = g.B + z1 * g.b_b1 + z2 * g.b_b2;
+  float* C = g.C + z1 * g.c_b1 + z2 * g.c_b2;
+  const int lr = lane & 31, lk = lane >> 5;
+  float ra[N1], rb[N1];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int t = 0; t < N1; ++t) {
+      const int e = lane + 64 * t;
+      const int kk = AK ? e % GK : e / 32, mm = AK ? e / GK : e % 32;
+      const int k = k0 + kk;
+      ra[t] = (live && mm < g.M && k < g.K) ? A[mm * g.a_rs + k * g.a_cs] : 0.f;
+      const int kb = BK ? e % GK : e / 32, nn = BK ? e / GK : e % 32;
+      const int kq = k0 + kb;
+      rb[t] = (live && nn < g.N && kq < g.K) ? B[kq * g.b_rs + nn * g.b_cs] : 0.f;
+    }
+  };
+  f32x16 acc = {};
+  load(0);
+  for (int k0 = 0; k0 < g.K; k0 += GK) {
+#pragma unroll
+    for (int t = 0; t < N1; ++t) {
+      const int e = lane + 64 * t;
+      As[wave][AK ? e % GK : e / 32][AK ? e / GK : e % 32] = ra[t];
+      Bs[wave][BK ? e % GK : e / 32][BK ? e / GK : e % 32] = rb[t];
+    }
+    __syncthreads();
+    if (k0 + GK < g.K) load(k0 + GK);
+#pragma unroll
+    for (int t = 0; t < GK / 2; ++t)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[wave][2 * t + lk][lr], Bs[wave][2 * t + lk][lr], acc, 0, 0, 0);
+    __syncthreads();
+  }
+  if (!live || lr >= g.N) return;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = 8 * q + 4 * lk + e;
+      if (i >= g.M) continue;
+      float r = g.alpha * acc[4 * q + e];
+      if (g.bias) r += g.bias[lr];
+      float* c = C + i * g.c_rs + lr;
+      *c = g.beta != 0.f ? r + g.beta * *c : r;
+    }
+}
+
 // ------------------------------------------------------------------------------------------
 // LayerNorm over rows of d values (biased variance, eps 1e-5): one wave per row.
 // ------------------------------------------------------------------------------------------
@@ -122,42 +180,52 @@ __global__ __launch_bounds__(256) void k_ln_fwd(const float* X, long long x_rs, 
   if (lane == 0) { mean[row] = mu; rstd[row] = rs; }
 }
 
-// dX += rstd (dxh - mean(dxh) - xh mean(dxh xh)) with dxh = dY g and xh the normalised input;
-// dg += sum_rows dY xh, db += sum_rows dY (per-workgroup partial sums, then atomics).
-__global__ __launch_bounds__(256) void k_ln_bwd(const float* X, long long x_rs, int rows, int d, const float* g,
-                                                const float* mean, const float* rstd, const float* dY, long long dy_rs,
-                                                float* dX, long long dx_rs, float* dg, float* db) {
-  extern __shared__ float part[];   // [4 waves][2][d]
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float* pg = part + wave * 2 * d;
-  float* pb = pg + d;
-  for (int j = lane; j < d; j += 64) { pg[j] = 0.f; pb[j] = 0.f; }
-  for (int row = blockIdx.x * 4 * TRAIN_LN_ROWS + wave; row < min(rows, (blockIdx.x + 1) * 4 * TRAIN_LN_ROWS); row += 4) {
-    const float* x = X + row * x_rs;
-    const float* dy = dY + row * dy_rs;
-    const float mu = mean[row], rs = rstd[row];
-    float s1 = 0.f, s2 = 0.f;
-    for (int j = lane; j < d; j += 64) {
-      const float xh = (x[j] - mu) * rs, dxh = dy[j] * g[j];
-      s1 += dxh;
-      s2 += dxh * xh;
-      pg[j] += dy[j] * xh;
-      pb[j] += dy[j];
-    }
-    s1 = wave_sum(s1) / d;
-    s2 = wave_sum(s2) / d;
-    float* dx = dX + row * dx_rs;
-    for (int j = lane; j < d; j += 64) {
-      const float xh = (x[j] - mu) * rs;
-      dx[j] += rs * (dy[j] * g[j] - s1 - xh * s2);
-    }
+// dX += rstd (dxh - mean(dxh) - xh mean(dxh xh)) with dxh = dY g and xh the normalised input:
+// one wave per row.
+__global__ __launch_bounds__(256) void k_ln_bwd_rows(const float* X, long long x_rs, int rows, int d, const float* g,
+                                                     const float* mean, const float* rstd, const float* dY,
+                                                     long long dy_rs, float* dX, long long dx_rs) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* x = X + row * x_rs;
+  const float* dy = dY + row * dy_rs;
+  const float mu = mean[row], rs = rstd[row];
+  float s1 = 0.f, s2 = 0.f;
+  for (int j = lane; j < d; j += 64) {
+    const float xh = (x[j] - mu) * rs, dxh = dy[j] * g[j];
+    s1 += dxh;
+    s2 += dxh * xh;
   }
+  s1 = wave_sum(s1) / d;
+  s2 = wave_sum(s2) / d;
+  float* dx = dX + row * dx_rs;
+  for (int j = lane; j < d; j += 64) {
+    const float xh = (x[j] - mu) * rs;
+    dx[j] += rs * (dy[j] * g[j] - s1 - xh * s2);
+  }
+}
+
+// dg[j] += sum_rows dY xh, db[j] += sum_rows dY: 64 columns x TRAIN_COL_ROWS rows per workgroup,
+// its four waves every fourth row, one atomic per column and workgroup.
+__global__ __launch_bounds__(256) void k_ln_bwd_params(const float* X, long long x_rs, int rows, int d,
+                                                       const float* mean, const float* rstd, const float* dY,
+                                                       long long dy_rs, float* dg, float* db) {
+  __shared__ float part[2][4][64];
+  const int c = threadIdx.x & 63, w = threadIdx.x >> 6, j = blockIdx.x * 64 + c;
+  const int r0 = blockIdx.y * TRAIN_COL_ROWS, r1 = min(rows, r0 + TRAIN_COL_ROWS);
+  float sg = 0.f, sb = 0.f;
+  if (j < d)
+    for (int r = r0 + w; r < r1; r += 4) {
+      const float dy = dY[r * dy_rs + j];
+      sg += dy * (X[r * x_rs + j] - mean[r]) * rstd[r];
+      sb += dy;
+    }
+  part[0][w][c] = sg;
+  part[1][w][c] = sb;
   __syncthreads();
-  for (int j = threadIdx.x; j < d; j += 256) {
-    float sg = 0.f, sb = 0.f;
-    for (int w = 0; w < 4; ++w) { sg += part[w * 2 * d + j]; sb += part[w * 2 * d + d + j]; }
-    atomicAdd(&dg[j], sg);
-    atomicAdd(&db[j], sb);
+  if (w == 0 && j < d) {
+    atomicAdd(&dg[j], part[0][0][c] + part[0][1][c] + part[0][2][c] + part[0][3][c]);
+    atomicAdd(&db[j], part[1][0][c] + part[1][1][c] + part[1][2][c] + part[1][3][c]);
   }
 }
 
@@ -397,8 +465,20 @@ hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.ksplit % GK)) return hipErrorInvalidValue;
   const int nk = g.ksplit > 0 ? (g.K + g.ksplit - 1) / g.ksplit : 1;
   const long long total = (long long)g.nbatch * nk;
-  if (g.N <= 32) gemm_orient<4, 1>(g, total, s);   // 128 x 32 tiles (one head's width)
-  else gemm_orient<2, 2>(g, total, s);             // 64 x 64 tiles
+  if (g.M <= 32 && g.N <= 32 && g.ksplit == 0) {
+    const bool ak = g.a_cs == 1 && g.a_rs != 1, bk = g.b_rs == 1 && g.b_cs != 1;
+    for (long long z0 = 0; z0 < total; z0 += 4LL * 65535) {
+      const unsigned nblk = (unsigned)std::min<long long>(65535, (total - z0 + 3) / 4);
+      if (ak && bk) hipLaunchKernelGGL((k_gemm_small<true, true>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
+      else if (ak) hipLaunchKernelGGL((k_gemm_small<true, false>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
+      else if (bk) hipLaunchKernelGGL((k_gemm_small<false, true>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
+      else hipLaunchKernelGGL((k_gemm_small<false, false>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
+    }
+  } else if (g.N <= 32) {
+    gemm_orient<4, 1>(g, total, s);                 // 128 x 32 tiles (one head's width)
+  } else {
+    gemm_orient<2, 2>(g, total, s);                 // 64 x 64 tiles
+  }
   return hipGetLastError();
 }
 
@@ -414,9 +494,10 @@ hipError_t t_ln_bwd(const float* X, long long x_rs, int rows, int d, const float
                     const float* rstd, const float* dY, long long dy_rs, float* dX, long long dx_rs, float* dg,
                     float* db, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  const unsigned nb = (unsigned)((rows + 4 * TRAIN_LN_ROWS - 1) / (4 * TRAIN_LN_ROWS));
-  hipLaunchKernelGGL(k_ln_bwd, dim3(nb), dim3(256), 8 * d * sizeof(float), s, X, x_rs, rows, d, g, mean, rstd, dY, dy_rs,
-                     dX, dx_rs, dg, db);
+  hipLaunchKernelGGL(k_ln_bwd_rows, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, X, x_rs, rows, d, g, mean, rstd, dY,
+                     dy_rs, dX, dx_rs);
+  hipLaunchKernelGGL(k_ln_bwd_params, dim3((unsigned)((d + 63) / 64), (unsigned)((rows + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
+                     dim3(256), 0, s, X, x_rs, rows, d, mean, rstd, dY, dy_rs, dg, db);
   return hipGetLastError();
 }
 
