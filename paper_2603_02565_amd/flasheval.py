@@ -241,8 +241,28 @@ def fe_train_workspace_size(cfg: fe_config, B: int, T: int, M: int, K: int, L: i
     return n.value
 
 
+def _need(t, name: str, dtype, numel: int) -> None:
+    """Argument check for tensors handed to the library as raw pointers: dtype, size, contiguity."""
+    if t is None or isinstance(t, int):
+        return
+    if t.dtype != dtype or t.numel() != numel or not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous {dtype} tensor of {numel} elements, got {t.dtype} "
+                         f"{tuple(t.shape)}")
+
+
 def fe_train_grads(cfg: fe_config, params, B: int, T: int, M: int, K: int, L: int, x, ctx_ids, pool, lists, relevant,
                    loss_kind: int, loss, scores, grads, ws, stream=None) -> None:
+    import torch
+    n = fe_param_count(cfg)
+    _need(params, "params", torch.float32, n)
+    _need(grads, "grads", torch.float32, n)
+    _need(loss, "loss", torch.float32, 1)
+    _need(scores, "scores", torch.float32, B * K)
+    _need(x, "x", torch.float32, B * T * cfg.d)
+    _need(pool, "pool", torch.float32, B * M * cfg.d)
+    _need(ctx_ids, "ctx_ids", torch.int32, B * T)
+    _need(lists, "lists", torch.int32, B * K * L)
+    _need(relevant, "relevant", torch.int32, B * M)
     _check(load_library().fe_train_grads(ctypes.byref(cfg), _ptr(params), B, T, M, K, L, _ptr(x), _ptr(ctx_ids),
                                          _ptr(pool), _ptr(lists), _ptr(relevant), loss_kind, _ptr(loss), _ptr(scores),
                                          _ptr(grads), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),

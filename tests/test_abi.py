@@ -124,3 +124,19 @@ def test_train_validation(kw, dims, status):
         fe.fe_train_workspace_size(_train_cfg(c, **kw), *dims)
     assert e.value.status == status
     assert fe.load_library().fe_last_error().decode()
+
+
+def test_train_binding_rejects_wrong_dtype_before_any_call():
+    """The binding hands raw pointers to the library; a float64 loss buffer (say, under a float64
+    default dtype) would be half-written, so it is refused before the call."""
+    import torch
+    c = gen.config(0)
+    cfg = _train_cfg(c)
+    n = fe.fe_param_count(cfg)
+    P = torch.zeros(n, dtype=torch.float32)
+    with pytest.raises(ValueError, match="loss"):
+        fe.fe_train_grads(cfg, P, 1, c.T, c.M, c.K, c.L, None, None, None, None, None, fe.FE_LOSS_CE,
+                          torch.zeros(1, dtype=torch.float64), None, torch.zeros_like(P), torch.zeros(8, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="grads"):
+        fe.fe_train_grads(cfg, P, 1, c.T, c.M, c.K, c.L, None, None, None, None, None, fe.FE_LOSS_CE,
+                          torch.zeros(1), None, torch.zeros(n - 1), torch.zeros(8, dtype=torch.uint8))

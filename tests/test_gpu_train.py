@@ -38,10 +38,11 @@ def run_train(c, W, I, a, kind):
     x, pool = (None, None) if c.vocab else (f32(I["x"]), f32(I["pool"]))
     ids = i32(I["ctx_ids"]) if c.vocab else None
     lists, rel = i32(I["lists"]), i32(a)
-    ws = torch.empty(fe.fe_train_workspace_size(cfg, B, T, M, K, L), dtype=torch.uint8, device=dev)
+    # the workspace needs no initialisation: start it as all-ones bytes (NaN as floats, -1 as ints)
+    ws = torch.full((fe.fe_train_workspace_size(cfg, B, T, M, K, L),), 255, dtype=torch.uint8, device=dev)
     G = torch.full_like(P, float("nan"))
-    loss = torch.full((1,), float("nan"), device=dev)
-    scores = torch.full((B * K,), float("nan"), device=dev)
+    loss = torch.full((1,), float("nan"), dtype=torch.float32, device=dev)
+    scores = torch.full((B * K,), float("nan"), dtype=torch.float32, device=dev)
     fe.fe_train_grads(cfg, P, B, T, M, K, L, x, ids, pool, lists, rel, fe.LOSS_KIND[kind], loss, scores, G, ws)
     torch.cuda.synchronize()
     flat = G.cpu().numpy()

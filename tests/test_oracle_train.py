@@ -11,7 +11,16 @@ import gen
 import oracle
 from oracle import train
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """float64 as torch's default dtype inside these tests only (restored afterwards, so other test
+    modules collected in the same process keep float32)."""
+    old = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(old)
 
 
 def _tiny(cid=0, **kw):
