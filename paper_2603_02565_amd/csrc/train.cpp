@@ -112,12 +112,12 @@ struct Dims {
 // saved activations of one encoder block (pre-LN self-attention + FFN)
 struct EncAct {
   const float* x;                 // block input [R][d]
-  float *h1, *m1, *r1, *qkv, *P, *o, *x2, *h2, *m2, *r2, *f1, *a1, *y;
+  float *h1, *m1, *r1, *qkv, *P, *o, *x2, *h2, *m2, *r2, *a1, *y;   // a1 = relu(h2 W1 + b1)
 };
 // saved activations of one item-set layer (self-attention, cross-attention to the context, FFN)
 struct ItemAct {
   const float* x;
-  float *h1, *m1, *r1, *qkv, *P, *o, *x2, *h2, *m2, *r2, *q, *Pc, *oc, *x3, *h3, *m3, *r3, *f1, *a1, *y;
+  float *h1, *m1, *r1, *qkv, *P, *o, *x2, *h2, *m2, *r2, *q, *Pc, *oc, *x3, *h3, *m3, *r3, *a1, *y;
   float *Kl, *Vl;                 // keys and values of the context for this layer [B][T][d]
 };
 // one encoder stack: nseq sequences of S rows and the final LayerNorm
@@ -158,7 +158,7 @@ void plan_enc_stack(Arena& A, Stack& st, const Dims& D, int nseq, int S, const i
     a.P = A.get<float>((size_t)nseq * D.H * S * S);
     a.o = A.get<float>(R * d); a.x2 = A.get<float>(R * d);
     a.h2 = A.get<float>(R * d); a.m2 = A.get<float>(R); a.r2 = A.get<float>(R);
-    a.f1 = A.get<float>(R * F); a.a1 = A.get<float>(R * F);
+    a.a1 = A.get<float>(R * F);
     a.y = A.get<float>(R * d);
   }
   const size_t rows_out = first_row_only ? (size_t)nseq : R;
@@ -193,7 +193,7 @@ Plan make_plan(Arena& A, const Dims& D) {
     a.Pc = A.get<float>(B * D.H * U * T);
     a.oc = A.get<float>(R * d); a.x3 = A.get<float>(R * d);
     a.h3 = A.get<float>(R * d); a.m3 = A.get<float>(R); a.r3 = A.get<float>(R);
-    a.f1 = A.get<float>(R * F); a.a1 = A.get<float>(R * F);
+    a.a1 = A.get<float>(R * F);
     a.y = A.get<float>(R * d);
     a.Kl = A.get<float>(B * T * d);
     a.Vl = A.get<float>(B * T * d);
@@ -239,26 +239,30 @@ TGemm gemm0() {
   return g;
 }
 
-// Y = X W + b (+ Y when accumulate), X [R][din] rows of stride x_rs, W [din][dout] row-major
+// Y = [relu](X W + b [+ resid]), X [R][din] rows of stride x_rs, W [din][dout] row-major, resid
+// laid out as Y
 hipError_t linear(const float* X, long long x_rs, int R, int din, const float* W, const float* b, int dout, float* Y,
-                  long long y_rs, bool accumulate, hipStream_t s) {
+                  long long y_rs, const float* resid, bool relu, hipStream_t s) {
   TGemm g = gemm0();
   g.A = X; g.a_rs = x_rs; g.a_cs = 1;
   g.B = W; g.b_rs = dout; g.b_cs = 1;
   g.C = Y; g.c_rs = y_rs;
   g.bias = b;
+  g.R = resid;
+  g.relu = relu;
   g.M = R; g.N = dout; g.K = din;
-  g.beta = accumulate ? 1.f : 0.f;
   return t_gemm(g, s);
 }
 
-// dX (=, or += when accumulate) dY W^T
+// dX (=, or += when accumulate) dY W^T, zeroed where mask <= 0 (the backward of a ReLU whose
+// output is mask; null: none)
 hipError_t linear_dx(const float* dY, long long dy_rs, int R, int dout, const float* W, int din, float* dX,
-                     long long dx_rs, bool accumulate, hipStream_t s) {
+                     long long dx_rs, bool accumulate, const float* mask, hipStream_t s) {
   TGemm g = gemm0();
   g.A = dY; g.a_rs = dy_rs; g.a_cs = 1;
   g.B = W; g.b_rs = 1; g.b_cs = dout;
   g.C = dX; g.c_rs = dx_rs;
+  g.mask = mask;
   g.M = R; g.N = din; g.K = dout;
   g.beta = accumulate ? 1.f : 0.f;
   return t_gemm(g, s);
@@ -372,15 +376,12 @@ hipError_t enc_fwd(const float* W, const EncP& p, EncAct& a, const Dims& D, int 
                    hipStream_t s) {
   const int R = nseq * S, d = D.d, F = D.F;
   TRY(t_ln_fwd(a.x, d, R, d, W + p.ln1g, W + p.ln1b, a.h1, d, a.m1, a.r1, s));
-  TRY(linear(a.h1, d, R, d, W + p.wqkv, W + p.bqkv, 3 * d, a.qkv, 3 * d, false, s));
+  TRY(linear(a.h1, d, R, d, W + p.wqkv, W + p.bqkv, 3 * d, a.qkv, 3 * d, nullptr, false, s));
   TRY(attn_fwd(self_io(a.qkv, D, nseq, S, valid), D, a.P, a.o, d, (long long)S * d, s));
-  TRY(t_copy(a.x, a.x2, (long long)R * d, s));
-  TRY(linear(a.o, d, R, d, W + p.wo, W + p.bo, d, a.x2, d, true, s));
+  TRY(linear(a.o, d, R, d, W + p.wo, W + p.bo, d, a.x2, d, a.x, false, s));
   TRY(t_ln_fwd(a.x2, d, R, d, W + p.ln2g, W + p.ln2b, a.h2, d, a.m2, a.r2, s));
-  TRY(linear(a.h2, d, R, d, W + p.w1, W + p.b1, F, a.f1, F, false, s));
-  TRY(t_relu(a.f1, a.a1, (long long)R * F, s));
-  TRY(t_copy(a.x2, a.y, (long long)R * d, s));
-  return linear(a.a1, F, R, F, W + p.w2, W + p.b2, d, a.y, d, true, s);
+  TRY(linear(a.h2, d, R, d, W + p.w1, W + p.b1, F, a.a1, F, nullptr, true, s));
+  return linear(a.a1, F, R, F, W + p.w2, W + p.b2, d, a.y, d, a.x2, false, s);
 }
 
 // dx holds d loss / d y on entry and d loss / d x on return; parameter gradients are added to G.
@@ -389,18 +390,17 @@ hipError_t enc_bwd(const float* W, float* G, const EncP& p, const EncAct& a, con
   const int R = nseq * S, d = D.d, F = D.F;
   // FFN
   TRY(linear_dw(a.a1, F, R, F, dx, d, d, G + p.w2, G + p.b2, s));
-  TRY(linear_dx(dx, d, R, d, W + p.w2, F, pl.tF, F, false, s));
-  TRY(t_relu_bwd(a.f1, pl.tF, pl.tF, (long long)R * F, s));
+  TRY(linear_dx(dx, d, R, d, W + p.w2, F, pl.tF, F, false, a.a1, s));
   TRY(linear_dw(a.h2, d, R, d, pl.tF, F, F, G + p.w1, G + p.b1, s));
-  TRY(linear_dx(pl.tF, F, R, F, W + p.w1, d, pl.td, d, false, s));
+  TRY(linear_dx(pl.tF, F, R, F, W + p.w1, d, pl.td, d, false, nullptr, s));
   TRY(t_ln_bwd(a.x2, d, R, d, W + p.ln2g, a.m2, a.r2, pl.td, d, dx, d, G + p.ln2g, G + p.ln2b, s));
   // self-attention
   TRY(linear_dw(a.o, d, R, d, dx, d, d, G + p.wo, G + p.bo, s));
-  TRY(linear_dx(dx, d, R, d, W + p.wo, d, pl.td, d, false, s));
+  TRY(linear_dx(dx, d, R, d, W + p.wo, d, pl.td, d, false, nullptr, s));
   const AttnIO io = self_io(a.qkv, D, nseq, S, valid);
   TRY(attn_bwd(io, D, a.P, pl.td, d, (long long)S * d, pl.dqkv, pl.dqkv + d, pl.dqkv + 2 * d, pl.dP, s));
   TRY(linear_dw(a.h1, d, R, d, pl.dqkv, 3 * d, 3 * d, G + p.wqkv, G + p.bqkv, s));
-  TRY(linear_dx(pl.dqkv, 3 * d, R, 3 * d, W + p.wqkv, d, pl.td, d, false, s));
+  TRY(linear_dx(pl.dqkv, 3 * d, R, 3 * d, W + p.wqkv, d, pl.td, d, false, nullptr, s));
   return t_ln_bwd(a.x, d, R, d, W + p.ln1g, a.m1, a.r1, pl.td, d, dx, d, G + p.ln1g, G + p.ln1b, s);
 }
 
@@ -450,23 +450,19 @@ AttnIO cross_io(const ItemAct& a, const Dims& D, const int32_t* n_uniq) {
 hipError_t item_fwd(const float* W, const ItemP& p, const KvP& kv, ItemAct& a, const float* Qc, const Dims& D,
                     const int32_t* n_uniq, hipStream_t s) {
   const int R = D.B * D.U, d = D.d, F = D.F, Rc = D.B * D.T;
-  TRY(linear(Qc, d, Rc, d, W + kv.wk, W + kv.bk, d, a.Kl, d, false, s));
-  TRY(linear(Qc, d, Rc, d, W + kv.wv, W + kv.bv, d, a.Vl, d, false, s));
+  TRY(linear(Qc, d, Rc, d, W + kv.wk, W + kv.bk, d, a.Kl, d, nullptr, false, s));
+  TRY(linear(Qc, d, Rc, d, W + kv.wv, W + kv.bv, d, a.Vl, d, nullptr, false, s));
   TRY(t_ln_fwd(a.x, d, R, d, W + p.ln1g, W + p.ln1b, a.h1, d, a.m1, a.r1, s));
-  TRY(linear(a.h1, d, R, d, W + p.wqkv, W + p.bqkv, 3 * d, a.qkv, 3 * d, false, s));
+  TRY(linear(a.h1, d, R, d, W + p.wqkv, W + p.bqkv, 3 * d, a.qkv, 3 * d, nullptr, false, s));
   TRY(attn_fwd(self_io(a.qkv, D, D.B, D.U, n_uniq), D, a.P, a.o, d, (long long)D.U * d, s));
-  TRY(t_copy(a.x, a.x2, (long long)R * d, s));
-  TRY(linear(a.o, d, R, d, W + p.wo, W + p.bo, d, a.x2, d, true, s));
+  TRY(linear(a.o, d, R, d, W + p.wo, W + p.bo, d, a.x2, d, a.x, false, s));
   TRY(t_ln_fwd(a.x2, d, R, d, W + p.ln2g, W + p.ln2b, a.h2, d, a.m2, a.r2, s));
-  TRY(linear(a.h2, d, R, d, W + p.wq, W + p.bq, d, a.q, d, false, s));
+  TRY(linear(a.h2, d, R, d, W + p.wq, W + p.bq, d, a.q, d, nullptr, false, s));
   TRY(attn_fwd(cross_io(a, D, n_uniq), D, a.Pc, a.oc, d, (long long)D.U * d, s));
-  TRY(t_copy(a.x2, a.x3, (long long)R * d, s));
-  TRY(linear(a.oc, d, R, d, W + p.wo2, W + p.bo2, d, a.x3, d, true, s));
+  TRY(linear(a.oc, d, R, d, W + p.wo2, W + p.bo2, d, a.x3, d, a.x2, false, s));
   TRY(t_ln_fwd(a.x3, d, R, d, W + p.ln3g, W + p.ln3b, a.h3, d, a.m3, a.r3, s));
-  TRY(linear(a.h3, d, R, d, W + p.w1, W + p.b1, F, a.f1, F, false, s));
-  TRY(t_relu(a.f1, a.a1, (long long)R * F, s));
-  TRY(t_copy(a.x3, a.y, (long long)R * d, s));
-  return linear(a.a1, F, R, F, W + p.w2, W + p.b2, d, a.y, d, true, s);
+  TRY(linear(a.h3, d, R, d, W + p.w1, W + p.b1, F, a.a1, F, nullptr, true, s));
+  return linear(a.a1, F, R, F, W + p.w2, W + p.b2, d, a.y, d, a.x3, false, s);
 }
 
 // dx: d / d (layer output) in, d / d (layer input) out; d / d (encoded context) added to dQc
@@ -475,29 +471,28 @@ hipError_t item_bwd(const float* W, float* G, const ItemP& p, const KvP& kv, con
   const int R = D.B * D.U, d = D.d, F = D.F, Rc = D.B * D.T;
   // FFN
   TRY(linear_dw(a.a1, F, R, F, dx, d, d, G + p.w2, G + p.b2, s));
-  TRY(linear_dx(dx, d, R, d, W + p.w2, F, pl.tF, F, false, s));
-  TRY(t_relu_bwd(a.f1, pl.tF, pl.tF, (long long)R * F, s));
+  TRY(linear_dx(dx, d, R, d, W + p.w2, F, pl.tF, F, false, a.a1, s));
   TRY(linear_dw(a.h3, d, R, d, pl.tF, F, F, G + p.w1, G + p.b1, s));
-  TRY(linear_dx(pl.tF, F, R, F, W + p.w1, d, pl.td, d, false, s));
+  TRY(linear_dx(pl.tF, F, R, F, W + p.w1, d, pl.td, d, false, nullptr, s));
   TRY(t_ln_bwd(a.x3, d, R, d, W + p.ln3g, a.m3, a.r3, pl.td, d, dx, d, G + p.ln3g, G + p.ln3b, s));
   // cross-attention to the context
   TRY(linear_dw(a.oc, d, R, d, dx, d, d, G + p.wo2, G + p.bo2, s));
-  TRY(linear_dx(dx, d, R, d, W + p.wo2, d, pl.td, d, false, s));
+  TRY(linear_dx(dx, d, R, d, W + p.wo2, d, pl.td, d, false, nullptr, s));
   TRY(attn_bwd(cross_io(a, D, n_uniq), D, a.Pc, pl.td, d, (long long)D.U * d, pl.tq, pl.dKl, pl.dVl, pl.dP, s));
   TRY(linear_dw(a.h2, d, R, d, pl.tq, d, d, G + p.wq, G + p.bq, s));
-  TRY(linear_dx(pl.tq, d, R, d, W + p.wq, d, pl.td, d, false, s));
+  TRY(linear_dx(pl.tq, d, R, d, W + p.wq, d, pl.td, d, false, nullptr, s));
   TRY(t_ln_bwd(a.x2, d, R, d, W + p.ln2g, a.m2, a.r2, pl.td, d, dx, d, G + p.ln2g, G + p.ln2b, s));
   TRY(linear_dw(Qc, d, Rc, d, pl.dKl, d, d, G + kv.wk, G + kv.bk, s));
   TRY(linear_dw(Qc, d, Rc, d, pl.dVl, d, d, G + kv.wv, G + kv.bv, s));
-  TRY(linear_dx(pl.dKl, d, Rc, d, W + kv.wk, d, pl.dQc, d, true, s));
-  TRY(linear_dx(pl.dVl, d, Rc, d, W + kv.wv, d, pl.dQc, d, true, s));
+  TRY(linear_dx(pl.dKl, d, Rc, d, W + kv.wk, d, pl.dQc, d, true, nullptr, s));
+  TRY(linear_dx(pl.dVl, d, Rc, d, W + kv.wv, d, pl.dQc, d, true, nullptr, s));
   // set self-attention
   TRY(linear_dw(a.o, d, R, d, dx, d, d, G + p.wo, G + p.bo, s));
-  TRY(linear_dx(dx, d, R, d, W + p.wo, d, pl.td, d, false, s));
+  TRY(linear_dx(dx, d, R, d, W + p.wo, d, pl.td, d, false, nullptr, s));
   TRY(attn_bwd(self_io(a.qkv, D, D.B, D.U, n_uniq), D, a.P, pl.td, d, (long long)D.U * d, pl.dqkv, pl.dqkv + d,
                pl.dqkv + 2 * d, pl.dP, s));
   TRY(linear_dw(a.h1, d, R, d, pl.dqkv, 3 * d, 3 * d, G + p.wqkv, G + p.bqkv, s));
-  TRY(linear_dx(pl.dqkv, 3 * d, R, 3 * d, W + p.wqkv, d, pl.td, d, false, s));
+  TRY(linear_dx(pl.dqkv, 3 * d, R, 3 * d, W + p.wqkv, d, pl.td, d, false, nullptr, s));
   return t_ln_bwd(a.x, d, R, d, W + p.ln1g, a.m1, a.r1, pl.td, d, dx, d, G + p.ln1g, G + p.ln1b, s);
 }
 
@@ -546,7 +541,7 @@ hipError_t run_step(const float* W, float* G, const PMap& pm, Plan& pl, const In
   // cross-sequence module over the K lists of each request (Section 4.4) and the linear head
   TRY(stack_fwd(W, pm.cross, pm.cross_g, pm.cross_b, pl.cross, pl.seqs.out, D, s));
   const int Rx = D.B * D.K;
-  TRY(linear(pl.cross.out, d, Rx, d, W + pm.head_w, W + pm.head_b, 1, pl.scores, 1, false, s));
+  TRY(linear(pl.cross.out, d, Rx, d, W + pm.head_w, W + pm.head_b, 1, pl.scores, 1, nullptr, false, s));
   if (in.scores_out)
     TRY(t_copy(pl.scores, in.scores_out, (long long)Rx, s));
   // ---- loss (Section 4.5) with the labels of Appendix B.1

@@ -15,12 +15,17 @@ constexpr int TRAIN_COL_ROWS = 64;   // rows per workgroup of a column reduction
 // z = z1 * nb2 + z2.  Element (i, k) of A[z] is A[z1*a_b1 + z2*a_b2 + i*a_rs + k*a_cs]; B (k, j)
 // and C (i, j) likewise (C with unit column stride).  ksplit > 0: the K range is cut into chunks
 // of ksplit (a multiple of 32) and each chunk adds alpha * its partial product into C atomically (beta must be 1,
-// bias null); the sum order then varies from run to run.
+// bias and the epilogue null); the sum order then varies from run to run.
 struct TGemm {
   const float* A;
   const float* B;
   float* C;
   const float* bias;
+  // epilogue, in this order after alpha and bias: + R (residual, laid out as C); relu; times
+  // [mask > 0] (mask laid out as C).  Null / 0: not applied.  Not with ksplit.
+  const float* R;
+  int relu;
+  const float* mask;
   int M, N, K;
   long long a_rs, a_cs, b_rs, b_cs, c_rs;
   long long a_b1, a_b2, b_b1, b_b2, c_b1, c_b2;
@@ -43,12 +48,7 @@ hipError_t t_softmax_fwd(const float* S, float* P, int nbatch, int nb2, int nq, 
                          const int32_t* qlen, const int32_t* klen, hipStream_t s);
 // dP <- scale * P * (dP - rowsum(P * dP)): the gradient of the pre-scale scores, in place
 hipError_t t_softmax_bwd(const float* P, float* dP, long long rows, int nk, float scale, hipStream_t s);
-hipError_t t_add(const float* a, const float* b, float* y, long long n, hipStream_t s);
 hipError_t t_copy(const float* x, float* y, long long n, hipStream_t s);
-hipError_t t_acc(float* y, const float* x, long long n, hipStream_t s);
-hipError_t t_relu(const float* x, float* y, long long n, hipStream_t s);
-// dx = x > 0 ? dy : 0
-hipError_t t_relu_bwd(const float* x, const float* dy, float* dx, long long n, hipStream_t s);
 hipError_t t_fill(float* y, long long n, float v, hipStream_t s);
 // db[j] += sum over rows of dY[r][j]
 hipError_t t_colsum(const float* dY, long long rs, int rows, int cols, float* db, hipStream_t s);

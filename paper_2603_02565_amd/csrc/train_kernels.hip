@@ -39,6 +39,8 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
   const float* A = g.A + z1 * g.a_b1 + z2 * g.a_b2;
   const float* B = g.B + z1 * g.b_b1 + z2 * g.b_b2;
   float* C = g.C + z1 * g.c_b1 + z2 * g.c_b2;
+  const float* Rz = g.R + z1 * g.c_b1 + z2 * g.c_b2;
+  const float* Mz = g.mask + z1 * g.c_b1 + z2 * g.c_b2;
   const int i0 = blockIdx.y * TM, j0 = blockIdx.x * TN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wi = (wave / WN) * 32, wj = (wave % WN) * 32;
@@ -93,12 +95,16 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
       const int i = i0 + wi + 8 * q + 4 * lk + e;
       if (i >= g.M) continue;
       float r = g.alpha * acc[4 * q + e];
-      float* c = C + i * g.c_rs + j;
+      const long long o = i * g.c_rs + j;
+      float* c = C + o;
       if (g.ksplit > 0) {
         atomicAdd(c, r);
         continue;
       }
       if (g.bias) r += g.bias[j];
+      if (g.R) r += Rz[o];
+      if (g.relu) r = fmaxf(r, 0.f);
+      if (g.mask && !(Mz[o] > 0.f)) r = 0.f;
       *c = g.beta != 0.f ? r + g.beta * *c : r;
     }
 }
@@ -117,6 +123,8 @@ __global__ __launch_bounds__(256) void k_gemm_small(TGemm g, int z0) {
   const float* A = g.A + z1 * g.a_b1 + z2 * g.a_b2;
   const float* B = g.B + z1 * g.b_b1 + z2 * g.b_b2;
   float* C = g.C + z1 * g.c_b1 + z2 * g.c_b2;
+  const float* Rz = g.R + z1 * g.c_b1 + z2 * g.c_b2;
+  const float* Mz = g.mask + z1 * g.c_b1 + z2 * g.c_b2;
   const int lr = lane & 31, lk = lane >> 5;
   float ra[N1], rb[N1];
   auto load = [&](int k0) {
@@ -155,8 +163,12 @@ __global__ __launch_bounds__(256) void k_gemm_small(TGemm g, int z0) {
       const int i = 8 * q + 4 * lk + e;
       if (i >= g.M) continue;
       float r = g.alpha * acc[4 * q + e];
+      const long long o = i * g.c_rs + lr;
       if (g.bias) r += g.bias[lr];
-      float* c = C + i * g.c_rs + lr;
+      if (g.R) r += Rz[o];
+      if (g.relu) r = fmaxf(r, 0.f);
+      if (g.mask && !(Mz[o] > 0.f)) r = 0.f;
+      float* c = C + o;
       *c = g.beta != 0.f ? r + g.beta * *c : r;
     }
 }
@@ -269,25 +281,9 @@ __global__ __launch_bounds__(256) void k_softmax_bwd(const float* P, float* dP, 
 // ------------------------------------------------------------------------------------------
 // Elementwise steps over n values.
 // ------------------------------------------------------------------------------------------
-__global__ void k_add(const float* a, const float* b, float* y, long long n) {
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) y[i] = a[i] + b[i];
-}
 __global__ void k_copy(const float* x, float* y, long long n) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) y[i] = x[i];
-}
-__global__ void k_acc(float* y, const float* x, long long n) {
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) y[i] += x[i];
-}
-__global__ void k_relu(const float* x, float* y, long long n) {
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) y[i] = fmaxf(x[i], 0.f);
-}
-__global__ void k_relu_bwd(const float* x, const float* dy, float* dx, long long n) {
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) dx[i] = x[i] > 0.f ? dy[i] : 0.f;
 }
 __global__ void k_fill(float* y, long long n, float v) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
@@ -462,7 +458,7 @@ void gemm_orient(const TGemm& g, long long total, hipStream_t s) {
 
 hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.nbatch <= 0) return hipSuccess;
-  if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.ksplit % GK)) return hipErrorInvalidValue;
+  if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.R || g.relu || g.mask || g.ksplit % GK)) return hipErrorInvalidValue;
   const int nk = g.ksplit > 0 ? (g.K + g.ksplit - 1) / g.ksplit : 1;
   const long long total = (long long)g.nbatch * nk;
   if (g.M <= 32 && g.N <= 32 && g.ksplit == 0) {
@@ -516,24 +512,8 @@ hipError_t t_softmax_bwd(const float* P, float* dP, long long rows, int nk, floa
   return hipGetLastError();
 }
 
-hipError_t t_add(const float* a, const float* b, float* y, long long n, hipStream_t s) {
-  if (n > 0) hipLaunchKernelGGL(k_add, dim3(blocks(n)), dim3(256), 0, s, a, b, y, n);
-  return hipGetLastError();
-}
 hipError_t t_copy(const float* x, float* y, long long n, hipStream_t s) {
   if (n > 0) hipLaunchKernelGGL(k_copy, dim3(blocks(n)), dim3(256), 0, s, x, y, n);
-  return hipGetLastError();
-}
-hipError_t t_acc(float* y, const float* x, long long n, hipStream_t s) {
-  if (n > 0) hipLaunchKernelGGL(k_acc, dim3(blocks(n)), dim3(256), 0, s, y, x, n);
-  return hipGetLastError();
-}
-hipError_t t_relu(const float* x, float* y, long long n, hipStream_t s) {
-  if (n > 0) hipLaunchKernelGGL(k_relu, dim3(blocks(n)), dim3(256), 0, s, x, y, n);
-  return hipGetLastError();
-}
-hipError_t t_relu_bwd(const float* x, const float* dy, float* dx, long long n, hipStream_t s) {
-  if (n > 0) hipLaunchKernelGGL(k_relu_bwd, dim3(blocks(n)), dim3(256), 0, s, x, dy, dx, n);
   return hipGetLastError();
 }
 hipError_t t_fill(float* y, long long n, float v, hipStream_t s) {
