@@ -268,7 +268,7 @@ hipError_t linear_dx(const float* dY, long long dy_rs, int R, int dout, const fl
   return t_gemm(g, s);
 }
 
-// dW += X^T dY over the R rows, db += column sums of dY (db may be null)
+// dW += X^T dY over the R rows, db += column sums of dY (db may be null; summed by the same launch)
 hipError_t linear_dw(const float* X, long long x_rs, int R, int din, const float* dY, long long dy_rs, int dout,
                      float* dW, float* db, hipStream_t s) {
   TGemm g = gemm0();
@@ -282,9 +282,8 @@ hipError_t linear_dw(const float* X, long long x_rs, int R, int din, const float
   long long chunks = std::max(1LL, 2048 / tiles);
   long long ks = std::max(256LL, (R + chunks - 1) / chunks);
   g.ksplit = (int)((ks + 31) / 32 * 32);
-  TRY(t_gemm(g, s));
-  if (db) TRY(t_colsum(dY, dy_rs, R, dout, db, s));
-  return hipSuccess;
+  g.colsum = db;
+  return t_gemm(g, s);
 }
 
 // Multi-head attention over nseq sequences, all heads at once.  Query rows of sequence z start at

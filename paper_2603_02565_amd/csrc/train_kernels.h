@@ -2,6 +2,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
+#include <type_traits>
 
 #include "flasheval.h"
 
@@ -26,6 +27,9 @@ struct TGemm {
   const float* R;
   int relu;
   const float* mask;
+  // colsum (k_gemm only, nbatch 1): colsum[j] += alpha * sum_k B[k][j] over this launch's k range (the
+  // bias gradient when B is dY and k runs over rows); null: not computed.
+  float* colsum;
   int M, N, K;
   long long a_rs, a_cs, b_rs, b_cs, c_rs;
   long long a_b1, a_b2, b_b1, b_b2, c_b1, c_b2;
@@ -50,8 +54,6 @@ hipError_t t_softmax_fwd(const float* S, float* P, int nbatch, int nb2, int nq, 
 hipError_t t_softmax_bwd(const float* P, float* dP, long long rows, int nk, float scale, hipStream_t s);
 hipError_t t_copy(const float* x, float* y, long long n, hipStream_t s);
 hipError_t t_fill(float* y, long long n, float v, hipStream_t s);
-// db[j] += sum over rows of dY[r][j]
-hipError_t t_colsum(const float* dY, long long rs, int rows, int cols, float* db, hipStream_t s);
 // Y[b][r] = row idx[b*idx_bs + r] of the table at T + b*t_bs, for r < nvalid[b] (all rows if null)
 // and ids in [0, n_table); other rows are zero
 hipError_t t_gather(const float* T, long long t_bs, int n_table, const int32_t* idx, int idx_bs, const int32_t* nvalid,

@@ -76,6 +76,8 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
     }
   };
   f32x16 acc = {};
+  const bool csum = g.colsum && blockIdx.y == 0 && threadIdx.x < TN;   // first row tile: column sums of B
+  float cs = 0.f;
   load(kbeg);
   for (int k0 = kbeg; k0 < kend; k0 += GK) {
     store();
@@ -84,8 +86,12 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
 #pragma unroll
     for (int t = 0; t < GK / 2; ++t)
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[2 * t + lk][wi + lr], Bs[2 * t + lk][wj + lr], acc, 0, 0, 0);
+    if (csum)
+#pragma unroll
+      for (int kk = 0; kk < GK; ++kk) cs += Bs[kk][threadIdx.x];
     __syncthreads();
   }
+  if (csum && j0 + (int)threadIdx.x < g.N) atomicAdd(&g.colsum[j0 + threadIdx.x], g.alpha * cs);
   const int j = j0 + wj + lr;
   if (j >= g.N) return;
 #pragma unroll
@@ -245,6 +251,9 @@ __global__ __launch_bounds__(256) void k_ln_bwd_params(const float* X, long long
 // Softmax over the keys of every score row: P = softmax(scale S) on keys j < klen(z1), 0 beyond;
 // query rows i >= qlen(z1) are all zero.  Row r of batch z = z1*nb2 + z2 is S + z*nq*nk + r*nk.
 // ------------------------------------------------------------------------------------------
+// One wave per row; NV > 0: the row (nk <= 64 NV) stays in registers between the passes, NV = 0: it
+// is re-read from memory (longer rows).
+template <int NV>
 __global__ __launch_bounds__(256) void k_softmax_fwd(const float* S, float* P, int nbatch, int nb2, int nq, int nk,
                                                      float scale, const int32_t* qlen, const int32_t* klen) {
   const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -255,27 +264,72 @@ __global__ __launch_bounds__(256) void k_softmax_fwd(const float* S, float* P, i
   const bool live = (qlen ? i < qlen[z1] : true) && kl > 0;
   const float* s = S + row * nk;
   float* p = P + row * nk;
-  float mx = -INFINITY;
-  for (int j = lane; j < kl; j += 64) mx = fmaxf(mx, s[j] * scale);
-  mx = wave_max(mx);
-  float sum = 0.f;
-  for (int j = lane; j < kl; j += 64) sum += expf(s[j] * scale - mx);
-  sum = wave_sum(sum);
-  const float inv = live ? 1.f / sum : 0.f;
-  for (int j = lane; j < nk; j += 64) p[j] = (live && j < kl) ? expf(s[j] * scale - mx) * inv : 0.f;
+  if constexpr (NV > 0) {
+    float v[NV];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int j = lane + 64 * u;
+      v[u] = j < kl ? s[j] * scale : -INFINITY;
+      mx = fmaxf(mx, v[u]);
+    }
+    mx = wave_max(mx);
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int j = lane + 64 * u;
+      v[u] = j < kl ? expf(v[u] - mx) : 0.f;
+      sum += v[u];
+    }
+    sum = wave_sum(sum);
+    const float inv = live ? 1.f / sum : 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int j = lane + 64 * u;
+      if (j < nk) p[j] = v[u] * inv;
+    }
+  } else {
+    float mx = -INFINITY;
+    for (int j = lane; j < kl; j += 64) mx = fmaxf(mx, s[j] * scale);
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int j = lane; j < kl; j += 64) sum += expf(s[j] * scale - mx);
+    sum = wave_sum(sum);
+    const float inv = live ? 1.f / sum : 0.f;
+    for (int j = lane; j < nk; j += 64) p[j] = (live && j < kl) ? expf(s[j] * scale - mx) * inv : 0.f;
+  }
 }
 
 // dS = scale P (dP - sum_j P_j dP_j), in place over dP.
+template <int NV>
 __global__ __launch_bounds__(256) void k_softmax_bwd(const float* P, float* dP, long long rows, int nk, float scale) {
   const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   const float* p = P + row * nk;
   float* dp = dP + row * nk;
-  float s = 0.f;
-  for (int j = lane; j < nk; j += 64) s += p[j] * dp[j];
-  s = wave_sum(s);
-  for (int j = lane; j < nk; j += 64) dp[j] = scale * p[j] * (dp[j] - s);
+  if constexpr (NV > 0) {
+    float pv[NV], gv[NV];
+    float s = 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int j = lane + 64 * u;
+      pv[u] = j < nk ? p[j] : 0.f;
+      gv[u] = j < nk ? dp[j] : 0.f;
+      s += pv[u] * gv[u];
+    }
+    s = wave_sum(s);
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int j = lane + 64 * u;
+      if (j < nk) dp[j] = scale * pv[u] * (gv[u] - s);
+    }
+  } else {
+    float s = 0.f;
+    for (int j = lane; j < nk; j += 64) s += p[j] * dp[j];
+    s = wave_sum(s);
+    for (int j = lane; j < nk; j += 64) dp[j] = scale * p[j] * (dp[j] - s);
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -289,21 +343,6 @@ __global__ void k_fill(float* y, long long n, float v) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) y[i] = v;
 }
-// db[j] += sum over rows of dY[r][j] (row stride rs): a workgroup takes 64 columns x
-// TRAIN_COL_ROWS rows, its four waves every fourth row, then one atomic per column.
-__global__ __launch_bounds__(256) void k_colsum(const float* dY, long long rs, int rows, int cols, float* db) {
-  __shared__ float part[4][64];
-  const int j = blockIdx.x * 64 + (threadIdx.x & 63), w = threadIdx.x >> 6;
-  const int r0 = blockIdx.y * TRAIN_COL_ROWS, r1 = min(rows, r0 + TRAIN_COL_ROWS);
-  float s = 0.f;
-  if (j < cols)
-    for (int r = r0 + w; r < r1; r += 4) s += dY[r * rs + j];
-  part[w][threadIdx.x & 63] = s;
-  __syncthreads();
-  if (w == 0 && j < cols) atomicAdd(&db[j], part[0][threadIdx.x] + part[1][threadIdx.x] + part[2][threadIdx.x] +
-                                               part[3][threadIdx.x]);
-}
-
 // Y[b][r] = row idx[b][r] of table T + b*t_bs for r < n (n = nvalid ? nvalid[b] : rows); rows past
 // n and ids outside [0, n_table) give zero rows.
 __global__ void k_gather(const float* T, long long t_bs, int n_table, const int32_t* idx, int idx_bs,
@@ -459,9 +498,10 @@ void gemm_orient(const TGemm& g, long long total, hipStream_t s) {
 hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.nbatch <= 0) return hipSuccess;
   if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.R || g.relu || g.mask || g.ksplit % GK)) return hipErrorInvalidValue;
+  if (g.colsum && g.nbatch != 1) return hipErrorInvalidValue;
   const int nk = g.ksplit > 0 ? (g.K + g.ksplit - 1) / g.ksplit : 1;
   const long long total = (long long)g.nbatch * nk;
-  if (g.M <= 32 && g.N <= 32 && g.ksplit == 0) {
+  if (g.M <= 32 && g.N <= 32 && g.ksplit == 0 && !g.colsum) {
     const bool ak = g.a_cs == 1 && g.a_rs != 1, bk = g.b_rs == 1 && g.b_cs != 1;
     for (long long z0 = 0; z0 < total; z0 += 4LL * 65535) {
       const unsigned nblk = (unsigned)std::min<long long>(65535, (total - z0 + 3) / 4);
@@ -497,33 +537,40 @@ hipError_t t_ln_bwd(const float* X, long long x_rs, int rows, int d, const float
   return hipGetLastError();
 }
 
+template <class F>
+void by_row_length(int nk, F&& launch) {
+  if (nk <= 64) launch(std::integral_constant<int, 1>());
+  else if (nk <= 128) launch(std::integral_constant<int, 2>());
+  else if (nk <= 256) launch(std::integral_constant<int, 4>());
+  else if (nk <= 512) launch(std::integral_constant<int, 8>());
+  else launch(std::integral_constant<int, 0>());
+}
+
 hipError_t t_softmax_fwd(const float* S, float* P, int nbatch, int nb2, int nq, int nk, float scale,
                          const int32_t* qlen, const int32_t* klen, hipStream_t s) {
   const long long rows = (long long)nbatch * nq;
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_softmax_fwd, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, S, P, nbatch, nb2, nq, nk, scale,
-                     qlen, klen);
+  by_row_length(nk, [&](auto nv) {
+    hipLaunchKernelGGL((k_softmax_fwd<decltype(nv)::value>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, S, P,
+                       nbatch, nb2, nq, nk, scale, qlen, klen);
+  });
   return hipGetLastError();
 }
 
 hipError_t t_softmax_bwd(const float* P, float* dP, long long rows, int nk, float scale, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_softmax_bwd, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, P, dP, rows, nk, scale);
+  by_row_length(nk, [&](auto nv) {
+    hipLaunchKernelGGL((k_softmax_bwd<decltype(nv)::value>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, P, dP,
+                       rows, nk, scale);
+  });
   return hipGetLastError();
 }
-
 hipError_t t_copy(const float* x, float* y, long long n, hipStream_t s) {
   if (n > 0) hipLaunchKernelGGL(k_copy, dim3(blocks(n)), dim3(256), 0, s, x, y, n);
   return hipGetLastError();
 }
 hipError_t t_fill(float* y, long long n, float v, hipStream_t s) {
   if (n > 0) hipLaunchKernelGGL(k_fill, dim3(blocks(n)), dim3(256), 0, s, y, n, v);
-  return hipGetLastError();
-}
-hipError_t t_colsum(const float* dY, long long rs, int rows, int cols, float* db, hipStream_t s) {
-  if (rows <= 0 || cols <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_colsum, dim3((unsigned)((cols + 63) / 64), (unsigned)((rows + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
-                     dim3(256), 0, s, dY, rs, rows, cols, db);
   return hipGetLastError();
 }
 hipError_t t_gather(const float* T, long long t_bs, int n_table, const int32_t* idx, int idx_bs, const int32_t* nvalid,
