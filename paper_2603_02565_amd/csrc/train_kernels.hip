@@ -380,16 +380,34 @@ __global__ void k_assemble_f32(const float* H, int U_cap, const int32_t* slot, i
   const float* src = j == 0 ? cls : H + ((long long)b * U_cap + sl) * d;
   for (int e = threadIdx.x; e < d; e += blockDim.x) o[e] = (sl >= 0 ? src[e] : 0.f) + pos[(long long)j * d + e];
 }
-// the assembly's backward: dH[b][slot] += dseq rows, dpos[j] += dseq[.][.][j], dcls += dseq[.][.][0]
-__global__ void k_assemble_bwd(const float* dseq, int U_cap, const int32_t* slot, int K, int L, int d, float* dH,
-                               float* dcls, float* dpos) {
-  const int b = blockIdx.z, k = blockIdx.y, j = blockIdx.x;
+// the assembly's backward, element rows: dH[b][slot] += dseq rows (a distinct element's row receives
+// the sum over its occurrences)
+__global__ void k_assemble_bwd(const float* dseq, int U_cap, const int32_t* slot, int K, int L, int d, float* dH) {
+  const int b = blockIdx.z, k = blockIdx.y, j = blockIdx.x + 1;
   const float* g = dseq + (((long long)b * K + k) * (L + 1) + j) * d;
-  const int sl = j == 0 ? 0 : slot[((long long)b * K + k) * L + j - 1];
-  float* dst = j == 0 ? dcls : dH + ((long long)b * U_cap + sl) * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) {
-    if (sl >= 0) atomicAdd(&dst[e], g[e]);
-    atomicAdd(&dpos[(long long)j * d + e], g[e]);
+  const int sl = slot[((long long)b * K + k) * L + j - 1];
+  if (sl < 0) return;
+  float* dst = dH + ((long long)b * U_cap + sl) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) atomicAdd(&dst[e], g[e]);
+}
+
+// ... and positions and [CLS]: dpos[c] += sum over the B K sequences of dseq[.][c] for the (L+1) d
+// entries c of a sequence, dcls[e] += the same sums of row 0.  64 entries x TRAIN_COL_ROWS sequences
+// per workgroup, one atomic per entry and workgroup.
+__global__ __launch_bounds__(256) void k_assemble_bwd_pos(const float* dseq, int nseq, int cols, int d, float* dpos,
+                                                          float* dcls) {
+  __shared__ float part[4][64];
+  const int c = blockIdx.x * 64 + (threadIdx.x & 63), w = threadIdx.x >> 6;
+  const int r0 = blockIdx.y * TRAIN_COL_ROWS, r1 = min(nseq, r0 + TRAIN_COL_ROWS);
+  float sum = 0.f;
+  if (c < cols)
+    for (int r = r0 + w; r < r1; r += 4) sum += dseq[(long long)r * cols + c];
+  part[w][threadIdx.x & 63] = sum;
+  __syncthreads();
+  if (w == 0 && c < cols) {
+    const float t = part[0][threadIdx.x] + part[1][threadIdx.x] + part[2][threadIdx.x] + part[3][threadIdx.x];
+    atomicAdd(&dpos[c], t);
+    if (c < d) atomicAdd(&dcls[c], t);
   }
 }
 
@@ -595,8 +613,12 @@ hipError_t t_assemble(const float* H, int B, int U_cap, const int32_t* slot, int
 }
 hipError_t t_assemble_bwd(const float* dseq, int B, int U_cap, const int32_t* slot, int K, int L, int d, float* dH,
                           float* dcls, float* dpos, hipStream_t s) {
-  hipLaunchKernelGGL(k_assemble_bwd, dim3((unsigned)(L + 1), (unsigned)K, (unsigned)B), dim3(128), 0, s, dseq, U_cap,
-                     slot, K, L, d, dH, dcls, dpos);
+  if (L > 0)
+    hipLaunchKernelGGL(k_assemble_bwd, dim3((unsigned)L, (unsigned)K, (unsigned)B), dim3(128), 0, s, dseq, U_cap, slot, K,
+                       L, d, dH);
+  const int nseq = B * K, cols = (L + 1) * d;
+  hipLaunchKernelGGL(k_assemble_bwd_pos, dim3((unsigned)((cols + 63) / 64), (unsigned)((nseq + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
+                     dim3(256), 0, s, dseq, nseq, cols, d, dpos, dcls);
   return hipGetLastError();
 }
 hipError_t t_loss(const float* scores, const int32_t* lists, const int32_t* relevant, int M, int B, int K, int L, int kind,
