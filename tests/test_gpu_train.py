@@ -136,3 +136,19 @@ def test_full_recsys_batch():
     want_b = float(np.mean(np.sum(2 * (sd - r) / c.K, 1)))
     assert abs(float(g["head.b"][0]) - want_b) <= 1e-4 * max(1.0, abs(want_b))
     assert all(np.all(np.isfinite(v)) for v in g.values())
+
+
+def test_long_context():
+    """The long-context model shape (d 256, 8 heads) over 2048 context rows: score rows longer than
+    512 keys take the softmax path that re-reads them from memory."""
+    c = gen.config(3, B=1, T=2048, K=4, L=5, M=30, n_layers=1, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "ce")
+
+
+def test_many_lists():
+    """300 lists per request: cross-sequence score rows of 300 keys (eight per lane in registers),
+    and a loss over 300 scores."""
+    c = gen.config(1, B=1, T=16, K=300, L=3, M=150, n_layers=1, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "bce")
