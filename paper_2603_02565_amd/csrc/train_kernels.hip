@@ -25,13 +25,13 @@ namespace {
 constexpr int GK = 32;
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-template <int WM, int WN, bool AK, bool BK>
+template <int WM, int WN, bool AK, bool BK, bool VA, bool VB>
 __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
   static_assert(WM * WN == 4, "four waves");
   constexpr int TM = 32 * WM, TN = 32 * WN, PA = TM + 4, PB = TN + 4;
   constexpr int NA = GK * TM / 256, NB = GK * TN / 256;   // elements per thread per k-step
-  __shared__ float As[GK][PA];
-  __shared__ float Bs[GK][PB];
+  __shared__ __align__(16) float As[GK][PA];
+  __shared__ __align__(16) float Bs[GK][PB];
   const int zz = z0 + blockIdx.z, z = zz % nz, kc = zz / nz;
   const int z1 = z / g.nb2, z2 = z % g.nb2;
   const int kbeg = g.ksplit > 0 ? kc * g.ksplit : 0;
@@ -46,33 +46,103 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
   const int wi = (wave / WN) * 32, wj = (wave % WN) * 32;
   const int lr = lane & 31, lk = lane >> 5;
   float ra[NA], rb[NB];
-  // the operands of k-step k0 into registers (zero outside the matrices and past kend)
+  // the operands of k-step k0 into registers (zero outside the matrices and past kend).  VA / VB:
+  // four consecutive elements of the contiguous index per load (the launcher has checked that
+  // they are 16-byte aligned); NA / NB stay the number of scalars per thread.
   auto load = [&](int k0) {
+    if constexpr (VA) {
 #pragma unroll
-    for (int t = 0; t < NA; ++t) {
-      const int e = threadIdx.x + 256 * t;
-      const int kk = AK ? e % GK : e / TM, mm = AK ? e / GK : e % TM;
-      const int i = i0 + mm, k = k0 + kk;
-      ra[t] = (i < g.M && k < kend) ? A[i * g.a_rs + k * g.a_cs] : 0.f;
+      for (int q = 0; q < NA / 4; ++q) {
+        const int e = threadIdx.x + 256 * q;
+        const int i = AK ? i0 + e / (GK / 4) : i0 + 4 * (e % (TM / 4));
+        const int k = AK ? k0 + 4 * (e % (GK / 4)) : k0 + e / (TM / 4);
+        const float* src = A + i * g.a_rs + k * g.a_cs;
+        if (AK ? (i < g.M && k + 3 < kend) : (i + 3 < g.M && k < kend)) {
+          const float4 v = *reinterpret_cast<const float4*>(src);
+          ra[4 * q] = v.x; ra[4 * q + 1] = v.y; ra[4 * q + 2] = v.z; ra[4 * q + 3] = v.w;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            ra[4 * q + c] = (AK ? (i < g.M && k + c < kend) : (i + c < g.M && k < kend))
+                                ? src[AK ? c : c * g.a_rs] : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < NA; ++t) {
+        const int e = threadIdx.x + 256 * t;
+        const int kk = AK ? e % GK : e / TM, mm = AK ? e / GK : e % TM;
+        const int i = i0 + mm, k = k0 + kk;
+        ra[t] = (i < g.M && k < kend) ? A[i * g.a_rs + k * g.a_cs] : 0.f;
+      }
     }
+    if constexpr (VB) {
 #pragma unroll
-    for (int t = 0; t < NB; ++t) {
-      const int e = threadIdx.x + 256 * t;
-      const int kk = BK ? e % GK : e / TN, nn = BK ? e / GK : e % TN;
-      const int j = j0 + nn, k = k0 + kk;
-      rb[t] = (j < g.N && k < kend) ? B[k * g.b_rs + j * g.b_cs] : 0.f;
+      for (int q = 0; q < NB / 4; ++q) {
+        const int e = threadIdx.x + 256 * q;
+        const int j = BK ? j0 + e / (GK / 4) : j0 + 4 * (e % (TN / 4));
+        const int k = BK ? k0 + 4 * (e % (GK / 4)) : k0 + e / (TN / 4);
+        const float* src = B + k * g.b_rs + j * g.b_cs;
+        if (BK ? (j < g.N && k + 3 < kend) : (j + 3 < g.N && k < kend)) {
+          const float4 v = *reinterpret_cast<const float4*>(src);
+          rb[4 * q] = v.x; rb[4 * q + 1] = v.y; rb[4 * q + 2] = v.z; rb[4 * q + 3] = v.w;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            rb[4 * q + c] = (BK ? (j < g.N && k + c < kend) : (j + c < g.N && k < kend))
+                                ? src[BK ? c : c * g.b_cs] : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < NB; ++t) {
+        const int e = threadIdx.x + 256 * t;
+        const int kk = BK ? e % GK : e / TN, nn = BK ? e / GK : e % TN;
+        const int j = j0 + nn, k = k0 + kk;
+        rb[t] = (j < g.N && k < kend) ? B[k * g.b_rs + j * g.b_cs] : 0.f;
+      }
     }
   };
   auto store = [&]() {
+    if constexpr (VA) {
 #pragma unroll
-    for (int t = 0; t < NA; ++t) {
-      const int e = threadIdx.x + 256 * t;
-      As[AK ? e % GK : e / TM][AK ? e / GK : e % TM] = ra[t];
+      for (int q = 0; q < NA / 4; ++q) {
+        const int e = threadIdx.x + 256 * q;
+        if constexpr (AK) {
+          const int mm = e / (GK / 4), kq = 4 * (e % (GK / 4));
+#pragma unroll
+          for (int c = 0; c < 4; ++c) As[kq + c][mm] = ra[4 * q + c];
+        } else {
+          *reinterpret_cast<float4*>(&As[e / (TM / 4)][4 * (e % (TM / 4))]) =
+              make_float4(ra[4 * q], ra[4 * q + 1], ra[4 * q + 2], ra[4 * q + 3]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < NA; ++t) {
+        const int e = threadIdx.x + 256 * t;
+        As[AK ? e % GK : e / TM][AK ? e / GK : e % TM] = ra[t];
+      }
     }
+    if constexpr (VB) {
 #pragma unroll
-    for (int t = 0; t < NB; ++t) {
-      const int e = threadIdx.x + 256 * t;
-      Bs[BK ? e % GK : e / TN][BK ? e / GK : e % TN] = rb[t];
+      for (int q = 0; q < NB / 4; ++q) {
+        const int e = threadIdx.x + 256 * q;
+        if constexpr (BK) {
+          const int nn = e / (GK / 4), kq = 4 * (e % (GK / 4));
+#pragma unroll
+          for (int c = 0; c < 4; ++c) Bs[kq + c][nn] = rb[4 * q + c];
+        } else {
+          *reinterpret_cast<float4*>(&Bs[e / (TN / 4)][4 * (e % (TN / 4))]) =
+              make_float4(rb[4 * q], rb[4 * q + 1], rb[4 * q + 2], rb[4 * q + 3]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < NB; ++t) {
+        const int e = threadIdx.x + 256 * t;
+        Bs[BK ? e % GK : e / TN][BK ? e / GK : e % TN] = rb[t];
+      }
     }
   };
   f32x16 acc = {};
@@ -493,24 +563,40 @@ inline unsigned blocks(long long n) { return (unsigned)((n + 255) / 256); }
 
 }  // namespace
 
-template <int WM, int WN, bool AK, bool BK>
+template <int WM, int WN, bool AK, bool BK, bool VA, bool VB>
 void gemm_launch(const TGemm& g, long long total, hipStream_t s) {
   constexpr int TM = 32 * WM, TN = 32 * WN;
   const dim3 grid((unsigned)((g.N + TN - 1) / TN), (unsigned)((g.M + TM - 1) / TM), 1);
   for (long long z0 = 0; z0 < total; z0 += 65535) {
     dim3 gz = grid;
     gz.z = (unsigned)std::min<long long>(65535, total - z0);
-    hipLaunchKernelGGL((k_gemm<WM, WN, AK, BK>), gz, dim3(256), 0, s, g, (int)z0, g.nbatch);
+    hipLaunchKernelGGL((k_gemm<WM, WN, AK, BK, VA, VB>), gz, dim3(256), 0, s, g, (int)z0, g.nbatch);
   }
+}
+
+// float4 loads of an operand are possible when its base and every stride but the contiguous one
+// are multiples of four floats (so every group of four along the contiguous index is aligned)
+inline bool vec4(const float* p, long long other_stride, long long b1, long long b2) {
+  return reinterpret_cast<uintptr_t>(p) % 16 == 0 && other_stride % 4 == 0 && b1 % 4 == 0 && b2 % 4 == 0;
+}
+
+template <int WM, int WN, bool AK, bool BK>
+void gemm_vec(const TGemm& g, long long total, hipStream_t s) {
+  const bool va = vec4(g.A, AK ? g.a_rs : g.a_cs, g.a_b1, g.a_b2) && (AK ? g.a_cs == 1 : g.a_rs == 1);
+  const bool vb = vec4(g.B, BK ? g.b_cs : g.b_rs, g.b_b1, g.b_b2) && (BK ? g.b_rs == 1 : g.b_cs == 1);
+  if (va && vb) gemm_launch<WM, WN, AK, BK, true, true>(g, total, s);
+  else if (va) gemm_launch<WM, WN, AK, BK, true, false>(g, total, s);
+  else if (vb) gemm_launch<WM, WN, AK, BK, false, true>(g, total, s);
+  else gemm_launch<WM, WN, AK, BK, false, false>(g, total, s);
 }
 
 template <int WM, int WN>
 void gemm_orient(const TGemm& g, long long total, hipStream_t s) {
   const bool ak = g.a_cs == 1 && g.a_rs != 1, bk = g.b_rs == 1 && g.b_cs != 1;
-  if (ak && bk) gemm_launch<WM, WN, true, true>(g, total, s);
-  else if (ak) gemm_launch<WM, WN, true, false>(g, total, s);
-  else if (bk) gemm_launch<WM, WN, false, true>(g, total, s);
-  else gemm_launch<WM, WN, false, false>(g, total, s);
+  if (ak && bk) gemm_vec<WM, WN, true, true>(g, total, s);
+  else if (ak) gemm_vec<WM, WN, true, false>(g, total, s);
+  else if (bk) gemm_vec<WM, WN, false, true>(g, total, s);
+  else gemm_vec<WM, WN, false, false>(g, total, s);
 }
 
 hipError_t t_gemm(const TGemm& g, hipStream_t s) {
