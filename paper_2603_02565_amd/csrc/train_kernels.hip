@@ -6,6 +6,7 @@
 #include "train_kernels.h"
 
 #include <algorithm>
+#include <initializer_list>
 
 namespace {
 
@@ -252,24 +253,63 @@ __global__ __launch_bounds__(256) void k_gemm_small(TGemm g, int z0) {
 // ------------------------------------------------------------------------------------------
 // LayerNorm over rows of d values (biased variance, eps 1e-5): one wave per row.
 // ------------------------------------------------------------------------------------------
+template <int V>
+FE_DEV void ldv(const float* p, float* v) {
+  if constexpr (V == 4) {
+    const float4 t = *reinterpret_cast<const float4*>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else if constexpr (V == 2) {
+    const float2 t = *reinterpret_cast<const float2*>(p);
+    v[0] = t.x; v[1] = t.y;
+  } else {
+    v[0] = *p;
+  }
+}
+template <int V>
+FE_DEV void stv(float* p, const float* v) {
+  if constexpr (V == 4) *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  else if constexpr (V == 2) *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  else *p = v[0];
+}
+
+// V consecutive values per lane and load (d a multiple of 64 V, rows and vectors aligned to V floats)
+template <int V>
 __global__ __launch_bounds__(256) void k_ln_fwd(const float* X, long long x_rs, int rows, int d, const float* g,
                                                 const float* b, float* Y, long long y_rs, float* mean, float* rstd) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= rows) return;
   const float* x = X + row * x_rs;
+  float v[V];
   float s = 0.f;
-  for (int j = lane; j < d; j += 64) s += x[j];
+  for (int j = lane * V; j < d; j += 64 * V) {
+    ldv<V>(x + j, v);
+#pragma unroll
+    for (int c = 0; c < V; ++c) s += v[c];
+  }
   const float mu = wave_sum(s) / d;
   float q = 0.f;
-  for (int j = lane; j < d; j += 64) { const float t = x[j] - mu; q += t * t; }
+  for (int j = lane * V; j < d; j += 64 * V) {
+    ldv<V>(x + j, v);
+#pragma unroll
+    for (int c = 0; c < V; ++c) q += (v[c] - mu) * (v[c] - mu);
+  }
   const float rs = rsqrtf(wave_sum(q) / d + 1e-5f);
   float* y = Y + row * y_rs;
-  for (int j = lane; j < d; j += 64) y[j] = (x[j] - mu) * rs * g[j] + b[j];
+  for (int j = lane * V; j < d; j += 64 * V) {
+    float gv[V], bv[V];
+    ldv<V>(x + j, v);
+    ldv<V>(g + j, gv);
+    ldv<V>(b + j, bv);
+#pragma unroll
+    for (int c = 0; c < V; ++c) v[c] = (v[c] - mu) * rs * gv[c] + bv[c];
+    stv<V>(y + j, v);
+  }
   if (lane == 0) { mean[row] = mu; rstd[row] = rs; }
 }
 
 // dX += rstd (dxh - mean(dxh) - xh mean(dxh xh)) with dxh = dY g and xh the normalised input:
-// one wave per row.
+// one wave per row, V values per lane and load.
+template <int V>
 __global__ __launch_bounds__(256) void k_ln_bwd_rows(const float* X, long long x_rs, int rows, int d, const float* g,
                                                      const float* mean, const float* rstd, const float* dY,
                                                      long long dy_rs, float* dX, long long dx_rs) {
@@ -278,18 +318,31 @@ __global__ __launch_bounds__(256) void k_ln_bwd_rows(const float* X, long long x
   const float* x = X + row * x_rs;
   const float* dy = dY + row * dy_rs;
   const float mu = mean[row], rs = rstd[row];
+  float xv[V], dv[V], gv[V];
   float s1 = 0.f, s2 = 0.f;
-  for (int j = lane; j < d; j += 64) {
-    const float xh = (x[j] - mu) * rs, dxh = dy[j] * g[j];
-    s1 += dxh;
-    s2 += dxh * xh;
+  for (int j = lane * V; j < d; j += 64 * V) {
+    ldv<V>(x + j, xv);
+    ldv<V>(dy + j, dv);
+    ldv<V>(g + j, gv);
+#pragma unroll
+    for (int c = 0; c < V; ++c) {
+      const float xh = (xv[c] - mu) * rs, dxh = dv[c] * gv[c];
+      s1 += dxh;
+      s2 += dxh * xh;
+    }
   }
   s1 = wave_sum(s1) / d;
   s2 = wave_sum(s2) / d;
   float* dx = dX + row * dx_rs;
-  for (int j = lane; j < d; j += 64) {
-    const float xh = (x[j] - mu) * rs;
-    dx[j] += rs * (dy[j] * g[j] - s1 - xh * s2);
+  for (int j = lane * V; j < d; j += 64 * V) {
+    float ov[V];
+    ldv<V>(x + j, xv);
+    ldv<V>(dy + j, dv);
+    ldv<V>(g + j, gv);
+    ldv<V>(dx + j, ov);
+#pragma unroll
+    for (int c = 0; c < V; ++c) ov[c] += rs * (dv[c] * gv[c] - s1 - (xv[c] - mu) * rs * s2);
+    stv<V>(dx + j, ov);
   }
 }
 
@@ -622,11 +675,26 @@ hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// widest V in {4, 2, 1} with d a multiple of 64 V and every pointer and row stride aligned to V floats
+inline int ln_width(int d, std::initializer_list<const void*> ptrs, std::initializer_list<long long> strides) {
+  for (int V : {4, 2}) {
+    bool ok = d % (64 * V) == 0;
+    for (const void* p : ptrs) ok = ok && reinterpret_cast<uintptr_t>(p) % (4 * V) == 0;
+    for (long long st : strides) ok = ok && st % V == 0;
+    if (ok) return V;
+  }
+  return 1;
+}
+
 hipError_t t_ln_fwd(const float* X, long long x_rs, int rows, int d, const float* g, const float* b, float* Y,
                     long long y_rs, float* mean, float* rstd, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_ln_fwd, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, X, x_rs, rows, d, g, b, Y, y_rs, mean,
-                     rstd);
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  switch (ln_width(d, {X, g, b, Y}, {x_rs, y_rs})) {
+    case 4: hipLaunchKernelGGL(k_ln_fwd<4>, grid, dim3(256), 0, s, X, x_rs, rows, d, g, b, Y, y_rs, mean, rstd); break;
+    case 2: hipLaunchKernelGGL(k_ln_fwd<2>, grid, dim3(256), 0, s, X, x_rs, rows, d, g, b, Y, y_rs, mean, rstd); break;
+    default: hipLaunchKernelGGL(k_ln_fwd<1>, grid, dim3(256), 0, s, X, x_rs, rows, d, g, b, Y, y_rs, mean, rstd);
+  }
   return hipGetLastError();
 }
 
@@ -634,8 +702,12 @@ hipError_t t_ln_bwd(const float* X, long long x_rs, int rows, int d, const float
                     const float* rstd, const float* dY, long long dy_rs, float* dX, long long dx_rs, float* dg,
                     float* db, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_ln_bwd_rows, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, X, x_rs, rows, d, g, mean, rstd, dY,
-                     dy_rs, dX, dx_rs);
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  switch (ln_width(d, {X, g, dY, dX}, {x_rs, dy_rs, dx_rs})) {
+    case 4: hipLaunchKernelGGL(k_ln_bwd_rows<4>, grid, dim3(256), 0, s, X, x_rs, rows, d, g, mean, rstd, dY, dy_rs, dX, dx_rs); break;
+    case 2: hipLaunchKernelGGL(k_ln_bwd_rows<2>, grid, dim3(256), 0, s, X, x_rs, rows, d, g, mean, rstd, dY, dy_rs, dX, dx_rs); break;
+    default: hipLaunchKernelGGL(k_ln_bwd_rows<1>, grid, dim3(256), 0, s, X, x_rs, rows, d, g, mean, rstd, dY, dy_rs, dX, dx_rs);
+  }
   hipLaunchKernelGGL(k_ln_bwd_params, dim3((unsigned)((d + 63) / 64), (unsigned)((rows + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
                      dim3(256), 0, s, X, x_rs, rows, d, mean, rstd, dY, dy_rs, dg, db);
   return hipGetLastError();
