@@ -17,6 +17,9 @@
 #include "flasheval_train.h"
 #include "train_kernels.h"
 
+static_assert(FE_LOSS_MSE == TRAIN_MSE && FE_LOSS_BCE == TRAIN_BCE && FE_LOSS_CE == TRAIN_CE,
+              "the loss kernel takes fe_loss values");
+
 namespace {
 
 fe_status tfail(fe_status st, const char* fmt, ...) {

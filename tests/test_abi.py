@@ -140,3 +140,30 @@ def test_train_binding_rejects_wrong_dtype_before_any_call():
     with pytest.raises(ValueError, match="grads"):
         fe.fe_train_grads(cfg, P, 1, c.T, c.M, c.K, c.L, None, None, None, None, None, fe.FE_LOSS_CE,
                           torch.zeros(1), None, torch.zeros(n - 1), torch.zeros(8, dtype=torch.uint8))
+
+
+def _train_call(cfg, c, *, loss_kind=fe.FE_LOSS_CE, ws=1 << 20, ws_bytes=None, pool=8192, x=8192):
+    """fe_train_grads with placeholder device addresses: every case below is refused by the host-side
+    checks before anything touches them."""
+    n = fe.fe_param_count(cfg)
+    need = fe.fe_train_workspace_size(cfg, 1, c.T, c.M, c.K, c.L)
+    lib = fe.load_library()
+    return lib.fe_train_grads(ctypes.byref(cfg), 4096, 1, c.T, c.M, c.K, c.L, x, None, pool, 12288, 16384, loss_kind,
+                              20480, None, 24576, ws, need if ws_bytes is None else ws_bytes, None), need
+
+
+@pytest.mark.parametrize("case", ["loss_kind", "misaligned", "small", "no_pool"])
+def test_train_grads_host_checks(case):
+    c = gen.config(0)
+    cfg = _train_cfg(c)
+    if case == "loss_kind":
+        st, _ = _train_call(cfg, c, loss_kind=3)
+    elif case == "misaligned":
+        st, _ = _train_call(cfg, c, ws=(1 << 20) + 64)
+    elif case == "small":
+        st, need = _train_call(cfg, c, ws_bytes=1024)
+    else:
+        st, _ = _train_call(cfg, c, pool=None)
+    assert st == fe.FE_EINVAL
+    msg = fe.load_library().fe_last_error().decode()
+    assert {"loss_kind": "loss_kind", "misaligned": "aligned", "small": "workspace", "no_pool": "pool"}[case] in msg
