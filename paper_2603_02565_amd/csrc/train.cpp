@@ -588,6 +588,9 @@ fe_status check(const fe_config* cfg, int B, int T, int M, int K, int L, Dims* D
   if (K > 1024) return tfail(FE_EUNSUPPORTED, "K=%d > 1024", K);
   if (M > 131072) return tfail(FE_EUNSUPPORTED, "M=%d > 131072", M);
   if (cfg->vocab > 0 && M != cfg->vocab) return tfail(FE_EINVAL, "token-id items need M = vocab (%d), got %d", cfg->vocab, M);
+  const long long U = std::min<long long>(M, (long long)K * L), rows_max = 0x7fffffffLL / 4;
+  if ((long long)B * K * (L + 1) > rows_max || (long long)B * T > rows_max || (long long)B * U > rows_max)
+    return tfail(FE_EUNSUPPORTED, "B=%d gives more than %lld rows in a module", B, rows_max);
   D->B = B; D->T = T; D->M = M; D->K = K; D->L = L;
   D->d = cfg->d; D->H = cfg->n_heads; D->dh = cfg->d / cfg->n_heads; D->F = cfg->ffn_dim; D->n = cfg->n_layers;
   D->U = (int)std::min<long long>(M, (long long)K * L);

@@ -117,6 +117,7 @@ def test_train_workspace_grows_with_the_batch():
     ({}, (2, 64, 200, 50, 11), fe.FE_EINVAL),                                      # L > max_L
     ({}, (0, 64, 200, 50, 10), fe.FE_EINVAL),
     (dict(vocab=40), (2, 64, 200, 50, 10), fe.FE_EINVAL),                          # token ids need M = vocab
+    ({}, (2_000_000, 64, 200, 50, 10), fe.FE_EUNSUPPORTED),                       # rows past 32-bit row indexing
 ])
 def test_train_validation(kw, dims, status):
     c = gen.config(1)
