@@ -152,3 +152,35 @@ def test_many_lists():
     c = gen.config(1, B=1, T=16, K=300, L=3, M=150, n_layers=1, dtype="f32")
     W, I = gen.make_weights(c), gen.make_inputs(c)
     check(c, W, I, _relevance(c), "bce")
+
+
+def test_workspace_reuse():
+    """Two steps in a row on one workspace, the second with fewer requests in the same (larger)
+    buffer: every accumulator is cleared inside the step, so each call matches the reference."""
+    dev = torch.device("cuda:0")
+    c2 = gen.config(1, B=2, T=16, K=5, L=4, M=20, n_layers=1, dtype="f32")
+    c1 = gen.config(1, B=1, T=16, K=5, L=4, M=20, n_layers=1, dtype="f32")
+    W = gen.make_weights(c2)
+    cfg = fe_cfg(c2)
+    ws = torch.full((fe.fe_train_workspace_size(cfg, 2, 16, 20, 5, 4),), 255, dtype=torch.uint8, device=dev)
+    P = torch.from_numpy(fe.pack_params(W, c2.n_layers, c2.vocab)).to(dev)
+    G = torch.empty_like(P)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    Wd = {k: np.asarray(v, np.float64) for k, v in W.items()}
+    for c in (c2, c1):
+        I = gen.make_inputs(c2)
+        I = {k: (None if v is None else np.ascontiguousarray(v[:c.B])) for k, v in I.items()}
+        a = _relevance(c2)[:c.B]
+        t = lambda v, dt: torch.from_numpy(np.ascontiguousarray(v, dt)).to(dev)
+        fe.fe_train_grads(cfg, P, c.B, c.T, c.M, c.K, c.L, t(I["x"], np.float32), None, t(I["pool"], np.float32),
+                          t(I["lists"], np.int32), t(a, np.int32), fe.FE_LOSS_CE, loss, None, G, ws)
+        torch.cuda.synchronize()
+        rloss, rg, _ = train.train_grads(c, Wd, I, a, "ce")
+        assert abs(float(loss.item()) - rloss) <= 1e-4 * max(1.0, abs(rloss)), (c.B, float(loss.item()), rloss)
+        flat, o = G.cpu().numpy(), 0
+        top = max(float(np.max(np.abs(v))) for v in rg.values())
+        for n in fe.param_names(c.n_layers, c.vocab):
+            k = int(np.prod(W[n].shape))
+            err = float(np.max(np.abs(flat[o:o + k].reshape(W[n].shape) - rg[n])))
+            assert err <= GRAD_RTOL * max(float(np.max(np.abs(rg[n]))), GRAD_FLOOR * top), (c.B, n, err)
+            o += k
