@@ -188,11 +188,11 @@ __global__ __launch_bounds__(256) void k_gemm(TGemm g, int z0, int nz) {
 
 // Batched products with M, N <= 32 (attention inside short sequences): each wave owns one batch
 // item's 32 x 32 tile, four items per workgroup, same k-steps and prefetch as k_gemm.
-template <bool AK, bool BK>
+template <bool AK, bool BK, bool VA, bool VB>
 __global__ __launch_bounds__(256) void k_gemm_small(TGemm g, int z0) {
   constexpr int P = 36, N1 = GK * 32 / 64;   // elements per lane per operand per k-step
-  __shared__ float As[4][GK][P];
-  __shared__ float Bs[4][GK][P];
+  __shared__ __align__(16) float As[4][GK][P];
+  __shared__ __align__(16) float Bs[4][GK][P];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int z = z0 + blockIdx.x * 4 + wave;
   const bool live = z < g.nbatch;
@@ -204,26 +204,98 @@ __global__ __launch_bounds__(256) void k_gemm_small(TGemm g, int z0) {
   const float* Mz = g.mask + z1 * g.c_b1 + z2 * g.c_b2;
   const int lr = lane & 31, lk = lane >> 5;
   float ra[N1], rb[N1];
+  // VA / VB: four consecutive elements of the contiguous index per load (aligned, checked by the
+  // launcher); the registers hold the same N1 scalars either way
   auto load = [&](int k0) {
+    if constexpr (VA) {
 #pragma unroll
-    for (int t = 0; t < N1; ++t) {
-      const int e = lane + 64 * t;
-      const int kk = AK ? e % GK : e / 32, mm = AK ? e / GK : e % 32;
-      const int k = k0 + kk;
-      ra[t] = (live && mm < g.M && k < g.K) ? A[mm * g.a_rs + k * g.a_cs] : 0.f;
-      const int kb = BK ? e % GK : e / 32, nn = BK ? e / GK : e % 32;
-      const int kq = k0 + kb;
-      rb[t] = (live && nn < g.N && kq < g.K) ? B[kq * g.b_rs + nn * g.b_cs] : 0.f;
+      for (int q = 0; q < N1 / 4; ++q) {
+        const int e = lane + 64 * q;
+        const int i = AK ? e / (GK / 4) : 4 * (e % 8), k = AK ? k0 + 4 * (e % (GK / 4)) : k0 + e / 8;
+        const float* src = A + i * g.a_rs + k * g.a_cs;
+        if (live && (AK ? (i < g.M && k + 3 < g.K) : (i + 3 < g.M && k < g.K))) {
+          const float4 v = *reinterpret_cast<const float4*>(src);
+          ra[4 * q] = v.x; ra[4 * q + 1] = v.y; ra[4 * q + 2] = v.z; ra[4 * q + 3] = v.w;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            ra[4 * q + c] = (live && (AK ? (i < g.M && k + c < g.K) : (i + c < g.M && k < g.K))) ? src[AK ? c : c * g.a_rs] : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < N1; ++t) {
+        const int e = lane + 64 * t;
+        const int kk = AK ? e % GK : e / 32, mm = AK ? e / GK : e % 32;
+        const int k = k0 + kk;
+        ra[t] = (live && mm < g.M && k < g.K) ? A[mm * g.a_rs + k * g.a_cs] : 0.f;
+      }
+    }
+    if constexpr (VB) {
+#pragma unroll
+      for (int q = 0; q < N1 / 4; ++q) {
+        const int e = lane + 64 * q;
+        const int j = BK ? e / (GK / 4) : 4 * (e % 8), k = BK ? k0 + 4 * (e % (GK / 4)) : k0 + e / 8;
+        const float* src = B + k * g.b_rs + j * g.b_cs;
+        if (live && (BK ? (j < g.N && k + 3 < g.K) : (j + 3 < g.N && k < g.K))) {
+          const float4 v = *reinterpret_cast<const float4*>(src);
+          rb[4 * q] = v.x; rb[4 * q + 1] = v.y; rb[4 * q + 2] = v.z; rb[4 * q + 3] = v.w;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            rb[4 * q + c] = (live && (BK ? (j < g.N && k + c < g.K) : (j + c < g.N && k < g.K))) ? src[BK ? c : c * g.b_cs] : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < N1; ++t) {
+        const int e = lane + 64 * t;
+        const int kb = BK ? e % GK : e / 32, nn = BK ? e / GK : e % 32;
+        const int kq = k0 + kb;
+        rb[t] = (live && nn < g.N && kq < g.K) ? B[kq * g.b_rs + nn * g.b_cs] : 0.f;
+      }
     }
   };
   f32x16 acc = {};
   load(0);
   for (int k0 = 0; k0 < g.K; k0 += GK) {
+    if constexpr (VA) {
 #pragma unroll
-    for (int t = 0; t < N1; ++t) {
-      const int e = lane + 64 * t;
-      As[wave][AK ? e % GK : e / 32][AK ? e / GK : e % 32] = ra[t];
-      Bs[wave][BK ? e % GK : e / 32][BK ? e / GK : e % 32] = rb[t];
+      for (int q = 0; q < N1 / 4; ++q) {
+        const int e = lane + 64 * q;
+        if constexpr (AK) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) As[wave][4 * (e % (GK / 4)) + c][e / (GK / 4)] = ra[4 * q + c];
+        } else {
+          *reinterpret_cast<float4*>(&As[wave][e / 8][4 * (e % 8)]) =
+              make_float4(ra[4 * q], ra[4 * q + 1], ra[4 * q + 2], ra[4 * q + 3]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < N1; ++t) {
+        const int e = lane + 64 * t;
+        As[wave][AK ? e % GK : e / 32][AK ? e / GK : e % 32] = ra[t];
+      }
+    }
+    if constexpr (VB) {
+#pragma unroll
+      for (int q = 0; q < N1 / 4; ++q) {
+        const int e = lane + 64 * q;
+        if constexpr (BK) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) Bs[wave][4 * (e % (GK / 4)) + c][e / (GK / 4)] = rb[4 * q + c];
+        } else {
+          *reinterpret_cast<float4*>(&Bs[wave][e / 8][4 * (e % 8)]) =
+              make_float4(rb[4 * q], rb[4 * q + 1], rb[4 * q + 2], rb[4 * q + 3]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < N1; ++t) {
+        const int e = lane + 64 * t;
+        Bs[wave][BK ? e % GK : e / 32][BK ? e / GK : e % 32] = rb[t];
+      }
     }
     __syncthreads();
     if (k0 + GK < g.K) load(k0 + GK);
@@ -652,6 +724,21 @@ void gemm_orient(const TGemm& g, long long total, hipStream_t s) {
   else gemm_vec<WM, WN, false, false>(g, total, s);
 }
 
+template <bool AK, bool BK>
+void small_launch_vec(bool va, bool vb, const TGemm& g, unsigned nblk, int z0, hipStream_t s) {
+  if (va && vb) hipLaunchKernelGGL((k_gemm_small<AK, BK, true, true>), dim3(nblk), dim3(256), 0, s, g, z0);
+  else if (va) hipLaunchKernelGGL((k_gemm_small<AK, BK, true, false>), dim3(nblk), dim3(256), 0, s, g, z0);
+  else if (vb) hipLaunchKernelGGL((k_gemm_small<AK, BK, false, true>), dim3(nblk), dim3(256), 0, s, g, z0);
+  else hipLaunchKernelGGL((k_gemm_small<AK, BK, false, false>), dim3(nblk), dim3(256), 0, s, g, z0);
+}
+
+void small_launch(bool ak, bool bk, bool va, bool vb, const TGemm& g, unsigned nblk, int z0, hipStream_t s) {
+  if (ak && bk) small_launch_vec<true, true>(va, vb, g, nblk, z0, s);
+  else if (ak) small_launch_vec<true, false>(va, vb, g, nblk, z0, s);
+  else if (bk) small_launch_vec<false, true>(va, vb, g, nblk, z0, s);
+  else small_launch_vec<false, false>(va, vb, g, nblk, z0, s);
+}
+
 hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.nbatch <= 0) return hipSuccess;
   if (g.ksplit > 0 && (g.beta != 1.f || g.bias || g.R || g.relu || g.mask || g.ksplit % GK)) return hipErrorInvalidValue;
@@ -660,12 +747,11 @@ hipError_t t_gemm(const TGemm& g, hipStream_t s) {
   const long long total = (long long)g.nbatch * nk;
   if (g.M <= 32 && g.N <= 32 && g.ksplit == 0 && !g.colsum) {
     const bool ak = g.a_cs == 1 && g.a_rs != 1, bk = g.b_rs == 1 && g.b_cs != 1;
+    const bool va = vec4(g.A, ak ? g.a_rs : g.a_cs, g.a_b1, g.a_b2) && (ak ? g.a_cs == 1 : g.a_rs == 1);
+    const bool vb = vec4(g.B, bk ? g.b_cs : g.b_rs, g.b_b1, g.b_b2) && (bk ? g.b_rs == 1 : g.b_cs == 1);
     for (long long z0 = 0; z0 < total; z0 += 4LL * 65535) {
       const unsigned nblk = (unsigned)std::min<long long>(65535, (total - z0 + 3) / 4);
-      if (ak && bk) hipLaunchKernelGGL((k_gemm_small<true, true>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
-      else if (ak) hipLaunchKernelGGL((k_gemm_small<true, false>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
-      else if (bk) hipLaunchKernelGGL((k_gemm_small<false, true>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
-      else hipLaunchKernelGGL((k_gemm_small<false, false>), dim3(nblk), dim3(256), 0, s, g, (int)z0);
+      small_launch(ak, bk, va, vb, g, nblk, (int)z0, s);
     }
   } else if (g.N <= 32) {
     gemm_orient<4, 1>(g, total, s);                 // 128 x 32 tiles (one head's width)
