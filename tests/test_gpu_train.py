@@ -184,3 +184,17 @@ def test_workspace_reuse():
             err = float(np.max(np.abs(flat[o:o + k].reshape(W[n].shape) - rg[n])))
             assert err <= GRAD_RTOL * max(float(np.max(np.abs(rg[n]))), GRAD_FLOOR * top), (c.B, n, err)
             o += k
+
+
+def test_large_vocabulary():
+    """Token ids over a 5000-entry table: the embedding gradient scatters into a large table and the
+    feedback rows are 5000 wide."""
+    c = gen.config(4, B=2, K=4, L=6, T=12, vocab=5000, M=5000, n_layers=1, d=64, n_heads=2, ffn=256, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "bce")
+
+
+def test_three_layers():
+    c = gen.config(1, B=2, T=14, K=5, L=4, M=22, n_layers=3, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    check(c, W, I, _relevance(c), "mse")
