@@ -57,8 +57,10 @@ fe_status fe_train_workspace_size(const fe_config* cfg, int B, int T, int M, int
  *   ctx_ids   int32 [B][T] context token ids (vocab > 0), else NULL; ids outside [0, vocab) embed
  *             as zero rows
  *   pool      fp32 [B][M][d] element embeddings (vocab == 0), else NULL (items are rows of emb)
- *   lists     int32 [B][K][L] element indices in [0, M); an entry outside that range contributes
- *             a zero row (as in fe_assemble) and no feedback
+ *   lists     int32 [B][K][L] element indices in [0, M); an entry outside that range is left out
+ *             of the distinct set and contributes a zero row without a position (as in
+ *             fe_assemble), no feedback and no gradient; such entries are not reported (the
+ *             inference calls report them in their status word)
  *   relevant  int32 [B][M] binary item-level feedback (0 or 1)
  *   loss_kind fe_loss
  *   loss      fp32 [1], overwritten with the batch loss

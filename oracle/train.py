@@ -29,14 +29,16 @@ LOSSES = ("mse", "bce", "ce")
 
 
 def sequence_labels(lists: np.ndarray, relevant: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """r[b][k] = sum_j relevant[b][lists[b][k][j]] and y[b] = min argmax_k r[b][k] (App. B.1)."""
+    """r[b][k] = sum_j relevant[b][lists[b][k][j]] and y[b] = min argmax_k r[b][k] (App. B.1).
+    An entry outside the pool [0, M) has no feedback (it adds 0)."""
     lists = np.asarray(lists)
     B, K, L = lists.shape
+    M = np.asarray(relevant).shape[1]
     r = np.zeros((B, K), dtype=np.int64)
     y = np.zeros(B, dtype=np.int64)
     for b in range(B):
         for k in range(K):
-            r[b, k] = sum(int(relevant[b][int(e)]) for e in lists[b, k])
+            r[b, k] = sum(int(relevant[b][int(e)]) for e in lists[b, k] if 0 <= int(e) < M)
         best = 0
         for k in range(1, K):
             if r[b, k] > r[b, best]:
@@ -81,7 +83,10 @@ def _stack(x, P, module, n, H):
 
 
 def request_scores(cfg, P: Dict[str, torch.Tensor], inp: Dict, b: int) -> torch.Tensor:
-    """s_1..s_K of request b: the joint pass (Sections 4.1-4.4) in the cached order."""
+    """s_1..s_K of request b: the joint pass (Sections 4.1-4.4) in the cached order.
+
+    A list entry outside the pool [0, M) is left out of the distinct set and its sequence row is
+    a zero row without a position (the reading the GPU step takes for such entries)."""
     if getattr(cfg, "attention", "softmax") != "softmax":
         raise NotImplementedError("the training reference covers softmax attention")
     n, H = cfg.n_layers, cfg.n_heads
@@ -90,7 +95,10 @@ def request_scores(cfg, P: Dict[str, torch.Tensor], inp: Dict, b: int) -> torch.
     Q = _stack(X, P, "ctx", n, H)
     lists_b = np.asarray(inp["lists"][b])
     K, L = lists_b.shape
-    uniq, slot = distinct_items(lists_b)
+    valid = (lists_b >= 0) & (lists_b < cfg.M)
+    uniq, _ = distinct_items(lists_b[valid])
+    rank = {int(v): i for i, v in enumerate(uniq)}
+    slot = np.array([[rank[int(e)] if ok else -1 for e, ok in zip(lists_b[k], valid[k])] for k in range(K)])
     idx = torch.as_tensor(uniq, dtype=torch.long)
     G = P["emb"][idx] if cfg.vocab else torch.as_tensor(np.asarray(inp["pool"][b], np.float64))[idx]
     for l in range(n):
@@ -105,8 +113,10 @@ def request_scores(cfg, P: Dict[str, torch.Tensor], inp: Dict, b: int) -> torch.
     pos = P["pos"]
     c = []
     for k in range(K):
-        rows = Hm[torch.as_tensor(slot[k], dtype=torch.long)]
-        seq = torch.cat([(P["cls"] + pos[0])[None, :], rows + pos[1:L + 1]], dim=0)
+        ok = torch.as_tensor(slot[k] >= 0)[:, None]
+        rows = Hm[torch.as_tensor(np.maximum(slot[k], 0), dtype=torch.long)] + pos[1:L + 1]
+        rows = torch.where(ok, rows, torch.zeros_like(rows))
+        seq = torch.cat([(P["cls"] + pos[0])[None, :], rows], dim=0)
         c.append(_stack(seq, P, "seq", n, H)[0])
     Cp = _stack(torch.stack(c), P, "cross", n, H)
     return Cp @ P["head.w"] + P["head.b"][0]

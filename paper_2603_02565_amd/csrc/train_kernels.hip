@@ -573,7 +573,8 @@ __global__ void k_assemble_f32(const float* H, int U_cap, const int32_t* slot, i
   float* o = seq + (((long long)b * K + k) * (L + 1) + j) * d;
   const int sl = j == 0 ? 0 : slot[((long long)b * K + k) * L + j - 1];
   const float* src = j == 0 ? cls : H + ((long long)b * U_cap + sl) * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) o[e] = (sl >= 0 ? src[e] : 0.f) + pos[(long long)j * d + e];
+  // an entry outside the pool (slot -1) gives a zero row, as in the inference assembly
+  for (int e = threadIdx.x; e < d; e += blockDim.x) o[e] = sl >= 0 ? src[e] + pos[(long long)j * d + e] : 0.f;
 }
 // the assembly's backward, element rows: dH[b][slot] += dseq rows (a distinct element's row receives
 // the sum over its occurrences)
@@ -587,16 +588,19 @@ __global__ void k_assemble_bwd(const float* dseq, int U_cap, const int32_t* slot
 }
 
 // ... and positions and [CLS]: dpos[c] += sum over the B K sequences of dseq[.][c] for the (L+1) d
-// entries c of a sequence, dcls[e] += the same sums of row 0.  64 entries x TRAIN_COL_ROWS sequences
-// per workgroup, one atomic per entry and workgroup.
-__global__ __launch_bounds__(256) void k_assemble_bwd_pos(const float* dseq, int nseq, int cols, int d, float* dpos,
-                                                          float* dcls) {
+// entries c of a sequence, dcls[e] += the same sums of row 0; the zero rows of entries outside the
+// pool (slot -1) carry no position and add nothing.  64 entries x TRAIN_COL_ROWS sequences per
+// workgroup, one atomic per entry and workgroup.
+__global__ __launch_bounds__(256) void k_assemble_bwd_pos(const float* dseq, const int32_t* slot, int L, int nseq,
+                                                          int cols, int d, float* dpos, float* dcls) {
   __shared__ float part[4][64];
   const int c = blockIdx.x * 64 + (threadIdx.x & 63), w = threadIdx.x >> 6;
   const int r0 = blockIdx.y * TRAIN_COL_ROWS, r1 = min(nseq, r0 + TRAIN_COL_ROWS);
+  const int j = c / d;                                   // row of the sequence: 0 [CLS], 1..L entries
   float sum = 0.f;
   if (c < cols)
-    for (int r = r0 + w; r < r1; r += 4) sum += dseq[(long long)r * cols + c];
+    for (int r = r0 + w; r < r1; r += 4)
+      if (j == 0 || slot[(long long)r * L + j - 1] >= 0) sum += dseq[(long long)r * cols + c];
   part[w][threadIdx.x & 63] = sum;
   __syncthreads();
   if (w == 0 && c < cols) {
@@ -862,7 +866,7 @@ hipError_t t_assemble_bwd(const float* dseq, int B, int U_cap, const int32_t* sl
                        L, d, dH);
   const int nseq = B * K, cols = (L + 1) * d;
   hipLaunchKernelGGL(k_assemble_bwd_pos, dim3((unsigned)((cols + 63) / 64), (unsigned)((nseq + TRAIN_COL_ROWS - 1) / TRAIN_COL_ROWS)),
-                     dim3(256), 0, s, dseq, nseq, cols, d, dpos, dcls);
+                     dim3(256), 0, s, dseq, slot, L, nseq, cols, d, dpos, dcls);
   return hipGetLastError();
 }
 hipError_t t_loss(const float* scores, const int32_t* lists, const int32_t* relevant, int M, int B, int K, int L, int kind,

@@ -9,3 +9,14 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: CPU test that takes more than a few seconds")
+
+
+import pytest  # noqa: E402
+
+
+@pytest.fixture(scope="session", autouse=True)
+def _oracle_pool_shutdown():
+    """Stop the oracle's CPU worker processes (started on first use) at the end of the session."""
+    yield
+    from tests import oracle_pool
+    oracle_pool.close()

@@ -7,7 +7,7 @@ import torch
 
 import gen
 import oracle
-from tests.gpu_harness import check_selection, make_evaluator, normwise, rtol_for, run_pass, score_scale, upload
+from tests.gpu_harness import check_scores, make_evaluator, normwise, rtol_for, run_pass, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -31,9 +31,7 @@ def _run_naive(c, W, I, ev=None):
 def _check_against(c, W, got, ref_scores, ref_Cp, b):
     tol = rtol_for(c)
     assert normwise(got["Cp"][b], ref_Cp) <= tol, "Cp"
-    stol = tol * score_scale(W, ref_Cp)
-    assert np.max(np.abs(got["scores"][b] - ref_scores)) <= stol, "scores"
-    check_selection(int(got["best"][b]), ref_scores, stol)
+    check_scores(c, got["scores"][b], got["best"][b], ref_scores, b)
 
 
 def test_naive_cfg0_fp32_matches_oracle_naive():

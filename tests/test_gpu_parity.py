@@ -6,8 +6,8 @@ import torch
 import gen
 import oracle
 from paper_2603_02565_amd import flasheval as fe
-from tests.gpu_harness import (check_selection, fetch, make_evaluator, normwise, rtol_for, run_pass, score_scale,
-                               upload)
+from tests.gpu_harness import check_scores, fetch, make_evaluator, normwise, rtol_for, run_pass, score_tol, upload
+from tests.oracle_pool import compare_batch
 
 pytestmark = pytest.mark.gpu
 
@@ -31,9 +31,44 @@ def _compare_request(cfg, W, out, ref, b, check_kv=True):
     assert np.all(out["H"][b, U:] == 0)
     assert normwise(out["seq"][b], ref["seq"]) <= tol, "seq"
     assert normwise(out["Cp"][b], ref["Cp"]) <= tol, "Cp"
-    stol = tol * score_scale(W, ref["Cp"])
-    assert np.max(np.abs(out["scores"][b] - ref["scores"])) <= stol, "scores"
-    check_selection(int(out["best"][b]), ref["scores"], stol)
+    if len(ref["scores"]) == 1:
+        # one list: a single score, whose size says nothing about its error (its d terms may
+        # cancel to almost nothing); it must be the head applied to this C' -- the oracle's score
+        # plus the propagated C' error and the fp32 dot product's own rounding -- and be selected
+        w = np.abs(W["head.w"].astype(np.float64))
+        Cg = out["Cp"][b, 0].astype(np.float64)
+        bound = np.abs(Cg - ref["Cp"][0]) @ w + (cfg.d + 2) * 2.0 ** -24 * (np.abs(Cg) @ w + abs(float(W["head.b"][0])))
+        assert abs(float(out["scores"][b, 0]) - ref["scores"][0]) <= bound, "scores"
+        assert int(out["best"][b]) == 0
+        return {"ratio": 0.0, "strict": True}
+    return check_scores(cfg, out["scores"][b], out["best"][b], ref["scores"], b)
+
+
+def check_whole_batch(c, out):
+    """Every request of a full-size batch against the cached-order oracle (stage by stage,
+    element by element); prints the measured worst error ratios and the fraction of requests in
+    the exact-selection regime."""
+    tol = rtol_for(c)
+    worst = {k: 0.0 for k in ("kv", "H", "seq", "Cp", "scores")}
+    strict = 0
+    for r in compare_batch(c, out):
+        b = r["b"]
+        assert r["n_uniq_ok"] and r["uniq_ok"] and r["slot_ok"], (c.label, b, "distinct set or slots differ")
+        assert r["H_pad_zero"], (c.label, b, "padding rows of H are not zero")
+        for k in ("H", "seq", "Cp"):
+            assert r[k] <= tol, (c.label, b, k, r[k])
+            worst[k] = max(worst[k], r[k])
+        if "kv" in r:
+            assert max(r["kv"]) <= tol, (c.label, b, "kv", r["kv"])
+            worst["kv"] = max(worst["kv"], max(r["kv"]))
+        m = check_scores(c, out["scores"][b], out["best"][b], r["scores_ref"], (c.label, b))
+        worst["scores"] = max(worst["scores"], m["ratio"])
+        strict += m["strict"]
+    assert np.all(out["status"] == 0)
+    print(f"\n[parity] {c.label}: {c.B} requests; worst normwise error " +
+          ", ".join(f"{k} {v:.3g}" for k, v in worst.items()) +
+          f"; exact-selection regime {strict}/{c.B}", flush=True)
+    return worst, strict
 
 
 def test_cfg0_all_stages_fp32():
@@ -41,17 +76,24 @@ def test_cfg0_all_stages_fp32():
     W, I = gen.make_weights(c), gen.make_inputs(c)
     out = run_pass(c, W, I)
     ref = _stage_refs(c, W, I, 0)
-    _compare_request(c, W, out, ref, 0)
+    m = _compare_request(c, W, out, ref, 0)
+    assert m["strict"]
     naive = oracle.evaluate_naive(c, W, I)[0]
-    assert normwise(out["scores"][0], naive["scores"]) <= 1e-4
+    check_scores(c, out["scores"][0], out["best"][0], naive["scores"], "naive")
     assert int(out["best"][0]) == naive["best"]
     assert out["status"][0] == 0
 
 
-@pytest.mark.parametrize("b", [0, 37, 63])
-def test_cfg1_end_to_end(cfg1_out, b):
+@pytest.fixture(scope="module")
+def cfg1_out():
+    c = gen.config(1)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    return c, W, I, run_pass(c, W, I)
+
+
+def test_cfg1_every_request(cfg1_out):
     c, W, I, out = cfg1_out
-    _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+    check_whole_batch(c, out)
 
 
 def test_cfg1_distinct_sets_all_requests(cfg1_out):
@@ -64,20 +106,14 @@ def test_cfg1_distinct_sets_all_requests(cfg1_out):
     assert np.all(out["status"] == 0)
 
 
-def test_cfg1_naive_oracle_request0(cfg1_out):
-    """Request 0 against the candidate-factorised oracle itself (context per list, items per occurrence)."""
+@pytest.mark.parametrize("b", [0, 63])
+def test_cfg1_naive_oracle(cfg1_out, b):
+    """Requests 0 and B-1 against the candidate-factorised oracle itself (context per list, items
+    per occurrence)."""
     c, W, I, out = cfg1_out
-    naive = oracle.evaluate_naive(c, W, I, requests=[0])[0]
-    stol = rtol_for(c) * score_scale(W, naive["Cp"])
-    assert np.max(np.abs(out["scores"][0] - naive["scores"])) <= stol
-    check_selection(int(out["best"][0]), naive["scores"], stol)
-
-
-@pytest.fixture(scope="module")
-def cfg1_out():
-    c = gen.config(1)
-    W, I = gen.make_weights(c), gen.make_inputs(c)
-    return c, W, I, run_pass(c, W, I)
+    naive = oracle.evaluate_naive(c, W, I, requests=[b])[b]
+    assert normwise(out["Cp"][b], naive["Cp"]) <= rtol_for(c)
+    check_scores(c, out["scores"][b], out["best"][b], naive["scores"], ("naive", b))
 
 
 @pytest.mark.parametrize("K", gen.K_SWEEP)
@@ -85,25 +121,25 @@ def test_cfg2_k_sweep(K):
     c = gen.config(2, K=K)
     W, I = gen.make_weights(c), gen.make_inputs(c)
     out = run_pass(c, W, I)
-    for b in (0, c.B - 1):
-        _compare_request(c, W, out, _stage_refs(c, W, I, b), b, check_kv=(b == 0))
+    check_whole_batch(c, out)
+    if K == 10:
+        for b in (0, c.B - 1):
+            naive = oracle.evaluate_naive(c, W, I, requests=[b])[b]
+            check_scores(c, out["scores"][b], out["best"][b], naive["scores"], ("naive", b))
 
 
 def test_cfg3_long_context():
     c = gen.config(3)
     W, I = gen.make_weights(c), gen.make_inputs(c)
     out = run_pass(c, W, I)
-    for b in (0, c.B - 1):
-        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
+    check_whole_batch(c, out)
 
 
 def test_cfg4_text_hypotheses():
     c = gen.config(4)
     W, I = gen.make_weights(c), gen.make_inputs(c)
     out = run_pass(c, W, I)
-    for b in (0, c.B - 1):
-        _compare_request(c, W, out, _stage_refs(c, W, I, b), b)
-    assert np.all(out["status"] == 0)
+    check_whole_batch(c, out)
 
 
 # ------------------------------------------------------------------------- stage-isolated parity
@@ -200,7 +236,7 @@ def test_permuting_lists_permutes_scores():
         # the distinct set and H are unchanged by a list permutation: bitwise
         assert np.array_equal(p["H"][b], a["H"][b])
         assert np.array_equal(p["seq"][b], a["seq"][b][perm])
-        assert np.max(np.abs(p["scores"][b] - a["scores"][b][perm])) <= rtol_for(c) * score_scale(W, a["Cp"][b])
+        assert np.max(np.abs(p["scores"][b] - a["scores"][b][perm])) <= score_tol(c, a["scores"][b])
 
 
 def test_identical_lists_identical_scores():
@@ -253,6 +289,42 @@ def test_bad_index_sets_status_and_zero_row():
     assert out["status"][1] & fe.FE_DEV_BAD_INDEX
     assert out["slot"][1, 2, 3] == -1 and out["slot"][1, 4, 0] == -1
     assert np.all(out["seq"][1, 2, 4] == 0) and np.all(out["seq"][1, 4, 1] == 0)
+
+
+@pytest.mark.parametrize("cid,shape", [
+    (0, dict(B=2)),                                    # fp32 model: distinct set and rows in one launch
+    (3, dict(B=2, T=64, K=30, L=20)),                  # d = 256, 500 distinct slots: separate set and row gathers
+    (4, dict(B=2, T=64, K=3, L=8)),                    # token ids: the set keyed on the vocabulary
+])
+def test_bad_index_on_separate_set_kernels(cid, shape):
+    """List entries outside [0, M) on the kernels that build the distinct set outside the first
+    item self-attention: the request's status word gets FE_DEV_BAD_INDEX, the entries' slots are
+    -1 and their sequence rows zero; the other request is unaffected and matches the oracle."""
+    c = gen.config(cid, **shape)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    lists = I["lists"].copy()
+    lists[1, 0, 1] = c.M
+    lists[1, c.K - 1, c.L - 1] = -7
+    out = run_pass(c, W, dict(I, lists=lists))
+    assert out["status"][0] == 0
+    assert out["status"][1] == fe.FE_DEV_BAD_INDEX
+    assert out["slot"][1, 0, 1] == -1 and out["slot"][1, c.K - 1, c.L - 1] == -1
+    assert np.all(out["seq"][1, 0, 2] == 0) and np.all(out["seq"][1, c.K - 1, c.L] == 0)
+    _compare_request(c, W, out, _stage_refs(c, W, I, 0), 0)
+
+
+def test_bad_token_sets_status():
+    """Context token ids outside [0, vocab): FE_DEV_BAD_TOKEN in that request's status word only;
+    the other request matches the oracle."""
+    c = gen.config(4, B=2, T=64, K=3, L=8)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ids = I["ctx_ids"].copy()
+    ids[1, 5] = c.vocab
+    ids[1, 63] = -1
+    out = run_pass(c, W, dict(I, ctx_ids=ids))
+    assert out["status"][0] == 0
+    assert out["status"][1] == fe.FE_DEV_BAD_TOKEN
+    _compare_request(c, W, out, _stage_refs(c, W, I, 0), 0)
 
 
 def test_nan_context_selects_minus_one():

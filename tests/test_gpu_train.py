@@ -111,6 +111,20 @@ def test_token_ids():
     check(c, W, I, _relevance(c), "mse")
 
 
+@pytest.mark.parametrize("kind", ["mse", "ce"])
+def test_entries_outside_the_pool(kind):
+    """List entries outside [0, M): left out of the distinct set, zero sequence rows without a
+    position (as in the inference assembly), no feedback and no gradient; loss, scores and every
+    gradient against the reference, which takes the same reading."""
+    c = gen.config(1, B=3, T=20, K=6, L=4, M=25, dtype="f32")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    lists = I["lists"].copy()
+    lists[0, 1, 2] = c.M
+    lists[2, 5, 0] = -3
+    lists[2, 0, 3] = c.M + 11
+    check(c, W, dict(I, lists=lists), _relevance(c), kind)
+
+
 def test_head_width_64():
     c = gen.config(1, B=2, T=12, K=5, L=4, M=18, d=128, n_heads=2, n_layers=1, dtype="f32")
     W, I = gen.make_weights(c), gen.make_inputs(c)

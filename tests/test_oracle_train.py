@@ -117,3 +117,32 @@ def test_relevance_generator_is_seeded_and_binary():
     c = gen.config(1, B=3)
     a, b = gen.make_relevance(c), gen.make_relevance(c)
     assert a.shape == (3, c.M) and np.array_equal(a, b) and set(np.unique(a)) <= {0, 1}
+
+
+def test_entries_outside_the_pool():
+    """An entry outside [0, M): the same scores whatever its value (it is out of the distinct set and
+    its row is a zero row), no feedback in the labels, and gradients that still equal finite
+    differences (the position of that row gets nothing)."""
+    c, W, I = _tiny(0, K=4, L=3, T=6, M=9)
+    W = {k: np.asarray(v, np.float64) for k, v in W.items()}
+    a = gen.make_relevance(c)
+    a[0, :] = 1
+    runs = []
+    for bad in (c.M, c.M + 4, -1, -9):
+        lists = I["lists"].copy()
+        lists[0, 2, 1] = bad
+        J = dict(I, lists=lists)
+        r, _ = train.sequence_labels(lists, a)
+        assert r[0, 2] == 2                             # every element relevant but the outside one
+        P = {k: torch.tensor(v) for k, v in W.items()}
+        runs.append((train.request_scores(c, P, J, 0).numpy(), J))
+    for s_, _ in runs[1:]:
+        assert np.array_equal(s_, runs[0][0])
+    J = runs[0][1]
+    _, g, _ = train.train_grads(c, W, J, a, "mse")
+    for name, idx in (("pos", (2, 3)), ("pos", (1, 0)), ("item.0.w1", (3, 7)), ("cls", (5,))):
+        h = 1e-6
+        Wp = dict(W); Wp[name] = W[name].copy(); Wp[name][idx] += h
+        Wm = dict(W); Wm[name] = W[name].copy(); Wm[name][idx] -= h
+        fd = (_loss_of(c, Wp, J, a, "mse") - _loss_of(c, Wm, J, a, "mse")) / (2 * h)
+        assert abs(fd - g[name][idx]) <= 1e-6 * max(1e-3, abs(fd)), (name, idx, fd, g[name][idx])
