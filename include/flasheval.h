@@ -224,6 +224,23 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
                             size_t ws_bytes, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): fe_cross_sequence without a workspace argument.  Same
+ * computation and kernels, same arguments otherwise (seq [B][K][L+1][d] act in, Cp [B][K][d]
+ * fp32 out, caller-owned device pointers), bit-identical results.  Its scratch (the c_k rows and,
+ * for long lists, many lists, wide or linear models, the block buffers) lives in a static device
+ * array of FE_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs on until the
+ * process ends; the call allocates and frees nothing.  A shape whose scratch exceeds that size
+ * returns FE_EUNSUPPORTED before any launch (e.g. B=64, K=50, L=10 at d=128 needs 1.6 MB).
+ * Every call on one device uses that device's single array: calls that overlap on one device
+ * (concurrent streams or threads) race and give undefined results; calls ordered on one stream
+ * are safe.  Nothing in the array needs to start at zero.
+ */
+#define FE_NOALLOC_SCRATCH_BYTES (32u << 20)
+fe_status fe_cross_sequence_noalloc(const fe_model* m, int B, int K, int L, const void* seq, float* Cp,
+                                    void* stream);
+
+/*
  * Section 4.4 and eq. (1): scores[b][k] = Cp[b][k] . head.w + head.b (fp32),
  * best[b] = smallest k with the maximal score, NaN scores skipped, -1 if all
  * are NaN.  Cp [B][K][d] fp32, scores [B][K] fp32, best [B] int32.

@@ -597,6 +597,84 @@ fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const fl
   return FE_OK;
 }
 
+// SeqEnc, then the cross-sequence module, on the buffers b (SeqEnc's separate-block path) and c
+// (fp32 [B*K][d], the c_k rows; the cross module's residual when it runs block by block); lin_st:
+// linear models' per-head state buffer of one module (fp32 [B][H][dh+1][dh]).
+fe_status cross_sequence_run(const fe_model* m, int B, int K, int L, const void* seq, float* Cp, const Bufs& b,
+                             float* c, float* lin_st, hipStream_t s) {
+  fe_status st = seq_encode(m, B, K, L, seq, c, b, s);
+  if (st != FE_OK) return st;
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  if (!lin && module_fits(m, K))
+    return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
+  Bufs bc{c, b.qkv, b.O, b.Hf, b.ln};
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin ? lin_st : nullptr);
+    if (st != FE_OK) return st;
+  }
+  FE_LAUNCH(F_LN, s, launch_layernorm(c, 1, m->cfg.d, B * K, m->cfg.d, m->cross_lnf_g, m->cross_lnf_b, Cp, 1, m->cfg.d,
+                                      m->bf16, s));
+  return FE_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Library-owned scratch of fe_cross_sequence_noalloc: one copy per device, held until the
+// process ends.  Host code never passes the symbol itself to a kernel or copy (on the host it
+// is only a stand-in); it uses the device address hipGetSymbolAddress returns for each device.
+// ------------------------------------------------------------------------------------------
+constexpr size_t kScratchBytes = FE_NOALLOC_SCRATCH_BYTES;
+static_assert(kScratchBytes % 256 == 0, "scratch pieces are 256-byte aligned");
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on `device`, looked up once per device with that device current.
+fe_status scratch_address(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices) return fail(FE_EUNSUPPORTED, "device %d outside [0, %d)", device, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    int cur = -1;
+    FE_HIP(hipGetDevice(&cur));
+    if (cur != device) FE_HIP(hipSetDevice(device));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != device) (void)hipSetDevice(cur);
+    if (e != hipSuccess) return fail(FE_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    if (!p) return fail(FE_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[device] = p;
+  }
+  *out = g_scratch_ptr[device];
+  return FE_OK;
+}
+
+// What fe_cross_sequence needs of its workspace, packed: the c rows always; SeqEnc's residual and
+// block buffers only when its lists are too long for the module kernel; the block buffers of the
+// cross module only when it runs block by block (K > 64, wide or linear models).
+struct CrossScratch { size_t c, X, qkv, O, Hf, ln, lin_st, total; };
+
+CrossScratch cross_scratch_layout(const fe_model* m, long long B, long long K, long long L) {
+  const long long d = m->cfg.d, F = m->cfg.ffn_dim, S = L + 1, H = m->cfg.n_heads, dh = d / H;
+  const size_t e = m->bf16 ? 2 : 4;
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  const bool seq_blocks = !module_fits(m, (int)S), cross_blocks = lin || !module_fits(m, (int)K);
+  CrossScratch w{};
+  Bump b{0};
+  w.c = b.take(B * K * d * 4);
+  const long long rows = std::max(seq_blocks ? B * K * S : 0, cross_blocks ? B * K : 0);
+  if (seq_blocks) w.X = b.take(B * K * S * d * 4);
+  if (rows > 0) {
+    w.qkv = b.take(rows * 3 * d * e);
+    w.O = b.take(rows * d * e);
+    w.Hf = b.take(rows * F * e);
+    if (wide(m)) w.ln = b.take(rows * d * 2);
+  }
+  if (lin) w.lin_st = b.take(B * H * (dh + 1) * dh * 4);
+  w.total = (b.at + 255) & ~size_t(255);
+  return w;
+}
+
 }  // namespace
 
 // Records the error text of a call implemented in another file of the library (the training step).
@@ -1010,24 +1088,28 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   if (!aligned16(seq) || !aligned16(Cp) || !aligned16(ws)) return fail(FE_EINVAL, "pointers must be 16-byte aligned");
   const Ws w = layout(m, B, 1, 1, K, L);
   if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const bool bf = m->bf16;
-  const int d = m->cfg.d;
   Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h), at<char>(ws, w.s_ln)};
-  float* c = at<float>(ws, w.s_c);
-  st = seq_encode(m, B, K, L, seq, c, b, s);
+  return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(ws, w.s_c),
+                            m->cfg.attention == FE_ATTN_LINEAR ? at<float>(ws, w.lin_st) : nullptr,
+                            static_cast<hipStream_t>(stream));
+}
+
+fe_status fe_cross_sequence_noalloc(const fe_model* m, int B, int K, int L, const void* seq, float* Cp, void* stream) {
+  fe_status st = check_dims(m, B, 1, 1, K, L);
   if (st != FE_OK) return st;
-  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
-  if (!lin && module_fits(m, K))
-    return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
-  Bufs bc{c, b.qkv, b.O, b.Hf, b.ln};
-  float* lin_st = lin ? at<float>(ws, w.lin_st) : nullptr;
-  for (int l = 0; l < m->cfg.n_layers; ++l) {
-    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin_st);
-    if (st != FE_OK) return st;
-  }
-  FE_LAUNCH(F_LN, s, launch_layernorm(c, 1, d, B * K, d, m->cross_lnf_g, m->cross_lnf_b, Cp, 1, d, bf, s));
-  return FE_OK;
+  if (!seq || !Cp) return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(seq) || !aligned16(Cp)) return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const CrossScratch w = cross_scratch_layout(m, B, K, L);
+  if (w.total > kScratchBytes)
+    return fail(FE_EUNSUPPORTED, "B=%d K=%d L=%d needs %zu bytes of scratch; the static scratch holds %zu", B, K, L,
+                w.total, kScratchBytes);
+  void* base = nullptr;
+  st = scratch_address(m->device, &base);
+  if (st != FE_OK) return st;
+  Bufs b{at<float>(base, w.X), at<char>(base, w.qkv), at<char>(base, w.O), at<char>(base, w.Hf), at<char>(base, w.ln)};
+  return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(base, w.c),
+                            m->cfg.attention == FE_ATTN_LINEAR ? at<float>(base, w.lin_st) : nullptr,
+                            static_cast<hipStream_t>(stream));
 }
 
 fe_status fe_encode_sequences(const fe_model* m, int B, int K, int L, const void* seq, float* C, void* ws,

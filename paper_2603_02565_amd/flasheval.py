@@ -25,7 +25,7 @@ LOSS_KIND = {"mse": FE_LOSS_MSE, "bce": FE_LOSS_BCE, "ce": FE_LOSS_CE}
 
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_kv_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
-            "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
+            "fe_cross_sequence_noalloc", "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
             "fe_trace_read_launches", "fe_trace_family", "fe_train_workspace_size", "fe_train_grads")
 FE_TRACE_FAMILIES = 12
 
@@ -68,6 +68,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_encode_items": (S, [P, I, I, P, P, I, I, P, I, P, P, P, P, P, Z, P]),
         "fe_assemble": (S, [P, I, I, I, I, P, P, P, P]),
         "fe_cross_sequence": (S, [P, I, I, I, P, P, P, Z, P]),
+        "fe_cross_sequence_noalloc": (S, [P, I, I, I, P, P, P]),
         "fe_score_select": (S, [P, I, I, P, P, P, P]),
         "fe_encode_sequences": (S, [P, I, I, I, P, P, P, Z, P]),
         "fe_score_objectives": (S, [P, I, I, P, I, P, P, P, P, P, P, P]),
@@ -201,6 +202,15 @@ def fe_assemble(model: int, B: int, K: int, L: int, U_cap: int, slot, H, seq, st
 def fe_cross_sequence(model: int, B: int, K: int, L: int, seq, Cp, ws, stream=None) -> None:
     _check(load_library().fe_cross_sequence(model, B, K, L, _ptr(seq), _ptr(Cp), _ptr(ws),
                                             ws.numel() * ws.element_size(), _stream(stream)), "fe_cross_sequence")
+
+
+FE_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def fe_cross_sequence_noalloc(model: int, B: int, K: int, L: int, seq, Cp, stream=None) -> None:
+    """fe_cross_sequence with the library's static scratch instead of a workspace (allocates nothing)."""
+    _check(load_library().fe_cross_sequence_noalloc(model, B, K, L, _ptr(seq), _ptr(Cp), _stream(stream)),
+           "fe_cross_sequence_noalloc")
 
 
 def fe_score_select(model: int, B: int, K: int, Cp, scores, best, stream=None) -> None:
