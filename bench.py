@@ -339,6 +339,116 @@ def time_pass(step, stream, steps, warmup):
     return e0.elapsed_time(e1) / steps
 
 
+def graph_us(fn, stream, reps: int = ASM_REPS, replays: int = 5) -> float:
+    """Mean duration of one call of `fn` when `reps` calls run back to back on the device: the calls
+    are captured as one HIP graph and the graph is replayed `replays` times between two events (no
+    per-launch event or host call in between), in microseconds."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(replays):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (replays * reps)
+    del g
+    return us
+
+
+def assemble_entry(c, U, ev, bufs, stream):
+    """The assembly alone (fe_assemble back to back from a HIP graph) against its algorithmic bytes,
+    beside two reference points timed the same way: torch's fill of a tensor the size of seq (the
+    write-only floor: the assembly writes those bytes and reads less than a tenth as much) and
+    torch's copy of it (read + write)."""
+    import torch
+    from paper_2603_02565_amd import flasheval as fe
+    b = bufs
+    asm_us = graph_us(lambda: fe.fe_assemble(ev.handle, c.B, c.K, c.L, b["U_cap"], b["slot"], b["H"], b["seq"]), stream)
+    nbytes = assemble_bytes(c, U)
+    scratch = torch.empty_like(b["seq"])
+    seq_bytes = scratch.numel() * scratch.element_size()
+    fill_us = graph_us(lambda: scratch.fill_(0.5), stream)
+    copy_us = graph_us(lambda: scratch.copy_(b["seq"]), stream)
+    del scratch
+    gbs = nbytes / (asm_us / 1e6) / 1e9
+    return {"avg_launch_us": round(asm_us, 3), "bytes_per_launch": int(nbytes), "GBps": round(gbs, 1),
+            "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+            "timing": f"mean of {5 * ASM_REPS} back-to-back launches replayed from a HIP graph",
+            "write_floor": {"avg_launch_us": round(fill_us, 3), "bytes_per_launch": seq_bytes,
+                            "GBps": round(seq_bytes / (fill_us / 1e6) / 1e9, 1),
+                            "what": "torch fill_ of a tensor the size of seq (write only), timed the same way"},
+            "copy_reference": {"avg_launch_us": round(copy_us, 3), "bytes_per_launch": 2 * seq_bytes,
+                               "GBps": round(2 * seq_bytes / (copy_us / 1e6) / 1e9, 1),
+                               "what": "torch copy_ of a tensor the size of seq (read + write), timed the same way"}}
+
+
+def workload_entry(c, steps: int, warmup: int, trace: bool = True):
+    """One workload's pass on this GPU: time per batch (events over `steps` back-to-back passes),
+    lists/s, the measured distinct-element counts, the item stage (fe_encode_items) timed alone, the
+    assembly against its write-only floor, and the dominant matrix-product kernel family with its
+    TFLOP/s (per-launch trace times scaled to the untraced pass)."""
+    import numpy as np
+    import torch
+    import gen
+    from paper_2603_02565_amd import flasheval as fe
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    ev = fe.Evaluator(c.d, c.n_heads, c.n_layers, c.ffn, c.max_L, c.vocab, c.dtype, W, attention=c.attention)
+    bufs = ev.allocate(c.B, c.T, c.M, c.K, c.L)
+    act = torch.bfloat16 if c.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    x = None if I["x"] is None else torch.from_numpy(I["x"]).to(dev).to(act)
+    pool = None if I["pool"] is None else torch.from_numpy(I["pool"]).to(dev).to(act)
+    ids = None if I["ctx_ids"] is None else torch.from_numpy(I["ctx_ids"]).to(dev)
+    lists = torch.from_numpy(I["lists"]).to(dev)
+    stream = torch.cuda.current_stream()
+    b = bufs
+
+    def step():
+        ev.run(x=x, ctx_ids=ids, pool=pool, lists=lists)
+
+    ms = time_pass(step, stream, steps, warmup)
+    U = b["n_uniq"].cpu().numpy().tolist()
+    items_us = time_pass(lambda: fe.fe_encode_items(ev.handle, c.B, c.M, pool, lists, c.K, c.L, b["kv"], c.T, b["uniq"],
+                                                    b["n_uniq"], b["slot"], b["H"], b["ws"]),
+                         stream, steps, warmup) * 1e3
+    entry = {"workload": c.label, "B": c.B, "T": c.T, "d": c.d, "K": c.K, "L": c.L, "M": c.M,
+             "attention": c.attention, "lists_per_batch": c.B * c.K, "ms_per_batch": round(ms, 5),
+             "lists_per_s": round(c.B * c.K / (ms / 1e3), 1), "U_mean": round(float(np.mean(U)), 2),
+             "rho": round(c.K * c.L / float(np.mean(U)), 3), "item_stage_us": round(items_us, 2),
+             "assemble": assemble_entry(c, U, ev, b, stream)}
+    if trace:
+        fe.fe_trace_enable(True)
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        fam = fe.fe_trace_read()
+        fe.fe_trace_enable(False)
+        fam = {k: v for k, v in fam.items() if v[1] > 0}
+        traced = sum(v[0] for v in fam.values()) / steps
+        scale = min(1.0, ms / traced) if traced > 0 else 1.0
+        flops = family_flops(c, U, set(fam))
+        peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
+        mm = {k: v for k, v in fam.items() if k in MATRIX_FAMILIES and flops.get(k, 0.0) > 0}
+        if mm:
+            dom = max(mm, key=lambda k: mm[k][0])
+            t_ms = mm[dom][0] / steps * scale
+            tf = flops[dom] / (t_ms / 1e3) / 1e12
+            entry["dominant_family"] = {"family": dom, "ms_per_batch": round(t_ms, 5), "tflops": round(tf, 2),
+                                        "mfma_frac": round(tf / peak, 4), "share_of_pass": round(t_ms / ms, 4)}
+            mm_ms = sum(v[0] for v in mm.values()) / steps * scale
+            entry["mfma_util_matrix_stages"] = round(sum(flops[k] for k in mm) / (mm_ms / 1e3) / 1e12 / peak, 4)
+    ev.close()
+    del bufs, x, pool, ids, lists
+    torch.cuda.empty_cache()
+    return entry
+
+
 def copy_calibration() -> int:
     """A plain elementwise copy of 256 MiB (fp32 x 1.0), three times: reads and writes 256 MiB each."""
     import torch
@@ -372,6 +482,8 @@ def main() -> int:
     ap.add_argument("--train-steps", type=int, default=10)
     ap.add_argument("--no-variants", action="store_true",
                     help="skip timing the pass without cross-sequence interaction (for profiler runs)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the K sweep and the long-context / text-hypothesis workloads after the headline run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB copy (to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -474,45 +586,8 @@ def main() -> int:
         graph_ms = g0.elapsed_time(g1) / args.steps
         del graph
 
-    # ---- the assembly alone: ASM_REPS launches of fe_assemble on the pass's own buffers, captured
-    #      as one HIP graph so that the launches run back to back on the device (per-launch host
-    #      calls would otherwise leave gaps longer than the kernel); average duration per launch
-    asm_loop_us = copy_ref = None
-    if not args.no_trace:
-        b = bufs
-        asm_graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(asm_graph):
-            for _ in range(ASM_REPS):
-                fe.fe_assemble(ev.handle, c.B, c.K, c.L, b["U_cap"], b["slot"], b["H"], b["seq"])
-        asm_graph.replay()
-        torch.cuda.synchronize()
-        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a0.record(stream)
-        for _ in range(5):
-            asm_graph.replay()
-        a1.record(stream)
-        torch.cuda.synchronize()
-        asm_loop_us = a0.elapsed_time(a1) * 1e3 / (5 * ASM_REPS)
-        del asm_graph
-        # reference point: torch's device copy of a tensor the size of seq, timed the same way
-        seq_copy = torch.empty_like(b["seq"])
-        copy_graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(copy_graph):
-            for _ in range(ASM_REPS):
-                seq_copy.copy_(b["seq"])
-        copy_graph.replay()
-        torch.cuda.synchronize()
-        a0.record(stream)
-        for _ in range(5):
-            copy_graph.replay()
-        a1.record(stream)
-        torch.cuda.synchronize()
-        copy_us = a0.elapsed_time(a1) * 1e3 / (5 * ASM_REPS)
-        copy_bytes = 2 * seq_copy.numel() * seq_copy.element_size()
-        copy_ref = {"avg_launch_us": round(copy_us, 3), "bytes_per_launch": copy_bytes,
-                    "GBps": round(copy_bytes / (copy_us / 1e6) / 1e9, 1),
-                    "what": "torch copy_ of a tensor the size of seq (read + write), back to back from a HIP graph"}
-        del copy_graph, seq_copy
+    # ---- the assembly alone, against its write-only floor and a copy of the same size
+    asm_entry = assemble_entry(c, U, ev, bufs, stream) if not args.no_trace else None
 
     # ---- kernel-timing region: the same steps with HIP events around every launch
     fam = {}
@@ -571,17 +646,12 @@ def main() -> int:
     if fam:
         peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_FP32_TFLOPS
         stages, flops = stage_table(c, U, fam, args.steps)
-        if "assemble" in stages:
+        if "assemble" in stages and asm_entry is not None:
             # per-launch events add their own overhead to a kernel this short: the back-to-back
             # average from the graph of assembly launches is the duration the fraction uses
-            stages["assemble"]["traced_avg_launch_us"] = stages["assemble"]["avg_launch_us"]
-            if asm_loop_us is not None:
-                stages["assemble"]["avg_launch_us"] = round(asm_loop_us, 3)
-            gbs = asm_bytes / (stages["assemble"]["avg_launch_us"] / 1e6) / 1e9
-            stages["assemble"].update(bytes_per_launch=int(asm_bytes), GBps=round(gbs, 1),
-                                      hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
-                                      timing=f"mean of {5 * ASM_REPS} back-to-back launches replayed from a HIP graph",
-                                      copy_reference=copy_ref)
+            traced_us = stages["assemble"]["avg_launch_us"]
+            stages["assemble"].update(asm_entry)
+            stages["assemble"]["traced_avg_launch_us"] = traced_us
         dom = max((k for k in stages if k != "linear"), key=lambda k: stages[k]["ms_per_step"])
         dom_ms, dom_n = fam[dom]
         avg_s = dom_ms / dom_n / 1e3
@@ -611,10 +681,21 @@ def main() -> int:
                                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": measured_traffic(dom),
                                "avg_launch_us": round(avg_s * 1e6, 3), "launches_per_step": dom_n // args.steps}
         mm_fams = [k for k in MATRIX_FAMILIES if k in stages]
-        mm_ms = sum(fam[k][0] for k in mm_fams) / args.steps
+        traced_ms = sum(v[0] for v in fam.values()) / args.steps
+        # each per-launch event pair adds its own overhead (about 2 us), so the traced kernel times
+        # sum to more than the untraced pass; the matrix stages' time is taken as their traced share
+        # of the untraced pass time (the pass runs its kernels back to back)
+        scale = min(1.0, ms_per_step / traced_ms) if traced_ms > 0 else 1.0
+        mm_ms = sum(fam[k][0] for k in mm_fams) / args.steps * scale
         mm_flops = sum(flops.get(k, 0.0) for k in mm_fams)
         out["mfma_util_matrix_stages"] = round(mm_flops / (mm_ms / 1e3) / 1e12 / peak, 4)
-        out["kernel_ms_per_step"] = round(sum(v[0] for v in fam.values()) / args.steps, 5)
+        out["mfma_util_timing"] = (f"matrix-stage kernel time = their share of the traced kernel time x the untraced "
+                                   f"pass time (scale {scale:.3f}); flops algorithmic")
+        for k in mm_fams:
+            if "tflops" in stages[k]:
+                tf = stages[k]["tflops"] / scale
+                stages[k].update(tflops_event_corrected=round(tf, 2), mfma_frac_event_corrected=round(tf / peak, 4))
+        out["kernel_ms_per_step"] = round(traced_ms, 5)
         out["stages"] = stages
     if not args.no_variants and c.attention == "softmax":
         # the linear-attention variant (the deployment setting of Appendix B.3) on the same weights
@@ -697,6 +778,18 @@ def main() -> int:
                     "parameter, on this batch in fp32"}
         del Pt, Gt, wst
         torch.cuda.empty_cache()
+    if not args.no_sweep and args.workload == 1:
+        # the other workloads on the same GPU in the same run: the K sweep on the RecSys-base shapes
+        # (Section 5.2: the item stage follows the distinct elements, not the K*L occurrences), the
+        # long-context workload (softmax and linear attention) and the text-hypothesis workload
+        n_steps = max(10, min(args.steps, 30))
+        ev.close()
+        del bufs
+        torch.cuda.empty_cache()
+        out["k_sweep"] = [workload_entry(gen.config(2, K=k), n_steps, 5, trace=not args.no_trace) for k in gen.K_SWEEP]
+        out["workloads"] = [workload_entry(gen.config(3), n_steps, 5, trace=not args.no_trace),
+                            workload_entry(gen.config(3, attention="linear"), n_steps, 5, trace=not args.no_trace),
+                            workload_entry(gen.config(4), n_steps, 5, trace=not args.no_trace)]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(c, W, I, args.cpu_seconds)
         out["cpu_baseline"]["joint_order"] = cpu_cached(c, W, I, args.cpu_seconds / 3)

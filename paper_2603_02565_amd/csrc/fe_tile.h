@@ -111,17 +111,18 @@ FE_DEV bool mark_rows(int row0, int R, const int32_t* nvalid, int rpb, int* s_va
 
 // Column-split product over an LDS tile: wave w computes the 32-column output blocks
 // w + 4j (j < NCB/4) of As[TM][K] x W, NBW blocks at a time, with the weight fragments
-// streamed through registers one 8-fragment stage ahead (all shapes compile-time, so the
-// stage loop unrolls completely and fragment addresses are immediate offsets).  start() issues the first
-// stage (so its latency can hide behind other work); run() calls epi(cb, rb, acc) for every
-// finished 32x32 block: epi(jj, cb, rb, acc) with jj the wave-local block index (compile-time
-// after unrolling), cb = wave + 4*jj the column block and rb the row block.
+// streamed through registers in stages of 8 fragments, PF stages ahead of the one being consumed
+// (PF >= the stage count: every fragment is requested by start()).  All shapes are compile-time,
+// so the stage loop unrolls completely and fragment addresses are immediate offsets.  start()
+// issues the first PF stages (so their latency can hide behind other work); run() calls
+// epi(jj, cb, rb, acc) for every finished 32x32 block, with jj the wave-local block index
+// (compile-time after unrolling), cb = wave + 4*jj the column block and rb the row block.
 //
 // The product is formed transposed, C^T = W^T A^T: the packed weight fragments are the A
 // operand and the activation fragments the B operand.  Each lane then holds one output ROW
 // (rb*32 + lane%32) and, in acc[4q..4q+3], the four consecutive output columns
 // 8q + 4*(lane/32) .. +3 of the block (q = 0..3), so epilogues write 8- or 16-byte vectors.
-template <int TM, int K, int NCB>
+template <int TM, int K, int NCB, int PF = 1>
 struct ColGemm {
   static constexpr int RB = TM / 32, KS = K / 16, NBW = 4 / RB;
   static constexpr int BPW = NCB / 4;                            // column blocks per wave
@@ -129,8 +130,10 @@ struct ColGemm {
   static constexpr int NSK = KS / KB;                            // stages per column group
   static constexpr int NG = (BPW + NBW - 1) / NBW;               // column groups per wave
   static constexpr int NST = NG * NSK;                           // stages per wave
-  static_assert(NCB % 4 == 0 && KS % KB == 0, "unsupported shape");
-  bf16x8 buf[2][NBW][KB];
+  static constexpr int AHEAD = PF < NST ? PF : NST;              // stages in flight ahead
+  static constexpr int NBUF = AHEAD < NST ? AHEAD + 1 : NST;     // register ring slots
+  static_assert(NCB % 4 == 0 && KS % KB == 0 && PF >= 1, "unsupported shape");
+  bf16x8 buf[NBUF][NBW][KB];
   const bf16x8* Wl;   // this wave's first column block, this lane's fragment slot
 
   static constexpr int blocks_in(int g) { return (g + 1) * NBW <= BPW ? NBW : BPW - g * NBW; }
@@ -140,13 +143,14 @@ struct ColGemm {
     for (int j = 0; j < NBW; ++j) {
       if (j >= blocks_in(g)) continue;
 #pragma unroll
-      for (int kk = 0; kk < KB; ++kk) buf[t & 1][j][kk] = Wl[((4 * (g * NBW + j)) * KS + sk * KB + kk) * 64];
+      for (int kk = 0; kk < KB; ++kk) buf[t % NBUF][j][kk] = Wl[((4 * (g * NBW + j)) * KS + sk * KB + kk) * 64];
     }
   }
   FE_DEV void start(const void* W) {
     const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3);   // wave within its group of four
     Wl = reinterpret_cast<const bf16x8*>(W) + (long long)wave * KS * 64 + (threadIdx.x & 63);
-    load(0);
+#pragma unroll
+    for (int t = 0; t < AHEAD; ++t) load(t);
   }
   template <class Epi>
   FE_DEV void run(const bf16* As, int lda, Epi&& epi) {
@@ -156,7 +160,7 @@ struct ColGemm {
 #pragma unroll
     for (int t = 0; t < NST; ++t) {
       const int g = t / NSK, sk = t % NSK;
-      if (t + 1 < NST) load(t + 1);
+      if (t + AHEAD < NST) load(t + AHEAD);
       if (sk == 0) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
@@ -178,7 +182,7 @@ struct ColGemm {
           if (j >= blocks_in(g)) continue;
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            acc[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t & 1][j][kk], af[kk][rb], acc[rb][j], 0, 0, 0);
+            acc[rb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(buf[t % NBUF][j][kk], af[kk][rb], acc[rb][j], 0, 0, 0);
         }
       if (sk != NSK - 1) continue;
 #pragma unroll
