@@ -293,6 +293,7 @@ bool wide(const fe_model* m) { return m->bf16 && m->cfg.d >= kWideD; }
 struct Ws {
   size_t status;                                        // int32 [2][B]: items, context
   size_t lin_st;                                        // linear models: fp32 [B][H][dh+1][dh], one module's state
+  size_t lin_part;                                      // linear models: the key splits' partial states
   size_t c_kvp;                                         // linear models: act [n][2][B][T][d] item-layer keys/values
   size_t c_xin, c_x, c_qkv, c_o, c_h, c_ln;             // context stage
   size_t i_g0, i_g, i_g1, i_qkv, i_o, i_q, i_h, i_ln;   // item stage
@@ -318,7 +319,11 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
   w.status = b0.take(2 * B * 4);
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
   const long long H = m->cfg.n_heads, dh = d / H;
-  if (lin) w.lin_st = b0.take(B * H * (dh + 1) * dh * 4);
+  if (lin) {
+    w.lin_st = b0.take(B * H * (dh + 1) * dh * 4);
+    const long long ns = std::max(lin_state_splits((int)(B * H), (int)T, m->bf16), lin_state_splits((int)(B * H), (int)K, m->bf16));
+    w.lin_part = b0.take(B * H * ns * (dh + 1) * dh * 4);
+  }
   size_t base = b0.at, end = base;
   {  // context
     const long long R = B * T;
@@ -463,7 +468,8 @@ struct KvOut {
 // lin_st != nullptr: the block's attention is linear, through the state buffer lin_st
 // (fp32 [nb][H][dh+1][dh]).
 fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const void* xin, bool xin_f32, const Bufs& b,
-                    const int32_t* nvalid, hipStream_t s, const KvOut* kvo = nullptr, float* lin_st = nullptr) {
+                    const int32_t* nvalid, hipStream_t s, const KvOut* kvo = nullptr, float* lin_st = nullptr,
+                    float* lin_part = nullptr) {
   const int d = m->cfg.d, F = m->cfg.ffn_dim, R = nb * per;
   const bool bf = m->bf16;
   const size_t e = bf ? 2 : 4;
@@ -477,7 +483,7 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     const int H = m->cfg.n_heads, dh = d / H;
     const char* qkv = static_cast<const char*>(b.qkv);
     FE_LAUNCH(F_LIN, s, launch_lin_state(qkv + d * e, qkv + 2 * d * e, (long long)per * 3 * d, 3 * d, nb, per, nvalid,
-                                          H, dh, lin_st, bf, s));
+                                          H, dh, lin_st, bf, s, lin_part));
     FE_LAUNCH(F_LIN, s, launch_lin_apply(qkv, 3 * d, lin_st, nb, per, nvalid, H, dh, b.O, d, bf, s));
   } else if (bf && self_attention_fits(d, m->cfg.n_heads, per)) {
     // LN1, q|k|v of one head and attention in one kernel per (batch, head)
@@ -601,7 +607,7 @@ fe_status run_ffn(const fe_model* m, float* X, int R, const float* lng, const fl
 // (fp32 [B*K][d], the c_k rows; the cross module's residual when it runs block by block); lin_st:
 // linear models' per-head state buffer of one module (fp32 [B][H][dh+1][dh]).
 fe_status cross_sequence_run(const fe_model* m, int B, int K, int L, const void* seq, float* Cp, const Bufs& b,
-                             float* c, float* lin_st, hipStream_t s) {
+                             float* c, float* lin_st, float* lin_part, hipStream_t s) {
   fe_status st = seq_encode(m, B, K, L, seq, c, b, s);
   if (st != FE_OK) return st;
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
@@ -609,7 +615,7 @@ fe_status cross_sequence_run(const fe_model* m, int B, int K, int L, const void*
     return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
   Bufs bc{c, b.qkv, b.O, b.Hf, b.ln};
   for (int l = 0; l < m->cfg.n_layers; ++l) {
-    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin ? lin_st : nullptr);
+    st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin ? lin_st : nullptr, lin_part);
     if (st != FE_OK) return st;
   }
   FE_LAUNCH(F_LN, s, launch_layernorm(c, 1, m->cfg.d, B * K, m->cfg.d, m->cross_lnf_g, m->cross_lnf_b, Cp, 1, m->cfg.d,
@@ -652,7 +658,7 @@ fe_status scratch_address(int device, void** out) {
 // What fe_cross_sequence needs of its workspace, packed: the c rows always; SeqEnc's residual and
 // block buffers only when its lists are too long for the module kernel; the block buffers of the
 // cross module only when it runs block by block (K > 64, wide or linear models).
-struct CrossScratch { size_t c, X, qkv, O, Hf, ln, lin_st, total; };
+struct CrossScratch { size_t c, X, qkv, O, Hf, ln, lin_st, lin_part, total; };
 
 CrossScratch cross_scratch_layout(const fe_model* m, long long B, long long K, long long L) {
   const long long d = m->cfg.d, F = m->cfg.ffn_dim, S = L + 1, H = m->cfg.n_heads, dh = d / H;
@@ -670,7 +676,10 @@ CrossScratch cross_scratch_layout(const fe_model* m, long long B, long long K, l
     w.Hf = b.take(rows * F * e);
     if (wide(m)) w.ln = b.take(rows * d * 2);
   }
-  if (lin) w.lin_st = b.take(B * H * (dh + 1) * dh * 4);
+  if (lin) {
+    w.lin_st = b.take(B * H * (dh + 1) * dh * 4);
+    w.lin_part = b.take(B * H * lin_state_splits((int)(B * H), (int)K, m->bf16) * (dh + 1) * dh * 4);
+  }
   w.total = (b.at + 255) & ~size_t(255);
   return w;
 }
@@ -875,6 +884,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
   // their per-head state
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
   float* lin_st = lin ? at<float>(ws, w.lin_st) : nullptr;
+  float* lin_part = lin ? at<float>(ws, w.lin_part) : nullptr;
   void* kvp = lin ? at<char>(ws, w.c_kvp) : kv;
   const bool whole = !lin && module_fits(m, T);
   b.xbf = bf && !wide(m) && !whole;   // block by block through the fused tails: bf16 between kernels
@@ -889,7 +899,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       const bool last = l + 1 == m->cfg.n_layers;
       st = enc_block(m, m->ctx[l], B, T, l == 0 ? src : b.X, l > 0 && !b.xbf, b, nullptr, s,
-                     bf && !wide(m) && last ? &kvo : nullptr, lin_st);
+                     bf && !wide(m) && last ? &kvo : nullptr, lin_st, lin_part);
       if (st != FE_OK) return st;
     }
   }
@@ -917,7 +927,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
       const char* K = static_cast<const char*>(kvp) + (size_t)(2 * l) * R * d * e;
       const char* V = static_cast<const char*>(kvp) + (size_t)(2 * l + 1) * R * d * e;
       float* out = static_cast<float*>(kv) + (size_t)l * B * H * (dh + 1) * dh;
-      FE_LAUNCH(F_LIN, s, launch_lin_state(K, V, (long long)T * d, d, B, T, nullptr, H, dh, out, bf, s));
+      FE_LAUNCH(F_LIN, s, launch_lin_state(K, V, (long long)T * d, d, B, T, nullptr, H, dh, out, bf, s, lin_part));
     }
   }
   return FE_OK;
@@ -1089,9 +1099,9 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   const Ws w = layout(m, B, 1, 1, K, L);
   if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
   Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h), at<char>(ws, w.s_ln)};
-  return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(ws, w.s_c),
-                            m->cfg.attention == FE_ATTN_LINEAR ? at<float>(ws, w.lin_st) : nullptr,
-                            static_cast<hipStream_t>(stream));
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(ws, w.s_c), lin ? at<float>(ws, w.lin_st) : nullptr,
+                            lin ? at<float>(ws, w.lin_part) : nullptr, static_cast<hipStream_t>(stream));
 }
 
 fe_status fe_cross_sequence_noalloc(const fe_model* m, int B, int K, int L, const void* seq, float* Cp, void* stream) {
@@ -1107,9 +1117,9 @@ fe_status fe_cross_sequence_noalloc(const fe_model* m, int B, int K, int L, cons
   st = scratch_address(m->device, &base);
   if (st != FE_OK) return st;
   Bufs b{at<float>(base, w.X), at<char>(base, w.qkv), at<char>(base, w.O), at<char>(base, w.Hf), at<char>(base, w.ln)};
-  return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(base, w.c),
-                            m->cfg.attention == FE_ATTN_LINEAR ? at<float>(base, w.lin_st) : nullptr,
-                            static_cast<hipStream_t>(stream));
+  const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
+  return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(base, w.c), lin ? at<float>(base, w.lin_st) : nullptr,
+                            lin ? at<float>(base, w.lin_part) : nullptr, static_cast<hipStream_t>(stream));
 }
 
 fe_status fe_encode_sequences(const fe_model* m, int B, int K, int L, const void* seq, float* C, void* ws,

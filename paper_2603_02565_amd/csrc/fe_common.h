@@ -232,7 +232,11 @@ hipError_t launch_layernorm_masked(const void* X, int x_f32, long long x_rs, int
 // St [B][H][dh + 1][dh] fp32 (rows 0..dh-1: sum_t phi(k_t) v_t^T, row dh: sum_t phi(k_t)); key row t
 // of batch b at K + b*bs + t*rs + h*dh elements (V likewise), keys t < nvalid[b] (or nk).
 hipError_t launch_lin_state(const void* K, const void* V, long long bs, int rs, int B, int nk, const int32_t* nvalid,
-                            int H, int dh, float* St, bool bf16_model, hipStream_t s);
+                            int H, int dh, float* St, bool bf16_model, hipStream_t s,
+                            float* part = nullptr);
+// Key splits launch_lin_state uses for BH (batch, head) states over nk keys when given a partial
+// buffer `part` of BH * splits * (dh + 1) * dh floats (bf16 models; 1 = no split, no buffer used).
+int lin_state_splits(int BH, int nk, bool bf16_model);
 // O[b*rpb + r][h*dh + j] = (phi(q) S)_j / (phi(q) . z) for q = Q[b*rpb + r][h*dh ..], rows r < rpb
 // and r < nvalid[b] (others untouched); row strides q_rs, o_rs (elements, 16-byte multiples).
 hipError_t launch_lin_apply(const void* Q, int q_rs, const float* St, int B, int rpb, const int32_t* nvalid, int H,

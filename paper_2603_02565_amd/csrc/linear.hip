@@ -11,6 +11,8 @@
 //   v_mfma_f32_32x32x16_bf16 from phi(k) and v rounded to bf16 (fp32 accumulation); z and fp32
 //   models use fp32 VALU sums.  Every sum runs in a fixed order, so results are reproducible.
 // k_lin_apply: the attention output of every valid query row from the state, fp32 arithmetic.
+#include <algorithm>
+
 #include "fe_common.h"
 
 namespace {
@@ -27,18 +29,20 @@ FE_DEV void wave_lds_sync() {
 }
 
 // ------------------------------------------------------------------------------------------
-// State, bf16 models.  One workgroup (four waves) per (batch, head).  Wave w takes the 64-key
-// chunks w, w + 4, ...; per chunk every lane loads its share of the keys and values (16-byte
+// State, bf16 models.  One workgroup (four waves) per (batch, head, key split): split sp of
+// nsplit takes the 64-key chunks [sp * cps, (sp + 1) * cps), cps = ceil(chunks / nsplit), and wave w
+// of it every fourth of them, starting at the w-th; per chunk every lane loads its share of the keys and values (16-byte
 // vectors, the next chunk's loads in flight while the current one is used), forms phi(k) in
 // fp32 (accumulating its part of z), and writes phi(k)^T and v^T (bf16) into the wave's LDS
 // area, from which the MFMA operands are read: S[i][j] += sum over 16 keys of
 // phi(k)^T[i][t] v^T[j][t].  The four waves' partial sums meet in LDS at the end, added in
-// wave order.
+// wave order.  With nsplit > 1 each split writes its partial state to its own slot of St
+// ([B][H][nsplit][dh + 1][dh]) and k_lin_merge adds the splits in order.
 // ------------------------------------------------------------------------------------------
 template <int DH>
 __global__ __launch_bounds__(256) void k_lin_state_bf16(const bf16* __restrict__ K, const bf16* __restrict__ V,
                                                         long long bs, int rs, int nk, const int32_t* __restrict__ nvalid,
-                                                        int H, float* __restrict__ St) {
+                                                        int H, int nsplit, float* __restrict__ St) {
   constexpr int CH = 64, LDT = CH + 8, VPR = DH / 8, NV = CH * VPR / 64, NB = DH / 32;
   constexpr int AREA = 2 * DH * LDT;                       // bf16 elements per wave: phi(k)^T | v^T
   constexpr int RED = 4 * DH * DH;                         // floats of the cross-wave reduction
@@ -46,7 +50,7 @@ __global__ __launch_bounds__(256) void k_lin_state_bf16(const bf16* __restrict__
   __shared__ __attribute__((aligned(16))) char smem[BYTES];
   __shared__ float s_z[4][DH];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int bh = xcd_tile(blockIdx.x, gridDim.x), b = bh / H, h = bh % H;
+  const int id = xcd_tile(blockIdx.x, gridDim.x), bh = id / nsplit, sp = id % nsplit, b = bh / H, h = bh % H;
   const int n = nvalid ? min(nk, nvalid[b]) : nk;
   bf16* fkT = reinterpret_cast<bf16*>(smem) + wave * AREA;   // [DH][LDT]
   bf16* vT = fkT + DH * LDT;                                  // [DH][LDT]
@@ -61,7 +65,8 @@ __global__ __launch_bounds__(256) void k_lin_state_bf16(const bf16* __restrict__
   for (int ib = 0; ib < NB; ++ib)
 #pragma unroll
     for (int jb = 0; jb < NB; ++jb) acc[ib][jb] = f32x16{};
-  const int nch = (n + CH - 1) / CH;
+  const int nall = (n + CH - 1) / CH, cps = (nall + nsplit - 1) / nsplit;
+  const int ch0 = min(nall, sp * cps), nch = min(nall, ch0 + cps);   // this split's chunks [ch0, nch)
   bf16x8 kr[NV], vr[NV];
   auto load = [&](int ch) {
 #pragma unroll
@@ -75,8 +80,8 @@ __global__ __launch_bounds__(256) void k_lin_state_bf16(const bf16* __restrict__
       }
     }
   };
-  if (wave < nch) load(wave);
-  for (int ch = wave; ch < nch; ch += 4) {
+  if (ch0 + wave < nch) load(ch0 + wave);
+  for (int ch = ch0 + wave; ch < nch; ch += 4) {
     // phi(k) and v of this chunk -> transposed LDS operands; keys past n are zero rows
 #pragma unroll
     for (int p = 0; p < NV; ++p) {
@@ -129,7 +134,7 @@ __global__ __launch_bounds__(256) void k_lin_state_bf16(const bf16* __restrict__
           red[(wave * DH + i) * DH + j] = acc[ib][jb][4 * q + e];
         }
   __syncthreads();
-  float* out = St + (long long)bh * (DH + 1) * DH;
+  float* out = St + ((long long)bh * nsplit + sp) * (DH + 1) * DH;
   for (int x = threadIdx.x; x < DH * DH; x += 256)
     out[x] = ((red[x] + red[DH * DH + x]) + red[2 * DH * DH + x]) + red[3 * DH * DH + x];
   if (threadIdx.x < DH) {
@@ -157,6 +162,18 @@ __global__ __launch_bounds__(256) void k_lin_state_f32(const float* __restrict__
       for (int t = 0; t < n; ++t) s += phi(Kb[(long long)t * rs + j]);
     }
     out[x] = s;
+  }
+}
+
+// The splits' partial states added in split order: St[bh][x] = sum_sp part[bh][sp][x].
+__global__ __launch_bounds__(256) void k_lin_merge(const float* __restrict__ part, int nsplit, long long per_bh,
+                                                  long long total, float* __restrict__ St) {
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    const long long bh = i / per_bh, x = i - bh * per_bh;
+    const float* p = part + bh * nsplit * per_bh + x;
+    float s = p[0];
+    for (int sp = 1; sp < nsplit; ++sp) s += p[sp * per_bh];
+    St[i] = s;
   }
 }
 
@@ -231,17 +248,34 @@ void apply_as(const void* Q, int q_rs, const float* St, int B, int rpb, const in
 
 }  // namespace
 
+int lin_state_splits(int BH, int nk, bool bf16_model) {
+  if (!bf16_model || BH <= 0) return 1;
+  // enough workgroups to fill the chip (about four per compute unit), at least one 64-key chunk
+  // per wave of each split
+  const int chunks = (nk + 63) / 64;
+  const int want = (1024 + BH - 1) / BH, most = chunks / 4;
+  return std::max(1, std::min(want, most));
+}
+
 hipError_t launch_lin_state(const void* K, const void* V, long long bs, int rs, int B, int nk, const int32_t* nvalid,
-                            int H, int dh, float* St, bool bf16_model, hipStream_t s) {
+                            int H, int dh, float* St, bool bf16_model, hipStream_t s, float* part) {
   if (B <= 0 || nk <= 0) return hipSuccess;
   if (bf16_model) {
     if ((rs % 8) || (bs % 8)) return hipErrorInvalidValue;   // 16-byte row vectors
+    const int ns = part ? lin_state_splits(B * H, nk, true) : 1;
+    float* dst = ns > 1 ? part : St;
+    const dim3 grid((unsigned)(B * H * ns));
     switch (dh) {
-      case 32: hipLaunchKernelGGL(k_lin_state_bf16<32>, dim3(B * H), dim3(256), 0, s, static_cast<const bf16*>(K),
-                                  static_cast<const bf16*>(V), bs, rs, nk, nvalid, H, St); break;
-      case 64: hipLaunchKernelGGL(k_lin_state_bf16<64>, dim3(B * H), dim3(256), 0, s, static_cast<const bf16*>(K),
-                                  static_cast<const bf16*>(V), bs, rs, nk, nvalid, H, St); break;
+      case 32: hipLaunchKernelGGL(k_lin_state_bf16<32>, grid, dim3(256), 0, s, static_cast<const bf16*>(K),
+                                  static_cast<const bf16*>(V), bs, rs, nk, nvalid, H, ns, dst); break;
+      case 64: hipLaunchKernelGGL(k_lin_state_bf16<64>, grid, dim3(256), 0, s, static_cast<const bf16*>(K),
+                                  static_cast<const bf16*>(V), bs, rs, nk, nvalid, H, ns, dst); break;
       default: return hipErrorInvalidValue;
+    }
+    if (ns > 1) {
+      const long long per_bh = (long long)(dh + 1) * dh, total = (long long)B * H * per_bh;
+      const int blocks = (int)std::min<long long>((total + 255) / 256, 4096);
+      hipLaunchKernelGGL(k_lin_merge, dim3(blocks), dim3(256), 0, s, part, ns, per_bh, total, St);
     }
   } else {
     hipLaunchKernelGGL(k_lin_state_f32, dim3(B * H), dim3(256), 0, s, static_cast<const float*>(K),
