@@ -164,7 +164,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention(AttnArgs a) {
 // transposed score / probability / output scheme as above.
 // ------------------------------------------------------------------------------------------
 template <int DH, int WAVES, int QT, int KC>
-__global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
+__global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 3 : 1) void k_attention_chunked(AttnArgs a) {
   constexpr int NT = WAVES * 64;
   constexpr int KLD = DH + 8, VLD = KC + 8, NB = DH / 16;
   constexpr int PER_T = KC * DH / 8 / NT;         // 16-byte vectors per thread per tensor
@@ -231,54 +231,78 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention_chunked(AttnArgs a) {
     if (c0 + KC < nk) load_chunk(c0 + KC);
     const int nkeys = min(KC, nk - c0);
 
+    // 64 keys (two 32-key blocks; 32 for 32-key chunks) per online-softmax step; every key and value fragment of them
+    // is read from LDS once and used by all QT query tiles of the wave.  Keys from nkeys on
+    // (zero rows in LDS, up to KC) are masked.
+    constexpr int NU = (KC >= 64 && QT >= 2) ? 2 : 1;   // 32-key blocks per step
+    static_assert(KC % (32 * NU) == 0, "whole steps per chunk");
+    for (int kb = 0; kb < nkeys; kb += 32 * NU) {
+      const int r = lane & 15;
+      bf16x8 ka[NU][DH / 32], kc[NU][DH / 32], vf[NU][NB];
 #pragma unroll
-    for (int t = 0; t < QT; ++t) {
-      if (q0_of(t) >= nq) continue;
-      for (int kb = 0; kb < nkeys; kb += 32) {
-        const int r = lane & 15;
-        const int k0 = kb + (r >> 2) * 8 + (r & 3), k1 = k0 + 4;
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      for (int u = 0; u < NU; ++u) {
+        const int k0 = kb + 32 * u + (r >> 2) * 8 + (r & 3), k1 = k0 + 4;
 #pragma unroll
         for (int c = 0; c < DH / 32; ++c) {
-          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&Ks[k0 * KLD + c * 32 + g * 8]);
-          const bf16x8 kb8 = *reinterpret_cast<const bf16x8*>(&Ks[k1 * KLD + c * 32 + g * 8]);
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[t][c], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qf[t][c], s1, 0, 0, 0);
+          ka[u][c] = *reinterpret_cast<const bf16x8*>(&Ks[k0 * KLD + c * 32 + g * 8]);
+          kc[u][c] = *reinterpret_cast<const bf16x8*>(&Ks[k1 * KLD + c * 32 + g * 8]);
         }
-        float p[8];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          p[j] = s0[j] * sl2;
-          p[4 + j] = s1[j] * sl2;
-        }
-        if (kb + 32 > nkeys) {                      // ragged last block (uniform branch)
+        for (int i = 0; i < NB; ++i)
+          vf[u][i] = *reinterpret_cast<const bf16x8*>(&Vt[(i * 16 + (lane & 15)) * VLD + kb + 32 * u + g * 8]);
+      }
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        if (q0_of(t) >= nq) continue;               // uniform
+        float p[NU][8];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+          f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int c = 0; c < DH / 32; ++c) {
+            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[u][c], qf[t][c], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[u][c], qf[t][c], s1, 0, 0, 0);
+          }
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            if (kb + g * 8 + j >= nkeys) p[j] = -INFINITY;
-            if (kb + g * 8 + 4 + j >= nkeys) p[4 + j] = -INFINITY;
+            p[u][j] = s0[j] * sl2;
+            p[u][4 + j] = s1[j] * sl2;
           }
         }
-        float mx = p[0];
+        if (kb + 32 * NU > nkeys) {                 // ragged last step (uniform branch)
 #pragma unroll
-        for (int j = 1; j < 8; ++j) mx = fmaxf(mx, p[j]);
+          for (int u = 0; u < NU; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              if (kb + 32 * u + g * 8 + j >= nkeys) p[u][j] = -INFINITY;
+              if (kb + 32 * u + g * 8 + 4 + j >= nkeys) p[u][4 + j] = -INFINITY;
+            }
+        }
+        float mx = p[0][0];
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) mx = fmaxf(mx, p[u][j]);
         mx = rows_max(mx);
-        const float m_new = fmaxf(m_run[t], mx);   // finite: every key block holds a valid key
+        const float m_new = fmaxf(m_run[t], mx);   // finite: every step holds a valid key
         const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);   // v_exp_f32; exp2(-inf) = 0
         float psum = 0.f;
-        bf16x8 pb;
+        bf16x8 pb[NU];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float e = __builtin_amdgcn_exp2f(p[j] - m_new);
-          psum += e;
-          pb[j] = (bf16)e;
-        }
+        for (int u = 0; u < NU; ++u)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float e = __builtin_amdgcn_exp2f(p[u][j] - m_new);
+            psum += e;
+            pb[u][j] = (bf16)e;
+          }
         l_run[t] = l_run[t] * alpha + psum;
         m_run[t] = m_new;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
           o[t][i] *= alpha;
-          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vt[(i * 16 + (lane & 15)) * VLD + kb + g * 8]);
-          o[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[t][i], 0, 0, 0);
+#pragma unroll
+          for (int u = 0; u < NU; ++u) o[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[u][i], pb[u], o[t][i], 0, 0, 0);
         }
       }
     }
