@@ -44,15 +44,16 @@ def _compare_request(cfg, W, out, ref, b, check_kv=True):
     return check_scores(cfg, out["scores"][b], out["best"][b], ref["scores"], b)
 
 
-def check_whole_batch(c, out):
-    """Every request of a full-size batch against the cached-order oracle (stage by stage,
-    element by element); prints the measured worst error ratios and the fraction of requests in
-    the exact-selection regime."""
+def check_whole_batch(c, out, requests=None):
+    """Every request of a full-size batch (or the listed ones) against the cached-order oracle
+    (stage by stage, element by element); prints the measured worst error ratios and the fraction
+    of requests in the exact-selection regime."""
     tol = rtol_for(c)
     worst = {k: 0.0 for k in ("kv", "H", "seq", "Cp", "scores")}
     strict = 0
-    for r in compare_batch(c, out):
-        b = r["b"]
+    n = 0
+    for r in compare_batch(c, out, requests):
+        b, n = r["b"], n + 1
         assert r["n_uniq_ok"] and r["uniq_ok"] and r["slot_ok"], (c.label, b, "distinct set or slots differ")
         assert r["H_pad_zero"], (c.label, b, "padding rows of H are not zero")
         for k in ("H", "seq", "Cp"):
@@ -65,9 +66,9 @@ def check_whole_batch(c, out):
         worst["scores"] = max(worst["scores"], m["ratio"])
         strict += m["strict"]
     assert np.all(out["status"] == 0)
-    print(f"\n[parity] {c.label}: {c.B} requests; worst normwise error " +
+    print(f"\n[parity] {c.label}: {n} of {c.B} requests; worst normwise error " +
           ", ".join(f"{k} {v:.3g}" for k, v in worst.items()) +
-          f"; exact-selection regime {strict}/{c.B}", flush=True)
+          f"; exact-selection regime {strict}/{n}", flush=True)
     return worst, strict
 
 
@@ -140,6 +141,15 @@ def test_cfg4_text_hypotheses():
     W, I = gen.make_weights(c), gen.make_inputs(c)
     out = run_pass(c, W, I)
     check_whole_batch(c, out)
+
+
+def test_wide_heads_two_query_tiles_per_wave():
+    """Head width 64 with 128 (request, head) pairs of 1024 queries: the chunked attention puts
+    two query tiles on each wave (text-hypothesis shapes at 16 requests; first and last request)."""
+    c = gen.config(4, B=16)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    check_whole_batch(c, out, requests=[0, c.B - 1])
 
 
 # ------------------------------------------------------------------------- stage-isolated parity
