@@ -388,11 +388,12 @@ def assemble_entry(c, U, ev, bufs, stream):
                                "what": "torch copy_ of a tensor the size of seq (read + write), timed the same way"}}
 
 
-def workload_entry(c, steps: int, warmup: int, trace: bool = True):
-    """One workload's pass on this GPU: time per batch (events over `steps` back-to-back passes),
-    lists/s, the measured distinct-element counts, the item stage (fe_encode_items) timed alone, the
-    assembly against its write-only floor, and the dominant matrix-product kernel family with its
-    TFLOP/s (per-launch trace times scaled to the untraced pass)."""
+def workload_entry(c, steps: int, warmup: int, trace: bool = True, cpu_seconds: float = 0.0):
+    """One workload's pass on this GPU: time per batch (events over `steps` back-to-back passes) and
+    its median over per-pass events, lists/s, the measured distinct-element counts, the item stage
+    (fe_encode_items) timed alone, the assembly against its write-only floor, the dominant
+    matrix-product kernel family with its TFLOP/s (per-launch trace times scaled to the untraced
+    pass), and with `cpu_seconds` > 0 the oracle timed on the same workload."""
     import numpy as np
     import torch
     import gen
@@ -413,13 +414,21 @@ def workload_entry(c, steps: int, warmup: int, trace: bool = True):
         ev.run(x=x, ctx_ids=ids, pool=pool, lists=lists)
 
     ms = time_pass(step, stream, steps, warmup)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record(stream)
+    for i in range(steps):
+        step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    p50 = float(np.median([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]))
     U = b["n_uniq"].cpu().numpy().tolist()
     items_us = time_pass(lambda: fe.fe_encode_items(ev.handle, c.B, c.M, pool, lists, c.K, c.L, b["kv"], c.T, b["uniq"],
                                                     b["n_uniq"], b["slot"], b["H"], b["ws"]),
                          stream, steps, warmup) * 1e3
     entry = {"workload": c.label, "B": c.B, "T": c.T, "d": c.d, "K": c.K, "L": c.L, "M": c.M,
              "attention": c.attention, "lists_per_batch": c.B * c.K, "ms_per_batch": round(ms, 5),
-             "lists_per_s": round(c.B * c.K / (ms / 1e3), 1), "U_mean": round(float(np.mean(U)), 2),
+             "lists_per_s": round(c.B * c.K / (ms / 1e3), 1), "p50_ms": round(p50, 5),
+             "U_mean": round(float(np.mean(U)), 2),
              "rho": round(c.K * c.L / float(np.mean(U)), 3), "item_stage_us": round(items_us, 2),
              "assemble": assemble_entry(c, U, ev, b, stream)}
     if trace:
@@ -443,6 +452,8 @@ def workload_entry(c, steps: int, warmup: int, trace: bool = True):
                                         "mfma_frac": round(tf / peak, 4), "share_of_pass": round(t_ms / ms, 4)}
             mm_ms = sum(v[0] for v in mm.values()) / steps * scale
             entry["mfma_util_matrix_stages"] = round(sum(flops[k] for k in mm) / (mm_ms / 1e3) / 1e12 / peak, 4)
+    if cpu_seconds > 0:
+        entry["cpu_baseline"] = cpu_baseline(c, W, I, cpu_seconds)
     ev.close()
     del bufs, x, pool, ids, lists
     torch.cuda.empty_cache()
@@ -484,6 +495,9 @@ def main() -> int:
                     help="skip timing the pass without cross-sequence interaction (for profiler runs)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the K sweep and the long-context / text-hypothesis workloads after the headline run")
+    ap.add_argument("--cpu-all", action="store_true",
+                    help="also time the oracle (candidate-factorised order, --cpu-seconds each) on every K-sweep "
+                         "and long-context / text-hypothesis workload")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB copy (to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -786,10 +800,12 @@ def main() -> int:
         ev.close()
         del bufs
         torch.cuda.empty_cache()
-        out["k_sweep"] = [workload_entry(gen.config(2, K=k), n_steps, 5, trace=not args.no_trace) for k in gen.K_SWEEP]
-        out["workloads"] = [workload_entry(gen.config(3), n_steps, 5, trace=not args.no_trace),
+        cs = args.cpu_seconds if args.cpu_all else 0.0
+        out["k_sweep"] = [workload_entry(gen.config(2, K=k), n_steps, 5, trace=not args.no_trace, cpu_seconds=cs)
+                          for k in gen.K_SWEEP]
+        out["workloads"] = [workload_entry(gen.config(3), n_steps, 5, trace=not args.no_trace, cpu_seconds=cs),
                             workload_entry(gen.config(3, attention="linear"), n_steps, 5, trace=not args.no_trace),
-                            workload_entry(gen.config(4), n_steps, 5, trace=not args.no_trace)]
+                            workload_entry(gen.config(4), n_steps, 5, trace=not args.no_trace, cpu_seconds=cs)]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(c, W, I, args.cpu_seconds)
         out["cpu_baseline"]["joint_order"] = cpu_cached(c, W, I, args.cpu_seconds / 3)
