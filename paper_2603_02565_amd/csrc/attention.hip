@@ -164,7 +164,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_attention(AttnArgs a) {
 // transposed score / probability / output scheme as above.
 // ------------------------------------------------------------------------------------------
 template <int DH, int WAVES, int QT, int KC>
-__global__ __launch_bounds__(WAVES * 64, WAVES != 4 ? 1 : DH == 64 && QT >= 2 ? 2 : 3) void k_attention_chunked(AttnArgs a) {
+__global__ __launch_bounds__(WAVES * 64, WAVES != 4 ? 1 : (DH == 64 && QT >= 2) || QT >= 8 ? 2 : 3) void k_attention_chunked(AttnArgs a) {
   constexpr int NT = WAVES * 64;
   constexpr int KLD = DH + 8, VLD = KC + 8, NB = DH / 16;
   constexpr int PER_T = KC * DH / 8 / NT;         // 16-byte vectors per thread per tensor
@@ -480,13 +480,16 @@ hipError_t launch_bf16(const AttnArgs& a, hipStream_t s) {
     // tiny groups (sequence encoder): one wave per (group, head)
     return a.nk <= 32 ? launch_chunked<DH, 1, 1, 32>(a, s) : launch_chunked<DH, 1, 1, 128>(a, s);
   }
-  // as many queries per workgroup as keep >= 1024 workgroups (four per compute unit, so each
-  // SIMD has several waves to switch between), so K/V chunks are still shared widely
+  // as many queries per workgroup as still fill the chip, so K/V chunks are shared widely: eight
+  // 32-dim query tiles per wave when that makes >= 512 workgroups (two per compute unit, by the
+  // variant's registers), four or two when >= 1024 (three per compute unit); two 64-dim tiles
+  // when >= 1024 (four would not fit the register file)
   const long long bh = (long long)a.n_heads * a.B;
   auto wgs = [&](int qt) { return (a.nq + 64 * qt - 1) / (64 * qt) * bh; };
-  // (four 64-dim query tiles per wave would not fit the register file without spilling)
-  if constexpr (DH == 32)
+  if constexpr (DH == 32) {
+    if (wgs(8) >= 512) return launch_chunked<DH, 4, 8, 128>(a, s);
     if (wgs(4) >= 1024) return launch_chunked<DH, 4, 4, 128>(a, s);
+  }
   if (wgs(2) >= 1024) return launch_chunked<DH, 4, 2, 128>(a, s);
   return launch_chunked<DH, 4, 1, 128>(a, s);
 }

@@ -143,6 +143,16 @@ def test_cfg4_text_hypotheses():
     check_whole_batch(c, out)
 
 
+def test_long_context_ragged_query_groups():
+    """Head width 32, 2000 context rows over 128 (request, head) pairs: the chunked attention puts
+    eight query tiles on each wave and the last query group of every pair is ragged (first and last
+    request)."""
+    c = gen.config(3, T=2000)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    check_whole_batch(c, out, requests=[0, c.B - 1])
+
+
 def test_wide_heads_two_query_tiles_per_wave():
     """Head width 64 with 128 (request, head) pairs of 1024 queries: the chunked attention puts
     two query tiles on each wave (text-hypothesis shapes at 16 requests; first and last request)."""
