@@ -30,6 +30,7 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12     # dense bf16 matrix-core peak, 
 PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 ASM_REPS = 100           # assembly launches per captured graph (gather-stage timing)
+PIPE_STREAMS = 3         # batches in flight in the pipelined executor (one buffer set each)
 
 
 def assemble_bytes(c, U):
@@ -414,6 +415,29 @@ def workload_entry(c, steps: int, warmup: int, trace: bool = True, cpu_seconds: 
         ev.run(x=x, ctx_ids=ids, pool=pool, lists=lists)
 
     ms = time_pass(step, stream, steps, warmup)
+    sets = [b] + [ev.allocate(c.B, c.T, c.M, c.K, c.L) for _ in range(PIPE_STREAMS - 1)]
+    ex = fe.Executor(ev, PIPE_STREAMS)
+    n_sub = [0]
+
+    def submit():
+        ex.submit(sets[n_sub[0] % PIPE_STREAMS], x=x, ctx_ids=ids, pool=pool, lists=lists)
+        n_sub[0] += 1
+
+    for _ in range(max(warmup, PIPE_STREAMS)):
+        submit()
+    ex.join()
+    torch.cuda.synchronize()
+    q0, q1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    q0.record(stream)
+    for _ in range(steps):
+        submit()
+    ex.join()
+    q1.record(stream)
+    torch.cuda.synchronize()
+    pipe_ms = q0.elapsed_time(q1) / steps
+    ex.close()
+    del sets
+    ev.buffers = b
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     evs[0].record(stream)
     for i in range(steps):
@@ -428,6 +452,8 @@ def workload_entry(c, steps: int, warmup: int, trace: bool = True, cpu_seconds: 
     entry = {"workload": c.label, "B": c.B, "T": c.T, "d": c.d, "K": c.K, "L": c.L, "M": c.M,
              "attention": c.attention, "lists_per_batch": c.B * c.K, "ms_per_batch": round(ms, 5),
              "lists_per_s": round(c.B * c.K / (ms / 1e3), 1), "p50_ms": round(p50, 5),
+             "pipelined": {"streams": PIPE_STREAMS, "ms_per_batch": round(pipe_ms, 5),
+                           "lists_per_s": round(c.B * c.K / (pipe_ms / 1e3), 1)},
              "U_mean": round(float(np.mean(U)), 2),
              "rho": round(c.K * c.L / float(np.mean(U)), 3), "item_stage_us": round(items_us, 2),
              "assemble": assemble_entry(c, U, ev, b, stream)}
@@ -538,20 +564,44 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
 
-    # ---- timed region: K whole passes, an event between consecutive passes
+    # ---- one stream: K whole passes back to back, an event between consecutive passes (the
+    # latency of one batch, and the throughput when batches are not overlapped)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     evs[0].record(stream)
     for i in range(args.steps):
         step()
         evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
-    total_ms = evs[0].elapsed_time(evs[-1])
-    ms_per_step = total_ms / args.steps
+    single_ms = evs[0].elapsed_time(evs[-1]) / args.steps
+
+    # ---- timed region: K whole passes, each over the full batch, through the pipelined executor
+    # (PIPE_STREAMS batches in flight on the library's streams, one buffer set per stream)
+    pipe_sets = [bufs] + [ev.allocate(c.B, c.T, c.M, c.K, c.L) for _ in range(PIPE_STREAMS - 1)]
+    ex = fe.Executor(ev, PIPE_STREAMS)
+
+    def submit(i):
+        ex.submit(pipe_sets[i % PIPE_STREAMS], x=x, ctx_ids=ids, pool=pool, lists=lists)
+
+    for i in range(max(args.warmup, PIPE_STREAMS)):
+        submit(i)
+    ex.join()
+    torch.cuda.synchronize()
+    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    p0.record(stream)
+    for i in range(args.steps):
+        submit(i)
+    ex.join()
+    p1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = p0.elapsed_time(p1) / args.steps
     lists_per_s = c.B * c.K / (ms_per_step / 1e3)
+    ex.close()
+    del pipe_sets
+    ev.buffers = bufs
 
     U = bufs["n_uniq"].cpu().numpy().tolist()
     asm_bytes = assemble_bytes(c, U)
@@ -651,6 +701,11 @@ def main() -> int:
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "pipelined": {"streams": PIPE_STREAMS,
+                      "what": "value and ms_per_step: K passes (each over the whole batch, B requests) submitted "
+                              "round-robin to fe_executor streams, one buffer set per stream, timed between two "
+                              "events around all K; p50/p90: per-pass latency of the same pass alone on one stream"},
+        "single_stream": {"ms_per_step": round(single_ms, 5), "value": round(c.B * c.K / (single_ms / 1e3), 1)},
         "without_cross_sequence": None if no_cross_ms is None else {
             "ms_per_step": round(no_cross_ms, 5), "value": round(c.B * c.K / (no_cross_ms / 1e3), 1)},
         "graph_replay": None if graph_ms is None else {"ms_per_step": round(graph_ms, 5),

@@ -28,7 +28,10 @@
  *     Scratch memory is the caller's workspace (size from fe_workspace_size).
  *   - Calls are asynchronous on `stream` (a hipStream_t, NULL = default
  *     stream) and return once their kernels are enqueued.  One workspace must
- *     not be used by two streams at the same time.
+ *     not be used by two streams at the same time.  The model is read-only
+ *     after creation: calls on different streams may run concurrently on one
+ *     model when they share no output and no workspace (fe_executor_* below
+ *     orders whole passes that way).
  *   - Tensors are dense and row-major with the model width d innermost.  Head
  *     h of an attention module owns columns h*dh .. h*dh+dh-1, dh = d/n_heads.
  *   - "act" is the model's activation type: float (FE_F32) or bfloat16
@@ -301,6 +304,55 @@ fe_status fe_naive_workspace_size(const fe_model* m, int B, int T, int M, int K,
 fe_status fe_evaluate_naive(const fe_model* m, int B, int T, int M, int K, int L, const void* x,
                             const int32_t* ctx_ids, const void* pool, const int32_t* lists, float* Cp,
                             float* scores, int32_t* best, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Pipelined executor for serving many batches: not a step of the method, it orders the five
+ * calls of independent batches on several streams so that their kernels share the GPU.  At
+ * serving batch sizes the pass's kernels are latency-bound (one workgroup per compute unit and
+ * long dependent chains inside each), so a second or third batch in flight fills compute units
+ * that one batch leaves idle.
+ *
+ * fe_executor_create: n_streams (1 .. FE_EXECUTOR_MAX_STREAMS) HIP streams on the model's device,
+ *   non-blocking and at the default priority, with two events each.  Allocates no device memory.
+ *   Call with the model's device current.
+ * fe_executor_submit: one whole pass -- fe_encode_context, fe_encode_items, fe_assemble,
+ *   fe_cross_sequence and fe_score_select with the arguments in `p` -- on the executor's next
+ *   stream in round-robin order, after that stream has waited for the work enqueued so far on
+ *   `stream` (the caller's stream, NULL = default, whose work produced the inputs).  Returns once
+ *   the kernels are enqueued.  The whole pass is validated first, with the rules of the five
+ *   calls (p->ws_bytes >= fe_workspace_size(B, T, M, K, L)); on a non-OK status nothing was
+ *   enqueued.  A submission must not share any output (kv, uniq, n_uniq, slot, H, seq, Cp,
+ *   scores, best) or the workspace with a submission still in flight; one buffer set per stream,
+ *   submission i using set i mod n_streams, satisfies this.  Inputs may be shared.
+ * fe_executor_join: makes `stream` wait (on the device) for every pass submitted so far; the
+ *   outputs are valid for work enqueued on `stream` after it.
+ * fe_executor_destroy: waits on the host for the submitted passes, then releases the streams and
+ *   events.  One executor must not be used by two host threads at once.
+ */
+#define FE_EXECUTOR_MAX_STREAMS 8
+typedef struct fe_executor fe_executor; /* opaque */
+typedef struct {
+  int B, T, M, K, L;
+  const void* x;          /* [B][T][d] act, or NULL when ctx_ids is given */
+  const int32_t* ctx_ids; /* [B][T] int32, or NULL when x is given */
+  const void* pool;       /* [B][M][d] act, or NULL on a vocabulary model */
+  const int32_t* lists;   /* [B][K][L] int32 */
+  void* kv;               /* fe_kv_size bytes */
+  int32_t* uniq;          /* [B][U_cap] */
+  int32_t* n_uniq;        /* [B] */
+  int32_t* slot;          /* [B][K][L] */
+  void* H;                /* [B][U_cap][d] act */
+  void* seq;              /* [B][K][L+1][d] act */
+  float* Cp;              /* [B][K][d] */
+  float* scores;          /* [B][K] */
+  int32_t* best;          /* [B] */
+  void* ws;
+  size_t ws_bytes;
+} fe_pass_args;
+fe_status fe_executor_create(const fe_model* m, int n_streams, fe_executor** out);
+fe_status fe_executor_submit(fe_executor* ex, const fe_pass_args* p, void* stream);
+fe_status fe_executor_join(fe_executor* ex, void* stream);
+void fe_executor_destroy(fe_executor* ex);
 
 #ifdef __cplusplus
 }

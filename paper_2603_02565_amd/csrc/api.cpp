@@ -1229,4 +1229,97 @@ fe_status fe_evaluate_naive(const fe_model* m, int B, int T, int M, int K, int L
   return fe_score_select(m, B, K, Cp, scores, best, stream);
 }
 
+// ------------------------------------------------------------------------------------------
+// Pipelined executor: whole passes of independent batches round-robin over its own streams
+// ------------------------------------------------------------------------------------------
+struct fe_executor {
+  const fe_model* m;
+  int n = 0, next = 0;
+  hipStream_t streams[FE_EXECUTOR_MAX_STREAMS] = {};
+  hipEvent_t ready[FE_EXECUTOR_MAX_STREAMS] = {};   // the caller's stream at a submission
+  hipEvent_t done[FE_EXECUTOR_MAX_STREAMS] = {};    // stream i after its last pass
+  bool used[FE_EXECUTOR_MAX_STREAMS] = {};
+};
+
+static void executor_release(fe_executor* ex) {
+  for (int i = 0; i < FE_EXECUTOR_MAX_STREAMS; ++i) {
+    if (ex->streams[i]) (void)hipStreamSynchronize(ex->streams[i]);
+    if (ex->ready[i]) (void)hipEventDestroy(ex->ready[i]);
+    if (ex->done[i]) (void)hipEventDestroy(ex->done[i]);
+    if (ex->streams[i]) (void)hipStreamDestroy(ex->streams[i]);
+  }
+  delete ex;
+}
+
+fe_status fe_executor_create(const fe_model* m, int n_streams, fe_executor** out) {
+  if (!m || !out) return fail(FE_EINVAL, "NULL argument");
+  *out = nullptr;
+  if (n_streams < 1 || n_streams > FE_EXECUTOR_MAX_STREAMS)
+    return fail(FE_EINVAL, "n_streams %d outside 1..%d", n_streams, FE_EXECUTOR_MAX_STREAMS);
+  fe_executor* ex = new (std::nothrow) fe_executor;
+  if (!ex) return fail(FE_EINVAL, "out of host memory");
+  ex->m = m;
+  ex->n = n_streams;
+  for (int i = 0; i < n_streams; ++i) {
+    if (hipStreamCreateWithFlags(&ex->streams[i], hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&ex->ready[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ex->done[i], hipEventDisableTiming) != hipSuccess) {
+      const hipError_t e = hipGetLastError();
+      executor_release(ex);
+      return fail(FE_EHIP, "stream or event creation failed: %s", hipGetErrorString(e));
+    }
+  }
+  *out = ex;
+  return FE_OK;
+}
+
+fe_status fe_executor_submit(fe_executor* ex, const fe_pass_args* p, void* stream) {
+  if (!ex || !p) return fail(FE_EINVAL, "NULL argument");
+  const fe_model* m = ex->m;
+  // the whole pass is checked before anything is enqueued, with the rules of the five calls
+  fe_status st = check_dims(m, p->B, p->T, p->M, p->K, p->L);
+  if (st != FE_OK) return st;
+  if ((p->x == nullptr) == (p->ctx_ids == nullptr)) return fail(FE_EINVAL, "give exactly one of x and ctx_ids");
+  if (p->ctx_ids && !m->emb) return fail(FE_EINVAL, "ctx_ids given but the model has no vocabulary");
+  if (!p->pool && !m->emb) return fail(FE_EINVAL, "pool is NULL and the model has no vocabulary");
+  if (!p->pool && p->M != m->cfg.vocab) return fail(FE_EINVAL, "token-id items need M == vocab (%d)", m->cfg.vocab);
+  if (!p->lists || !p->kv || !p->uniq || !p->n_uniq || !p->slot || !p->H || !p->seq || !p->Cp || !p->scores ||
+      !p->best || !p->ws)
+    return fail(FE_EINVAL, "NULL pointer argument");
+  if (!aligned16(p->x) || !aligned16(p->ctx_ids) || !aligned16(p->pool) || !aligned16(p->lists) ||
+      !aligned16(p->kv) || !aligned16(p->uniq) || !aligned16(p->slot) || !aligned16(p->H) || !aligned16(p->seq) ||
+      !aligned16(p->Cp) || !aligned16(p->ws))
+    return fail(FE_EINVAL, "pointers must be 16-byte aligned");
+  const Ws w = layout(m, p->B, p->T, p->M, p->K, p->L);
+  if (p->ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", p->ws_bytes, w.total);
+  const int i = ex->next;
+  hipStream_t s = ex->streams[i];
+  FE_HIP(hipEventRecord(ex->ready[i], static_cast<hipStream_t>(stream)));
+  FE_HIP(hipStreamWaitEvent(s, ex->ready[i], 0));
+  const int U_cap = std::min(p->M, p->K * p->L);
+  st = fe_encode_context(m, p->B, p->T, p->x, p->ctx_ids, p->kv, p->ws, p->ws_bytes, s);
+  if (st == FE_OK)
+    st = fe_encode_items(m, p->B, p->M, p->pool, p->lists, p->K, p->L, p->kv, p->T, p->uniq, p->n_uniq, p->slot, p->H,
+                         p->ws, p->ws_bytes, s);
+  if (st == FE_OK) st = fe_assemble(m, p->B, p->K, p->L, U_cap, p->slot, p->H, p->seq, s);
+  if (st == FE_OK) st = fe_cross_sequence(m, p->B, p->K, p->L, p->seq, p->Cp, p->ws, p->ws_bytes, s);
+  if (st == FE_OK) st = fe_score_select(m, p->B, p->K, p->Cp, p->scores, p->best, s);
+  if (st != FE_OK) return st;
+  FE_HIP(hipEventRecord(ex->done[i], s));
+  ex->used[i] = true;
+  ex->next = (i + 1) % ex->n;
+  return FE_OK;
+}
+
+fe_status fe_executor_join(fe_executor* ex, void* stream) {
+  if (!ex) return fail(FE_EINVAL, "NULL argument");
+  for (int i = 0; i < ex->n; ++i)
+    if (ex->used[i]) FE_HIP(hipStreamWaitEvent(static_cast<hipStream_t>(stream), ex->done[i], 0));
+  return FE_OK;
+}
+
+void fe_executor_destroy(fe_executor* ex) {
+  if (ex) executor_release(ex);
+}
+
 }  // extern "C"

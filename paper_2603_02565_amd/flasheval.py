@@ -26,7 +26,9 @@ LOSS_KIND = {"mse": FE_LOSS_MSE, "bce": FE_LOSS_BCE, "ce": FE_LOSS_CE}
 EXPORTED = ("fe_param_count", "fe_model_create", "fe_model_destroy", "fe_workspace_size", "fe_kv_size", "fe_last_error",
             "fe_read_device_status", "fe_encode_context", "fe_encode_items", "fe_assemble", "fe_cross_sequence",
             "fe_cross_sequence_noalloc", "fe_score_select", "fe_encode_sequences", "fe_score_objectives", "fe_naive_workspace_size", "fe_evaluate_naive", "fe_trace_enable", "fe_trace_read",
-            "fe_trace_read_launches", "fe_trace_family", "fe_train_workspace_size", "fe_train_grads")
+            "fe_trace_read_launches", "fe_trace_family", "fe_train_workspace_size", "fe_train_grads",
+            "fe_executor_create", "fe_executor_submit", "fe_executor_join", "fe_executor_destroy")
+FE_EXECUTOR_MAX_STREAMS = 8
 FE_TRACE_FAMILIES = 12
 
 
@@ -40,6 +42,15 @@ class fe_config(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_layers", ctypes.c_int32),
                 ("ffn_dim", ctypes.c_int32), ("max_L", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("attention", ctypes.c_int32)]
+
+
+class fe_pass_args(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("M", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("L", ctypes.c_int32), ("x", ctypes.c_void_p), ("ctx_ids", ctypes.c_void_p), ("pool", ctypes.c_void_p),
+                ("lists", ctypes.c_void_p), ("kv", ctypes.c_void_p), ("uniq", ctypes.c_void_p),
+                ("n_uniq", ctypes.c_void_p), ("slot", ctypes.c_void_p), ("H", ctypes.c_void_p), ("seq", ctypes.c_void_p),
+                ("Cp", ctypes.c_void_p), ("scores", ctypes.c_void_p), ("best", ctypes.c_void_p), ("ws", ctypes.c_void_p),
+                ("ws_bytes", ctypes.c_size_t)]
 
 
 _lib = None
@@ -80,6 +91,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "fe_trace_family": (ctypes.c_char_p, [I]),
         "fe_train_workspace_size": (S, [cfgp, I, I, I, I, I, ctypes.POINTER(Z)]),
         "fe_train_grads": (S, [cfgp, P, I, I, I, I, I, P, P, P, P, P, I, P, P, P, P, Z, P]),
+        "fe_executor_create": (S, [P, I, ctypes.POINTER(P)]),
+        "fe_executor_submit": (S, [P, ctypes.POINTER(fe_pass_args), P]),
+        "fe_executor_join": (S, [P, P]),
+        "fe_executor_destroy": (None, [P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -205,6 +220,28 @@ def fe_cross_sequence(model: int, B: int, K: int, L: int, seq, Cp, ws, stream=No
 
 
 FE_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def fe_executor_create(model: int, n_streams: int) -> int:
+    out = ctypes.c_void_p()
+    _check(load_library().fe_executor_create(model, n_streams, ctypes.byref(out)), "fe_executor_create")
+    return out.value
+
+
+def fe_executor_submit(ex: int, B: int, T: int, M: int, K: int, L: int, x, ctx_ids, pool, lists, kv, uniq, n_uniq,
+                       slot, H, seq, Cp, scores, best, ws, stream=None) -> None:
+    a = fe_pass_args(B, T, M, K, L, _ptr(x), _ptr(ctx_ids), _ptr(pool), _ptr(lists), _ptr(kv), _ptr(uniq),
+                     _ptr(n_uniq), _ptr(slot), _ptr(H), _ptr(seq), _ptr(Cp), _ptr(scores), _ptr(best), _ptr(ws),
+                     ws.numel() * ws.element_size())
+    _check(load_library().fe_executor_submit(ex, ctypes.byref(a), _stream(stream)), "fe_executor_submit")
+
+
+def fe_executor_join(ex: int, stream=None) -> None:
+    _check(load_library().fe_executor_join(ex, _stream(stream)), "fe_executor_join")
+
+
+def fe_executor_destroy(ex: int) -> None:
+    load_library().fe_executor_destroy(ex)
 
 
 def fe_cross_sequence_noalloc(model: int, B: int, K: int, L: int, seq, Cp, stream=None) -> None:
@@ -376,9 +413,10 @@ class Evaluator:
         assert t.numel() * t.element_size() == fe_kv_size(self.handle, B, T)
         return t
 
-    def run(self, x=None, ctx_ids=None, pool=None, lists=None, stream=None) -> Dict:
-        """Enqueue the five calls on device tensors already resident on the GPU."""
-        b = self.buffers
+    def run(self, x=None, ctx_ids=None, pool=None, lists=None, stream=None, buffers=None) -> Dict:
+        """Enqueue the five calls on device tensors already resident on the GPU (into `buffers`, a
+        dict from `allocate`, else the last allocated set)."""
+        b = self.buffers if buffers is None else buffers
         B, T, M, K, L = b["shape"]
         h = self.handle
         fe_encode_context(h, B, T, x, ctx_ids, b["kv"], b["ws"], stream)
@@ -410,3 +448,37 @@ class Evaluator:
         fe_evaluate_naive(self.handle, B, T, M, K, L, x, ctx_ids, pool, lists, b["Cp"], b["scores"], b["best"],
                           b["ws"], stream)
         return b
+
+
+class Executor:
+    """Whole passes of independent batches, round-robin over `n_streams` HIP streams of the
+    library (fe_executor_*).  Give every stream its own buffer set (`Evaluator.allocate`): pass i
+    writes set i mod n_streams, so a set is reused only after n_streams - 1 other passes."""
+
+    def __init__(self, evaluator: "Evaluator", n_streams: int):
+        self.evaluator = evaluator
+        self.n_streams = n_streams
+        self.handle = fe_executor_create(evaluator.handle, n_streams)
+
+    def submit(self, buffers: Dict, x=None, ctx_ids=None, pool=None, lists=None, stream=None) -> Dict:
+        """Enqueue one pass into `buffers` after the work already on `stream` (the inputs')."""
+        b = buffers
+        B, T, M, K, L = b["shape"]
+        fe_executor_submit(self.handle, B, T, M, K, L, x, ctx_ids, pool, lists, b["kv"], b["uniq"], b["n_uniq"],
+                           b["slot"], b["H"], b["seq"], b["Cp"], b["scores"], b["best"], b["ws"], stream)
+        return b
+
+    def join(self, stream=None) -> None:
+        """Make `stream` wait for every submitted pass."""
+        fe_executor_join(self.handle, stream)
+
+    def close(self) -> None:
+        if self.handle:
+            fe_executor_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

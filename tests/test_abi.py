@@ -168,3 +168,13 @@ def test_train_grads_host_checks(case):
     assert st == fe.FE_EINVAL
     msg = fe.load_library().fe_last_error().decode()
     assert {"loss_kind": "loss_kind", "misaligned": "aligned", "small": "workspace", "no_pool": "pool"}[case] in msg
+
+
+def test_executor_host_checks():
+    """The executor's entry points reject NULL handles and arguments before touching the device."""
+    lib = fe.load_library()
+    out = ctypes.c_void_p()
+    assert lib.fe_executor_create(None, 2, ctypes.byref(out)) == fe.FE_EINVAL
+    assert lib.fe_executor_submit(None, None, None) == fe.FE_EINVAL
+    assert lib.fe_executor_join(None, None) == fe.FE_EINVAL
+    lib.fe_executor_destroy(None)
