@@ -521,6 +521,8 @@ def main() -> int:
                     help="skip timing the pass without cross-sequence interaction (for profiler runs)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the K sweep and the long-context / text-hypothesis workloads after the headline run")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="time the headline passes on one stream only (for profiler runs of single kernels)")
     ap.add_argument("--cpu-all", action="store_true",
                     help="also time the oracle (candidate-factorised order, --cpu-seconds each) on every K-sweep "
                          "and long-context / text-hypothesis workload")
@@ -577,27 +579,32 @@ def main() -> int:
     single_ms = evs[0].elapsed_time(evs[-1]) / args.steps
 
     # ---- timed region: K whole passes, each over the full batch, through the pipelined executor
-    # (PIPE_STREAMS batches in flight on the library's streams, one buffer set per stream)
-    pipe_sets = [bufs] + [ev.allocate(c.B, c.T, c.M, c.K, c.L) for _ in range(PIPE_STREAMS - 1)]
-    ex = fe.Executor(ev, PIPE_STREAMS)
+    # (PIPE_STREAMS batches in flight on the library's streams, one buffer set per stream); with
+    # --no-pipeline (profiler runs of single kernels) the one-stream passes are the timed region
+    n_streams = 1 if args.no_pipeline else PIPE_STREAMS
+    pipe_sets = [bufs] + [ev.allocate(c.B, c.T, c.M, c.K, c.L) for _ in range(n_streams - 1)]
+    ex = fe.Executor(ev, n_streams)
 
     def submit(i):
-        ex.submit(pipe_sets[i % PIPE_STREAMS], x=x, ctx_ids=ids, pool=pool, lists=lists)
+        ex.submit(pipe_sets[i % n_streams], x=x, ctx_ids=ids, pool=pool, lists=lists)
 
-    for i in range(max(args.warmup, PIPE_STREAMS)):
-        submit(i)
-    ex.join()
-    torch.cuda.synchronize()
-    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    p0.record(stream)
-    for i in range(args.steps):
-        submit(i)
-    ex.join()
-    p1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = p0.elapsed_time(p1) / args.steps
+    if args.no_pipeline:
+        wall, ms_per_step = None, single_ms
+    else:
+        for i in range(max(args.warmup, n_streams)):
+            submit(i)
+        ex.join()
+        torch.cuda.synchronize()
+        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        p0.record(stream)
+        for i in range(args.steps):
+            submit(i)
+        ex.join()
+        p1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms_per_step = p0.elapsed_time(p1) / args.steps
     lists_per_s = c.B * c.K / (ms_per_step / 1e3)
     ex.close()
     del pipe_sets
@@ -700,11 +707,12 @@ def main() -> int:
                    "B": c.B, "T": c.T, "d": c.d, "M": c.M, "K": c.K, "L": c.L, "parallelism": "none (1 GPU)"},
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
-        "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
-        "pipelined": {"streams": PIPE_STREAMS,
-                      "what": "value and ms_per_step: K passes (each over the whole batch, B requests) submitted "
-                              "round-robin to fe_executor streams, one buffer set per stream, timed between two "
-                              "events around all K; p50/p90: per-pass latency of the same pass alone on one stream"},
+        "wall_ms_per_step": None if wall is None else round(wall * 1e3 / args.steps, 5),
+        "pipelined": None if args.no_pipeline else {
+            "streams": n_streams,
+            "what": "value and ms_per_step: K passes (each over the whole batch, B requests) submitted round-robin "
+                    "to fe_executor streams, one buffer set per stream, timed between two events around all K; "
+                    "p50/p90: per-pass latency of the same pass alone on one stream"},
         "single_stream": {"ms_per_step": round(single_ms, 5), "value": round(c.B * c.K / (single_ms / 1e3), 1)},
         "without_cross_sequence": None if no_cross_ms is None else {
             "ms_per_step": round(no_cross_ms, 5), "value": round(c.B * c.K / (no_cross_ms / 1e3), 1)},
