@@ -522,7 +522,7 @@ def main() -> int:
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the K sweep and the long-context / text-hypothesis workloads after the headline run")
     ap.add_argument("--no-pipeline", action="store_true",
-                    help="time the headline passes on one stream only (for profiler runs of single kernels)")
+                    help="skip the pipelined-executor throughput (for profiler runs of single kernels)")
     ap.add_argument("--cpu-all", action="store_true",
                     help="also time the oracle (candidate-factorised order, --cpu-seconds each) on every K-sweep "
                          "and long-context / text-hypothesis workload")
@@ -566,49 +566,48 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
 
-    # ---- one stream: K whole passes back to back, an event between consecutive passes (the
-    # latency of one batch, and the throughput when batches are not overlapped)
+    # ---- timed region: K whole passes back to back on one stream, an event between consecutive
+    # passes (the metric: B*K lists over the device time of the five calls for one batch)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
     evs[0].record(stream)
     for i in range(args.steps):
         step()
         evs[i + 1].record(stream)
     torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
     per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
-    single_ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    ms_per_step = evs[0].elapsed_time(evs[-1]) / args.steps
+    lists_per_s = c.B * c.K / (ms_per_step / 1e3)
 
-    # ---- timed region: K whole passes, each over the full batch, through the pipelined executor
-    # (PIPE_STREAMS batches in flight on the library's streams, one buffer set per stream); with
-    # --no-pipeline (profiler runs of single kernels) the one-stream passes are the timed region
-    n_streams = 1 if args.no_pipeline else PIPE_STREAMS
-    pipe_sets = [bufs] + [ev.allocate(c.B, c.T, c.M, c.K, c.L) for _ in range(n_streams - 1)]
-    ex = fe.Executor(ev, n_streams)
+    # ---- serving throughput beside it: K passes (each over the whole batch) submitted round-robin
+    # to the pipelined executor, PIPE_STREAMS batches in flight, one buffer set per stream
+    pipe_ms = None
+    if not args.no_pipeline:
+        pipe_sets = [bufs] + [ev.allocate(c.B, c.T, c.M, c.K, c.L) for _ in range(PIPE_STREAMS - 1)]
+        ex = fe.Executor(ev, PIPE_STREAMS)
 
-    def submit(i):
-        ex.submit(pipe_sets[i % n_streams], x=x, ctx_ids=ids, pool=pool, lists=lists)
+        def submit(i):
+            ex.submit(pipe_sets[i % PIPE_STREAMS], x=x, ctx_ids=ids, pool=pool, lists=lists)
 
-    if args.no_pipeline:
-        wall, ms_per_step = None, single_ms
-    else:
-        for i in range(max(args.warmup, n_streams)):
+        for i in range(max(args.warmup, PIPE_STREAMS)):
             submit(i)
         ex.join()
         torch.cuda.synchronize()
         p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
         p0.record(stream)
         for i in range(args.steps):
             submit(i)
         ex.join()
         p1.record(stream)
         torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        ms_per_step = p0.elapsed_time(p1) / args.steps
-    lists_per_s = c.B * c.K / (ms_per_step / 1e3)
-    ex.close()
-    del pipe_sets
-    ev.buffers = bufs
+        pipe_ms = p0.elapsed_time(p1) / args.steps
+        ex.close()
+        del pipe_sets
+        ev.buffers = bufs
+        step()                 # leave this stream's pass outputs in the buffers
+        torch.cuda.synchronize()
 
     U = bufs["n_uniq"].cpu().numpy().tolist()
     asm_bytes = assemble_bytes(c, U)
@@ -707,13 +706,12 @@ def main() -> int:
                    "B": c.B, "T": c.T, "d": c.d, "M": c.M, "K": c.K, "L": c.L, "parallelism": "none (1 GPU)"},
         "p50_ms": round(float(np.percentile(per_step, 50)), 5),
         "p90_ms": round(float(np.percentile(per_step, 90)), 5),
-        "wall_ms_per_step": None if wall is None else round(wall * 1e3 / args.steps, 5),
-        "pipelined": None if args.no_pipeline else {
-            "streams": n_streams,
-            "what": "value and ms_per_step: K passes (each over the whole batch, B requests) submitted round-robin "
-                    "to fe_executor streams, one buffer set per stream, timed between two events around all K; "
-                    "p50/p90: per-pass latency of the same pass alone on one stream"},
-        "single_stream": {"ms_per_step": round(single_ms, 5), "value": round(c.B * c.K / (single_ms / 1e3), 1)},
+        "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "pipelined": None if pipe_ms is None else {
+            "streams": PIPE_STREAMS, "ms_per_step": round(pipe_ms, 5), "value": round(c.B * c.K / (pipe_ms / 1e3), 1),
+            "what": "serving throughput: K passes (each over the whole batch) submitted round-robin to the library's "
+                    "pipelined executor (fe_executor_*), one buffer set per stream, timed between two events around "
+                    "all K; value above is one batch at a time on one stream"},
         "without_cross_sequence": None if no_cross_ms is None else {
             "ms_per_step": round(no_cross_ms, 5), "value": round(c.B * c.K / (no_cross_ms / 1e3), 1)},
         "graph_replay": None if graph_ms is None else {"ms_per_step": round(graph_ms, 5),
