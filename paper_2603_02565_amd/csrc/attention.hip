@@ -231,10 +231,12 @@ __global__ __launch_bounds__(WAVES * 64, WAVES != 4 ? 1 : (DH == 64 && QT >= 2) 
     if (c0 + KC < nk) load_chunk(c0 + KC);
     const int nkeys = min(KC, nk - c0);
 
-    // 64 keys (two 32-key blocks; 32 for 32-key chunks) per online-softmax step; every key and value fragment of them
-    // is read from LDS once and used by all QT query tiles of the wave.  Keys from nkeys on
-    // (zero rows in LDS, up to KC) are masked.
-    constexpr int NU = (KC >= 64 && QT >= 2) ? 2 : 1;   // 32-key blocks per step
+    // 64 keys (two 32-key blocks) per online-softmax step at head width 32 with several query
+    // tiles per wave, else 32 (head width 64: a tile's arithmetic is then the same whatever the
+    // number of tiles per wave); every key and value fragment of a step is read from LDS once and
+    // used by all QT query tiles of the wave.  Keys from nkeys on (zero rows in LDS, up to KC) are
+    // masked.
+    constexpr int NU = (KC >= 64 && QT >= 2 && DH == 32) ? 2 : 1;   // 32-key blocks per step
     static_assert(KC % (32 * NU) == 0, "whole steps per chunk");
     for (int kb = 0; kb < nkeys; kb += 32 * NU) {
       const int r = lane & 15;
@@ -483,14 +485,14 @@ hipError_t launch_bf16(const AttnArgs& a, hipStream_t s) {
   // as many queries per workgroup as still fill the chip, so K/V chunks are shared widely: eight
   // 32-dim query tiles per wave when that makes >= 512 workgroups (two per compute unit, by the
   // variant's registers), four or two when >= 1024 (three per compute unit); two 64-dim tiles
-  // when >= 1024 (four would not fit the register file)
+  // when >= 512 (two per compute unit; four would not fit the register file)
   const long long bh = (long long)a.n_heads * a.B;
   auto wgs = [&](int qt) { return (a.nq + 64 * qt - 1) / (64 * qt) * bh; };
   if constexpr (DH == 32) {
     if (wgs(8) >= 512) return launch_chunked<DH, 4, 8, 128>(a, s);
     if (wgs(4) >= 1024) return launch_chunked<DH, 4, 4, 128>(a, s);
   }
-  if (wgs(2) >= 1024) return launch_chunked<DH, 4, 2, 128>(a, s);
+  if (wgs(2) >= (DH == 64 ? 512 : 1024)) return launch_chunked<DH, 4, 2, 128>(a, s);
   return launch_chunked<DH, 4, 1, 128>(a, s);
 }
 
