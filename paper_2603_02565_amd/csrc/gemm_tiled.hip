@@ -60,21 +60,30 @@ __global__ __launch_bounds__(64 * WM * WN, 2) void k_gemm_tiled(GemmArgs a) {
   const bf16* A = static_cast<const bf16*>(a.A);
   const bf16* W = static_cast<const bf16*>(a.Wt);
   // the copies of stage s: wave w issues copies w, w + NW, ... of the (BM + BN) / 32 * KSS
-  // fragments (A first); copy c lands at buffer (s % NST), offset c KiB
+  // fragments (A first); copy c lands at buffer (s % NST), offset c KiB.  Each copy's source for
+  // stage 0 is formed once; stage s adds s * BK elements (A) or s * KSS fragments (W).
+  const bf16* src0[DPW];
+  bool is_a[DPW];
+#pragma unroll
+  for (int i = 0; i < DPW; ++i) {
+    const int c = wave + NW * i;
+    is_a[i] = c < (BM / 32) * KSS;
+    if (is_a[i]) {
+      const int rb = c / KSS, kk = c % KSS;
+      const int rr = rb * 32 + (lane & 31);
+      const int r = s_valid[rr] ? row0 + rr : row0;
+      src0[i] = A + (long long)r * a.lda + kk * 16 + 8 * (lane >> 5);
+    } else {
+      const int cw = c - (BM / 32) * KSS, nb = cw / KSS, kk = cw % KSS;
+      src0[i] = W + ((long long)(cb0 + nb) * KS + kk) * FRAG + lane * 8;
+    }
+  }
   auto issue = [&](int s) {
     bf16* buf = smem + (s % NST) * ST;
 #pragma unroll
     for (int i = 0; i < DPW; ++i) {
       const int c = wave + NW * i;
-      if (c < (BM / 32) * KSS) {
-        const int rb = c / KSS, kk = c % KSS;
-        const int rr = rb * 32 + (lane & 31);
-        const int r = s_valid[rr] ? row0 + rr : row0;
-        lds_dma16(A + (long long)r * a.lda + s * BK + kk * 16 + 8 * (lane >> 5), buf + c * FRAG);
-      } else {
-        const int cw = c - (BM / 32) * KSS, nb = cw / KSS, kk = cw % KSS;
-        lds_dma16(W + ((long long)(cb0 + nb) * KS + s * KSS + kk) * FRAG + lane * 8, buf + c * FRAG);
-      }
+      lds_dma16(src0[i] + (is_a[i] ? (long long)s * BK : (long long)s * KSS * FRAG), buf + c * FRAG);
     }
   };
   f32x16 acc[RBW][CBW];
