@@ -343,22 +343,24 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
   if (n <= 0) return;                                // uniform over the workgroup
   const int nrb = (n + 31) / 32;
   const int nk = a.T, nkb = (nk + 31) / 32;
-  // Wo fragments of this wave's column block, requested first: their latency hides behind the
-  // staging below
   const int cb = wave & 3, rb0 = wave >> 2;
+  // Every global load of the prologue is issued before any of them is used -- this wave's Wo
+  // fragments, the block's vectors, the head's context keys and values, the attention output rows,
+  // the residual rows -- so their latencies overlap; out-of-range rows and keys read a valid row and
+  // are zeroed when staged.
   bf16x8 wf[KS];
   {
     const bf16x8* W = static_cast<const bf16x8*>(a.wo);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) wf[ks] = W[((long long)cb * KS + ks) * 64 + lane];
   }
-  if (tid < D) {   // the block's vectors, read after the first barrier
+  float4 vec4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (tid < D) {
     const int v = tid / (D / 4), o = (tid % (D / 4)) * 4;
     const float* src = v == 0 ? a.bo : v == 1 ? a.ln2g : v == 2 ? a.ln2b : a.bq;
-    reinterpret_cast<float4*>(s_vec)[tid] = *reinterpret_cast<const float4*>(src + o);
+    vec4 = *reinterpret_cast<const float4*>(src + o);
   }
-
-  // ---- context keys and values of head h: loads issued first, staged in LDS below --------
+  // context keys and values of head h
   constexpr int KV_PER = NR * DH / 8 / NT;           // 16-byte vectors per thread per tensor
   static_assert(KV_PER >= 1, "keys do not split over the workgroup");
   uint4 kr[KV_PER], vr[KV_PER];
@@ -368,52 +370,80 @@ __global__ __launch_bounds__(1024) void k_cross_attention(CrossAttnArgs a) {
 #pragma unroll
     for (int p = 0; p < KV_PER; ++p) {
       const int e = p * NT + tid, key = e / (DH / 8), d0 = (e % (DH / 8)) * 8;
-      const bool ok = key < nk;
-      kr[p] = ok ? *reinterpret_cast<const uint4*>(Kb + (long long)key * D + d0) : make_uint4(0, 0, 0, 0);
-      vr[p] = ok ? *reinterpret_cast<const uint4*>(Vb + (long long)key * D + d0) : make_uint4(0, 0, 0, 0);
+      const long long kk = key < nk ? key : 0;
+      kr[p] = *reinterpret_cast<const uint4*>(Kb + kk * D + d0);
+      vr[p] = *reinterpret_cast<const uint4*>(Vb + kk * D + d0);
     }
   }
-  // ---- attention output rows O (all heads) -> As; rows n .. 32*nrb-1 zero ---------------
+  // attention output rows O (all heads): row r of the group for vector p
   const long long rbase = (long long)b * a.per;
-  for (int e = tid; e < 32 * nrb * (D / 8); e += NT) {
-    const int r = e / (D / 8), c = (e % (D / 8)) * 8;
-    bf16x8 v = {};
-    if (r < n) v = *reinterpret_cast<const bf16x8*>(static_cast<const bf16*>(a.O) + (rbase + r) * D + c);
-    *reinterpret_cast<bf16x8*>(&As[r * LDA + c]) = v;
+  constexpr int O_PER = NR * (D / 8) / NT;
+  uint4 orow[O_PER];
+#pragma unroll
+  for (int p = 0; p < O_PER; ++p) {
+    const int e = p * NT + tid, r = e / (D / 8), c = (e % (D / 8)) * 8;
+    if (r < 32 * nrb)
+      orow[p] = *reinterpret_cast<const uint4*>(static_cast<const bf16*>(a.O) + (rbase + (r < n ? r : 0)) * D + c);
   }
-  // ---- residual rows: wave w holds column block cb = w % 4 of row blocks w/4 and w/4 + 4, in
-  //      the transposed accumulator layout (row rb*32 + lane%32, columns cb*32 + 8q + 4(lane/32) + e)
+  // residual rows: wave w holds column block cb = w % 4 of row blocks w/4 and w/4 + 4, in the
+  // transposed accumulator layout (row rb*32 + lane%32, columns cb*32 + 8q + 4(lane/32) + e)
   const int colq = cb * 32 + 4 * (lane >> 5);       // + 8q
   f32x16 x[2];
+  if (a.xin_f32) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int rb = rb0 + 4 * i, row = rb * 32 + (lane & 31);
-    const bool ok = rb < nrb && row < n;
-    const long long grow = rbase + (ok ? row : 0);
+    for (int i = 0; i < 2; ++i) {
+      const int rb = rb0 + 4 * i, row = rb * 32 + (lane & 31);
+      const bool ok = rb < nrb && row < n;
+      const long long grow = rbase + (ok ? row : 0);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float4 t;
-      if (a.xin_f32) {
-        t = *reinterpret_cast<const float4*>(static_cast<const float*>(a.Xin) + grow * D + colq + 8 * q);
-      } else {
-        const bf16x4 u = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(a.Xin) + grow * D + colq + 8 * q);
-        t = make_float4((float)u[0], (float)u[1], (float)u[2], (float)u[3]);
+      for (int q = 0; q < 4; ++q) {
+        const float4 t = *reinterpret_cast<const float4*>(static_cast<const float*>(a.Xin) + grow * D + colq + 8 * q);
+        x[i][4 * q] = ok ? t.x : 0.f;
+        x[i][4 * q + 1] = ok ? t.y : 0.f;
+        x[i][4 * q + 2] = ok ? t.z : 0.f;
+        x[i][4 * q + 3] = ok ? t.w : 0.f;
       }
-      x[i][4 * q] = ok ? t.x : 0.f;
-      x[i][4 * q + 1] = ok ? t.y : 0.f;
-      x[i][4 * q + 2] = ok ? t.z : 0.f;
-      x[i][4 * q + 3] = ok ? t.w : 0.f;
     }
   }
-  // stage the keys (row-major) and values (transposed); keys nk .. 32*nkb-1 are zero
+  bf16x4 xr[2][4];                                   // bf16 residual rows, converted after the staging
+  if (!a.xin_f32) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int rb = rb0 + 4 * i, row = rb * 32 + (lane & 31);
+      const long long grow = rbase + (rb < nrb && row < n ? row : 0);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        xr[i][q] = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(a.Xin) + grow * D + colq + 8 * q);
+    }
+  }
+  // stage: the vectors, the keys (row-major) and values (transposed; keys nk .. 32*nkb-1 zero),
+  // the O rows (rows n .. 32*nrb-1 zero)
+  if (tid < D) reinterpret_cast<float4*>(s_vec)[tid] = vec4;
 #pragma unroll
   for (int p = 0; p < KV_PER; ++p) {
     const int e = p * NT + tid, key = e / (DH / 8), d0 = (e % (DH / 8)) * 8;
     if (key >= nkb * 32) continue;                   // never read
-    *reinterpret_cast<uint4*>(&Ks[key * QLD + d0]) = kr[p];
+    const bool ok = key < nk;
+    *reinterpret_cast<uint4*>(&Ks[key * QLD + d0]) = ok ? kr[p] : make_uint4(0, 0, 0, 0);
     const bf16* v = reinterpret_cast<const bf16*>(&vr[p]);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) Vt[(d0 + i) * VLD + key] = v[i];
+    for (int i = 0; i < 8; ++i) Vt[(d0 + i) * VLD + key] = ok ? v[i] : (bf16)0.f;
+  }
+#pragma unroll
+  for (int p = 0; p < O_PER; ++p) {
+    const int e = p * NT + tid, r = e / (D / 8), c = (e % (D / 8)) * 8;
+    if (r < 32 * nrb) *reinterpret_cast<uint4*>(&As[r * LDA + c]) = r < n ? orow[p] : make_uint4(0, 0, 0, 0);
+  }
+  if (!a.xin_f32) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int rb = rb0 + 4 * i, row = rb * 32 + (lane & 31);
+      const bool ok = rb < nrb && row < n;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[i][4 * q + e] = ok ? (float)xr[i][q][e] : 0.f;
+    }
   }
   lds_barrier();
 
