@@ -136,6 +136,17 @@ def test_cfg3_long_context():
     check_whole_batch(c, out)
 
 
+@pytest.mark.parametrize("cid", [1, 3])
+def test_linear_attention_every_request(cid):
+    """The linear-attention workloads the bench times (RecSys base, long context), every request:
+    the per-head state that replaces the key/value cache (its key ranges split over workgroups and
+    merged in order), H, the sequences, C', scores and selection."""
+    c = gen.config(cid, attention="linear")
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    check_whole_batch(c, out)
+
+
 def test_cfg4_text_hypotheses():
     c = gen.config(4)
     W, I = gen.make_weights(c), gen.make_inputs(c)
