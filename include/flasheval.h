@@ -322,9 +322,10 @@ fe_status fe_evaluate_naive(const fe_model* m, int B, int T, int M, int K, int L
  *   the kernels are enqueued.  The whole pass is validated first, with the rules of the five
  *   calls (p->ws_bytes >= fe_workspace_size(B, T, M, K, L)); on FE_EINVAL or FE_EUNSUPPORTED
  *   nothing was enqueued (FE_EHIP, a failed launch, may leave the pass's earlier kernels
- *   enqueued, as for the five calls).  A submission must not share any output (kv, uniq, n_uniq, slot, H, seq, Cp,
- *   scores, best) or the workspace with a submission still in flight; one buffer set per stream,
- *   submission i using set i mod n_streams, satisfies this.  Inputs may be shared.
+ *   enqueued, as for the five calls).  A submission must not share any output (kv, uniq,
+ *   n_uniq, slot, H, seq, Cp, scores, best) or the workspace with a submission still in flight;
+ *   one buffer set per stream, submission i using set i mod n_streams, satisfies this.  Inputs
+ *   may be shared.
  * fe_executor_join: makes `stream` wait (on the device) for every pass submitted so far; the
  *   outputs are valid for work enqueued on `stream` after it.
  * fe_executor_destroy: waits on the host for the submitted passes, then releases the streams and
