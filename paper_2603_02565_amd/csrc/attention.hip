@@ -484,15 +484,15 @@ hipError_t launch_bf16(const AttnArgs& a, hipStream_t s) {
   }
   // as many queries per workgroup as still fill the chip, so K/V chunks are shared widely: eight
   // 32-dim query tiles per wave when that makes >= 512 workgroups (two per compute unit, by the
-  // variant's registers), four or two when >= 1024 (three per compute unit); two 64-dim tiles
-  // when >= 512 (two per compute unit; four would not fit the register file)
+  // variant's registers), four when >= 1024 (three per compute unit), two when >= 512; two
+  // 64-dim tiles when >= 512 (two per compute unit; four would not fit the register file)
   const long long bh = (long long)a.n_heads * a.B;
   auto wgs = [&](int qt) { return (a.nq + 64 * qt - 1) / (64 * qt) * bh; };
   if constexpr (DH == 32) {
     if (wgs(8) >= 512) return launch_chunked<DH, 4, 8, 128>(a, s);
     if (wgs(4) >= 1024) return launch_chunked<DH, 4, 4, 128>(a, s);
   }
-  if (wgs(2) >= (DH == 64 ? 512 : 1024)) return launch_chunked<DH, 4, 2, 128>(a, s);
+  if (wgs(2) >= 512) return launch_chunked<DH, 4, 2, 128>(a, s);
   return launch_chunked<DH, 4, 1, 128>(a, s);
 }
 
