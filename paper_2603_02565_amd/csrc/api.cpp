@@ -298,6 +298,7 @@ struct Ws {
   size_t c_xin, c_x, c_qkv, c_o, c_h, c_ln;             // context stage
   size_t i_g0, i_g, i_g1, i_qkv, i_o, i_q, i_h, i_ln;   // item stage
   size_t s_x, s_qkv, s_o, s_h, s_c, s_ln;               // sequence + cross stages
+  size_t c_h_bytes, i_h_bytes, s_h_bytes;               // sizes of the FFN hidden buffers
   // *_ln: wide bf16 models only, bf16 [rows][d] LayerNorm outputs feeding the tiled products
   size_t total;
 };
@@ -333,7 +334,8 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     w.c_x = b.take(R * d * 4);
     w.c_qkv = b.take(R * 3 * d * e);
     w.c_o = b.take(R * d * e);
-    w.c_h = b.take(R * F * e);
+    w.c_h_bytes = std::max((size_t)(R * F * e), post_part_bytes(R, (int)d, (int)F));
+    w.c_h = b.take(w.c_h_bytes);
     if (wide(m)) w.c_ln = b.take(R * d * 2);
     end = std::max(end, b.at);
   }
@@ -347,7 +349,8 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     w.i_qkv = b.take(R * 3 * d * e);
     w.i_o = b.take(R * d * e);
     w.i_q = b.take(R * d * e);
-    w.i_h = b.take(R * F * e);
+    w.i_h_bytes = std::max((size_t)(R * F * e), post_part_bytes(R, (int)d, (int)F));
+    w.i_h = b.take(w.i_h_bytes);
     if (wide(m)) w.i_ln = b.take(R * d * 2);
     end = std::max(end, b.at);
   }
@@ -357,7 +360,8 @@ Ws layout(const fe_model* m, long long B, long long T, long long M, long long K,
     w.s_x = b.take(R * d * 4);
     w.s_qkv = b.take(R * 3 * d * e);
     w.s_o = b.take(R * d * e);
-    w.s_h = b.take(R * F * e);
+    w.s_h_bytes = std::max({(size_t)(R * F * e), post_part_bytes(R, (int)d, (int)F), post_part_bytes(B * K, (int)d, (int)F)});
+    w.s_h = b.take(w.s_h_bytes);
     w.s_c = b.take(B * K * d * 4);
     if (wide(m)) w.s_ln = b.take(R * d * 2);
     end = std::max(end, b.at);
@@ -453,6 +457,7 @@ struct Bufs {
   void* Hf;      // act [rows][F]
   void* ln;      // wide bf16 models: bf16 [rows][d] LayerNorm output (else unused)
   bool xbf = false;   // X holds bf16 (the fused tails of bf16 models write it so between kernels)
+  size_t hf_bytes = 0;   // bytes of Hf (the fused tails borrow it for the partial sums of split FFNs)
 };
 
 // One pre-LN encoder block over nb batches of `per` rows; attention stays inside a batch.
@@ -509,6 +514,8 @@ fe_status enc_block(const fe_model* m, const EncW& w, int nb, int per, const voi
     PostArgs p{b.O, xin, xin_f32, b.X, R, per, nvalid, d, F, 0, w.wo, w.bo, w.ln2g, w.ln2b,
                w.w1, w.b1, w.w2, w.b2, nullptr, nullptr, nullptr};
     p.xout_bf16 = b.xbf;
+    p.part = b.Hf;
+    p.part_bytes = b.hf_bytes;
     if (kvo) {
       p.Xout = nullptr;   // nothing reads the module's residual after its key/value projections
       p.lnfg = kvo->lnf_g;
@@ -614,6 +621,7 @@ fe_status cross_sequence_run(const fe_model* m, int B, int K, int L, const void*
   if (!lin && module_fits(m, K))
     return run_module(m, m->cross, B, K, c, true, m->cross_lnf_g, m->cross_lnf_b, Cp, false, s);
   Bufs bc{c, b.qkv, b.O, b.Hf, b.ln};
+  bc.hf_bytes = b.hf_bytes;
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     st = enc_block(m, m->cross[l], B, K, c, true, bc, nullptr, s, nullptr, lin ? lin_st : nullptr, lin_part);
     if (st != FE_OK) return st;
@@ -658,7 +666,7 @@ fe_status scratch_address(int device, void** out) {
 // What fe_cross_sequence needs of its workspace, packed: the c rows always; SeqEnc's residual and
 // block buffers only when its lists are too long for the module kernel; the block buffers of the
 // cross module only when it runs block by block (K > 64, wide or linear models).
-struct CrossScratch { size_t c, X, qkv, O, Hf, ln, lin_st, lin_part, total; };
+struct CrossScratch { size_t c, X, qkv, O, Hf, ln, lin_st, lin_part, total, hf_bytes; };
 
 CrossScratch cross_scratch_layout(const fe_model* m, long long B, long long K, long long L) {
   const long long d = m->cfg.d, F = m->cfg.ffn_dim, S = L + 1, H = m->cfg.n_heads, dh = d / H;
@@ -673,7 +681,9 @@ CrossScratch cross_scratch_layout(const fe_model* m, long long B, long long K, l
   if (rows > 0) {
     w.qkv = b.take(rows * 3 * d * e);
     w.O = b.take(rows * d * e);
-    w.Hf = b.take(rows * F * e);
+    w.hf_bytes = std::max({(size_t)(rows * F * e), seq_blocks ? post_part_bytes(B * K * S, (int)d, (int)F) : size_t(0),
+                           cross_blocks ? post_part_bytes(B * K, (int)d, (int)F) : size_t(0)});
+    w.Hf = b.take(w.hf_bytes);
     if (wide(m)) w.ln = b.take(rows * d * 2);
   }
   if (lin) {
@@ -880,6 +890,7 @@ fe_status fe_encode_context(const fe_model* m, int B, int T, const void* x, cons
     src = at<char>(ws, w.c_xin);
   }
   Bufs b{at<float>(ws, w.c_x), at<char>(ws, w.c_qkv), at<char>(ws, w.c_o), at<char>(ws, w.c_h), at<char>(ws, w.c_ln)};
+  b.hf_bytes = w.c_h_bytes;
   // linear models: the item layers' keys and values go to the workspace first, and kv receives
   // their per-head state
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
@@ -1022,6 +1033,8 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
                  iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr,
                  last ? m->item_lnf_g : nullptr, last ? m->item_lnf_b : nullptr, last ? H : nullptr};
       p.xout_bf16 = rbf;
+      p.part = Hf;
+      p.part_bytes = w.i_h_bytes;
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }
@@ -1064,6 +1077,8 @@ fe_status fe_encode_items(const fe_model* m, int B, int M, const void* pool, con
                  iw.w1, iw.b1, iw.w2, iw.b2, nullptr, nullptr, nullptr,
                  last ? m->item_lnf_g : nullptr, last ? m->item_lnf_b : nullptr, last ? H : nullptr};
       p.xout_bf16 = rbf;
+      p.part = Hf;
+      p.part_bytes = w.i_h_bytes;
       FE_LAUNCH(F_POST, s, launch_post(p, s));
       continue;
     }
@@ -1099,6 +1114,7 @@ fe_status fe_cross_sequence(const fe_model* m, int B, int K, int L, const void* 
   const Ws w = layout(m, B, 1, 1, K, L);
   if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
   Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h), at<char>(ws, w.s_ln)};
+  b.hf_bytes = w.s_h_bytes;
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
   return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(ws, w.s_c), lin ? at<float>(ws, w.lin_st) : nullptr,
                             lin ? at<float>(ws, w.lin_part) : nullptr, static_cast<hipStream_t>(stream));
@@ -1117,6 +1133,7 @@ fe_status fe_cross_sequence_noalloc(const fe_model* m, int B, int K, int L, cons
   st = scratch_address(m->device, &base);
   if (st != FE_OK) return st;
   Bufs b{at<float>(base, w.X), at<char>(base, w.qkv), at<char>(base, w.O), at<char>(base, w.Hf), at<char>(base, w.ln)};
+  b.hf_bytes = w.hf_bytes;
   const bool lin = m->cfg.attention == FE_ATTN_LINEAR;
   return cross_sequence_run(m, B, K, L, seq, Cp, b, at<float>(base, w.c), lin ? at<float>(base, w.lin_st) : nullptr,
                             lin ? at<float>(base, w.lin_part) : nullptr, static_cast<hipStream_t>(stream));
@@ -1131,6 +1148,7 @@ fe_status fe_encode_sequences(const fe_model* m, int B, int K, int L, const void
   const Ws w = layout(m, B, 1, 1, K, L);
   if (ws_bytes < w.total) return fail(FE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, w.total);
   Bufs b{at<float>(ws, w.s_x), at<char>(ws, w.s_qkv), at<char>(ws, w.s_o), at<char>(ws, w.s_h), at<char>(ws, w.s_ln)};
+  b.hf_bytes = w.s_h_bytes;
   return seq_encode(m, B, K, L, seq, C, b, static_cast<hipStream_t>(stream));
 }
 

@@ -188,6 +188,10 @@ struct PostArgs {
   const void* wkv; const float* bkv; void* kv; int kv_layers;
   int32_t* zero; int zero_n;            // zero[0 .. zero_n) is cleared (or nullptr)
   int xout_bf16;                        // Xout is bf16 (else fp32)
+  // tail 0 without kv: scratch of part_bytes bytes (16-byte aligned) that lets a launch with few
+  // row tiles split the FFN's hidden width over several workgroups per tile (fp32 partial sums
+  // [parts][R][D], added in a fixed order by a second kernel); nullptr: one workgroup per tile
+  void* part; size_t part_bytes;
 };
 
 // Device pointers of one pre-LN encoder block (matrices of bf16 models in packed fragment order).
@@ -215,6 +219,10 @@ struct ModuleArgs {
 int module_small_tile_rows(int d);
 hipError_t launch_module_small(ModuleArgs a, hipStream_t s);
 hipError_t launch_post(const PostArgs& a, hipStream_t s);
+// workgroups per row tile of a tail launch of R rows whose FFN is split by hidden width, and the
+// bytes of the fp32 partial sums it needs in PostArgs::part (0 when it is not split)
+int post_split_parts(long long R, int D, int F);
+size_t post_part_bytes(long long R, int D, int F);
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_model, hipStream_t s);   // fp32 models
 hipError_t launch_proj(const GemmArgs& a, hipStream_t s);                    // bf16 models, K = d
 // bf16 models with d >= 256: 128 x 128 tiles, LDS-staged operands; A bf16 without LayerNorm

@@ -2,8 +2,9 @@
 //
 // Layout choices for CDNA4:
 //  * A workgroup owns TM consecutive rows and one slab of NCB 32-column blocks (grid.y walks
-//    the slabs): the q|k|v projection is one slab of 3D columns, the key/value cache of all
-//    item layers n slabs of 2D columns.  Every input row is read once per slab and normalised
+//    the slabs): the q|k|v projection is one slab of 3D columns (two, three or six narrower
+//    slabs when the launch has few row tiles), the key/value cache of all item layers n slabs
+//    of 2D columns.  Every input row is read once per slab and normalised
 //    once (LayerNorm statistics in fp32, two passes over values held in registers); the
 //    normalised tile lives in LDS as bf16 for the whole k loop.
 //  * Weights are pre-packed in the fragment order of v_mfma_f32_32x32x16_bf16 (see
@@ -46,11 +47,37 @@ __global__ __launch_bounds__(WG, 2) void k_proj(GemmArgs a) {
   });
 }
 
+// q|k|v columns per workgroup: all 3D, or, for launches with few row tiles, a slab of 3D/S (S of 6,
+// 3 or 2, at most 512 workgroups in all) so that more compute units share the weight stream.
+// Every output element is formed the same way whatever the slab width.
+template <int TM, int D, int NB>
+void launch_qkv(const GemmArgs& a, unsigned tiles, hipStream_t s) {
+  if constexpr (NB % 6 == 0 && (NB / 6) % 4 == 0) {
+    if (tiles * 6 <= 512) {
+      hipLaunchKernelGGL((k_proj<TM, D, NB / 6>), dim3(tiles, 6), dim3(WG), 0, s, a);
+      return;
+    }
+  }
+  if constexpr (NB % 3 == 0 && (NB / 3) % 4 == 0) {
+    if (tiles * 3 <= 512) {
+      hipLaunchKernelGGL((k_proj<TM, D, NB / 3>), dim3(tiles, 3), dim3(WG), 0, s, a);
+      return;
+    }
+  }
+  if constexpr (NB % 2 == 0 && (NB / 2) % 4 == 0) {
+    if (tiles * 2 <= 512) {
+      hipLaunchKernelGGL((k_proj<TM, D, NB / 2>), dim3(tiles, 2), dim3(WG), 0, s, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((k_proj<TM, D, NB>), dim3(tiles, 1), dim3(WG), 0, s, a);
+}
+
 template <int TM, int D>
 hipError_t launch_proj_d(const GemmArgs& a, hipStream_t s) {
   const unsigned tiles = (a.R + TM - 1) / TM;
   if (a.N == 3 * D) {
-    hipLaunchKernelGGL((k_proj<TM, D, 3 * D / 32>), dim3(tiles, 1), dim3(WG), 0, s, a);
+    launch_qkv<TM, D, 3 * D / 32>(a, tiles, s);
   } else if (a.N % (2 * D) == 0) {
     hipLaunchKernelGGL((k_proj<TM, D, 2 * D / 32>), dim3(tiles, a.N / (2 * D)), dim3(WG), 0, s, a);
   } else {

@@ -342,18 +342,20 @@ struct FfnStream {
     if (t + 1 < NS) load(c, t + 1);
     else if (c + 1 < nchunks) load(c + 1, 0);
   }
-  FE_DEV void start(const void* w1p, const void* w2p, int f) {
+  // c0: the first hidden chunk this tile streams (its first stage is requested here)
+  FE_DEV void start(const void* w1p, const void* w2p, int f, int c0 = 0) {
     const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3), lane = threadIdx.x & 63;
     F = f;
     W1l = reinterpret_cast<const bf16x8*>(w1p) + (long long)wave * KS * 64 + lane;
     W2l = reinterpret_cast<const bf16x8*>(w2p) + (long long)wave * (f / 16) * 64 + lane;
-    load(0, 0);
+    load(c0, 0);
   }
+  // x += the FFN's contribution of hidden chunks [c0, c1) (c1 < 0: through the last chunk)
   template <class Acc>
-  FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x) {
+  FE_DEV void run(const bf16* As, bf16* Hs, const float* b1, Acc& x, int c0 = 0, int c1 = -1) {
     const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
-    const int nchunks = F / HC;
-    for (int c = 0; c < nchunks; ++c) chunk(c, nchunks, As, Hs, b1, x, lane, wave);
+    const int nchunks = c1 < 0 ? F / HC : c1;
+    for (int c = c0; c < nchunks; ++c) chunk(c, nchunks, As, Hs, b1, x, lane, wave);
   }
   template <class Acc>
   FE_DEV void chunk(int c, int nchunks, const bf16* As, bf16* Hs, const float* b1, Acc& x, int lane, int wave) {
@@ -811,9 +813,13 @@ __global__ __launch_bounds__(WG, 2) void k_post(PostArgs a) {
   Resid<TM, D> x;
   resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
   FfnOf<TM, D, NCH> ffn;
-  if constexpr (TAIL == 0) ffn.start(a.w1, a.w2, a.F);
+  // at D = 256 the first FFN stage is requested after the Wo product: held across it, its
+  // registers would push the product's operands and accumulators into scratch
+  constexpr bool early = D < 256;
+  if constexpr (TAIL == 0 && early) ffn.start(a.w1, a.w2, a.F);
   lds_barrier();
   go.run(As, LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, a.bo); });
+  if constexpr (TAIL == 0 && !early) ffn.start(a.w1, a.w2, a.F);
   ColGemm<TM, D, D / 32> gq;
   if constexpr (TAIL == 1) gq.start(a.wq);
   // LN2 -> As (the barrier inside the statistics retires every read of As by the Wo product)
@@ -924,9 +930,128 @@ hipError_t launch_module_t(const ModuleArgs& a, hipStream_t s) {
   return launch_module_c<TM, D, DH, false, 1>(a, s);
 }
 
+// The tail of TAIL 0 (no key/value projections) for launches with few row tiles, split by the
+// FFN's hidden width over `parts` workgroups per tile so that the weight streams of a tile run on
+// several compute units at once.  Workgroup (tile, p) forms x1 = Xin + O Wo + bo and LN2(x1) as
+// k_post does, then only hidden chunks [p n / parts, (p + 1) n / parts) of the n, and writes its
+// fp32 sums of the tile's valid rows to slab p of a.part ([parts][R][D]): slab 0 holds x1 plus its
+// chunks, every other slab its chunks alone.  k_post_reduce finishes the tail.
+template <int TM, int D>
+__global__ __launch_bounds__(WG, 2) void k_post_part(PostArgs a, int parts) {
+  constexpr int LDA = D + APAD, HS_BYTES = 2 * TM * HLD * 2;
+  __shared__ __attribute__((aligned(16))) bf16 As[TM * LDA];
+  __shared__ __attribute__((aligned(16))) bf16 Hs[HS_BYTES / 2];
+  __shared__ __attribute__((aligned(16))) float2 s_stat[4 * TM];
+  __shared__ int s_valid[TM];
+  const int id = xcd_tile(blockIdx.x, gridDim.x);          // the parts of a tile share an XCD
+  const int tile = id / parts, p = id % parts;
+  const int row0 = tile * TM;
+  if (!mark_rows<TM>(row0, a.R, a.nvalid, a.rows_per_batch, s_valid)) return;
+  const int nch = a.F / HC, c0 = p * nch / parts, c1 = (p + 1) * nch / parts;
+  ColGemm<TM, D, D / 32> go;
+  go.start(a.wo);
+  stage_rows<TM, D>(a.O, false, D, row0, s_valid, nullptr, nullptr, As);
+  Resid<TM, D> x;
+  resid_load<TM, D>(x, a.Xin, a.xin_f32, row0, s_valid);
+  FfnStream<TM, D> ffn;
+  constexpr bool early = D < 256;                           // as in k_post
+  if constexpr (early) ffn.start(a.w1, a.w2, a.F, c0);
+  lds_barrier();
+  go.run(As, LDA, [&](int jj, int, int rb, const f32x16& acc) { resid_add<TM, D>(x, jj, rb, acc, a.bo); });
+  if constexpr (!early) ffn.start(a.w1, a.w2, a.F, c0);
+  // LN2 -> As (the barrier inside the statistics retires every read of As by the Wo product)
+  resid_ln_to_lds<TM, D>(x, a.ln2g, a.ln2b, s_stat, As);
+  lds_barrier();
+  if (p > 0) {
+#pragma unroll
+    for (int j = 0; j < D / 128; ++j)
+#pragma unroll
+      for (int rb = 0; rb < TM / 32; ++rb) x.v[j][rb] = f32x16{};
+  }
+  ffn.run(As, Hs, a.b1, x, c0, c1);
+  resid_store<TM, D>(x, static_cast<float*>(a.part) + (long long)p * a.R * D, false, row0, s_valid);
+}
+
+// Second half of the split tail, one wave per row: x2 = slab 0 + slab 1 + ... (in that order) + b2
+// -> Xout (fp32 or bf16); when Hout is set, Hout = LNf(x2) in bf16.  Padding rows are not read;
+// their Hout rows become zeros.
+template <int D, int PARTS>
+__global__ __launch_bounds__(WG) void k_post_reduce(PostArgs a) {
+  constexpr int NV = D / 64;                                 // consecutive columns per lane
+  typedef float vecf __attribute__((ext_vector_type(NV)));
+  const int lane = threadIdx.x & 63;
+  const long long r = (long long)blockIdx.x * (WG / 64) + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  const int c = lane * NV;
+  const bool ok = !a.nvalid || (r % a.rows_per_batch) < a.nvalid[r / a.rows_per_batch];
+  if (!ok) {
+    if (a.Hout) {
+#pragma unroll
+      for (int e = 0; e < NV; ++e) static_cast<bf16*>(a.Hout)[r * D + c + e] = (bf16)0.f;
+    }
+    return;
+  }
+  const float* P = static_cast<const float*>(a.part) + r * D + c;
+  const long long slab = (long long)a.R * D;
+  vecf t[PARTS];
+#pragma unroll
+  for (int q = 0; q < PARTS; ++q) t[q] = *reinterpret_cast<const vecf*>(P + q * slab);
+  vecf v = t[0];
+#pragma unroll
+  for (int q = 1; q < PARTS; ++q) v += t[q];
+  const vecf b2 = *reinterpret_cast<const vecf*>(a.b2 + c);
+  v += b2;
+  if (a.Xout) {
+    if (a.xout_bf16) {
+      bf16* y = static_cast<bf16*>(a.Xout) + r * D + c;
+#pragma unroll
+      for (int e = 0; e < NV; ++e) y[e] = (bf16)v[e];
+    } else {
+      *reinterpret_cast<vecf*>(static_cast<float*>(a.Xout) + r * D + c) = v;
+    }
+  }
+  if (a.Hout) {
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < NV; ++e) sum += v[e];
+    const float mu = wave_sum(sum) * (1.f / D);
+    float m2 = 0.f;
+#pragma unroll
+    for (int e = 0; e < NV; ++e) m2 += (v[e] - mu) * (v[e] - mu);
+    const float rstd = rsqrtf(wave_sum(m2) * (1.f / D) + 1e-5f), nm = -mu * rstd;
+    const vecf g = *reinterpret_cast<const vecf*>(a.lnfg + c), b = *reinterpret_cast<const vecf*>(a.lnfb + c);
+    bf16* h = static_cast<bf16*>(a.Hout) + r * D + c;
+#pragma unroll
+    for (int e = 0; e < NV; ++e) h[e] = (bf16)fmaf(fmaf(v[e], rstd, nm), g[e], b[e]);
+  }
+}
+
+// Workgroups per row tile of a TAIL 0 launch without key/value projections (0: the scratch the
+// caller lent is missing, too small or misaligned).
+template <int TM, int D>
+int post_parts(const PostArgs& a) {
+  if (a.tail != 0 || a.kv) return 1;
+  const int parts = post_split_parts(a.R, D, a.F);
+  if (parts == 1) return 1;
+  if (!a.part || (reinterpret_cast<uintptr_t>(a.part) & 15) || a.part_bytes < post_part_bytes(a.R, D, a.F)) return 0;
+  return parts;
+}
+
 template <int TM, int D>
 hipError_t launch_post_t(const PostArgs& a, hipStream_t s) {
   dim3 grid((a.R + TM - 1) / TM);
+  const int parts = post_parts<TM, D>(a);
+  if (parts == 0) return hipErrorInvalidValue;
+  if (parts > 1) {
+    hipLaunchKernelGGL((k_post_part<TM, D>), dim3(grid.x * parts), dim3(WG), 0, s, a, parts);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 rgrid((a.R + WG / 64 - 1) / (WG / 64));
+    if (parts == 2) hipLaunchKernelGGL((k_post_reduce<D, 2>), rgrid, dim3(WG), 0, s, a);
+    else if (parts == 4) hipLaunchKernelGGL((k_post_reduce<D, 4>), rgrid, dim3(WG), 0, s, a);
+    else hipLaunchKernelGGL((k_post_reduce<D, 8>), rgrid, dim3(WG), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.tail == 1) hipLaunchKernelGGL((k_post<TM, D, 1, 0>), grid, dim3(WG), 0, s, a);
   else if (D == 128 && a.F == 4 * D) hipLaunchKernelGGL((k_post<TM, D, 0, (D == 128 ? 4 : 0)>), grid, dim3(WG), 0, s, a);
   else hipLaunchKernelGGL((k_post<TM, D, 0, 0>), grid, dim3(WG), 0, s, a);
@@ -954,6 +1079,23 @@ hipError_t launch_module_small(ModuleArgs a, hipStream_t s) {
 }
 
 // d >= 512 models take the tiled products instead of the fused tails
+// A power of two up to 8 that divides the FFN's chunk count when the launch has few row tiles (at
+// most 256 workgroups in all), else 1.  A function of the shape alone, so that every caller of a
+// shape sums the partial results in the same order.
+int post_split_parts(long long R, int D, int F) {
+  if (D != 128 && D != 256) return 1;
+  const long long tiles = (R + 63) / 64, nch = F / HC;
+  if (F % HC) return 1;
+  for (int p = 8; p >= 2; p /= 2)
+    if (nch % p == 0 && tiles * p <= 256) return p;
+  return 1;
+}
+
+size_t post_part_bytes(long long R, int D, int F) {
+  const int p = post_split_parts(R, D, F);
+  return p > 1 ? (size_t)p * R * D * 4 : 0;
+}
+
 hipError_t launch_post(const PostArgs& a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
   switch (a.D) {
