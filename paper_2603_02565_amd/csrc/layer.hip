@@ -1078,7 +1078,6 @@ hipError_t launch_module_small(ModuleArgs a, hipStream_t s) {
   }
 }
 
-// d >= 512 models take the tiled products instead of the fused tails
 // A power of two up to 8 that divides the FFN's chunk count when the launch has few row tiles (at
 // most 256 workgroups in all), else 1.  A function of the shape alone, so that every caller of a
 // shape sums the partial results in the same order.
@@ -1096,6 +1095,7 @@ size_t post_part_bytes(long long R, int D, int F) {
   return p > 1 ? (size_t)p * R * D * 4 : 0;
 }
 
+// d >= 512 models take the tiled products instead of the fused tails
 hipError_t launch_post(const PostArgs& a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
   switch (a.D) {
