@@ -94,7 +94,9 @@ hipError_t launch_proj(const GemmArgs& a, hipStream_t s) {
   if (a.epi != EPI_STORE || a.c_f32 || !a.bias || a.col_block % 32) return hipErrorInvalidValue;
   switch (a.K) {
     case 128: return launch_proj_d<32, 128>(a, s);
-    case 256: return launch_proj_d<32, 256>(a, s);
+    // 64-row tiles once they fill every workgroup slot: each weight fragment then feeds two row
+    // blocks, halving the weight stream per row
+    case 256: return a.R >= 512 * 64 ? launch_proj_d<64, 256>(a, s) : launch_proj_d<32, 256>(a, s);
     case 512: return launch_proj_d<32, 512>(a, s);
     default: return hipErrorInvalidValue;
   }
