@@ -164,6 +164,16 @@ template <typename T, int NC>
 FE_DEV void ln_row_wide(const void* X, int x_f32, long long x_rs, int r, const float* g, const float* b, void* Y,
                         int y_f32, long long y_rs, bool valid, int lane) {
   constexpr int D = 512 * NC;
+  // gains and offsets are requested with the row, so their latency overlaps the row's
+  float4 gv[NC][2], bv[NC][2];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int k = c * 512 + lane * 8;
+    gv[c][0] = *reinterpret_cast<const float4*>(g + k);
+    gv[c][1] = *reinterpret_cast<const float4*>(g + k + 4);
+    bv[c][0] = *reinterpret_cast<const float4*>(b + k);
+    bv[c][1] = *reinterpret_cast<const float4*>(b + k + 4);
+  }
   float v[8 * NC];
   float sum = 0.f;
 #pragma unroll
@@ -190,8 +200,7 @@ FE_DEV void ln_row_wide(const void* X, int x_f32, long long x_rs, int r, const f
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int k = c * 512 + lane * 8;
-    const float4 g0 = *reinterpret_cast<const float4*>(g + k), g1 = *reinterpret_cast<const float4*>(g + k + 4);
-    const float4 b0 = *reinterpret_cast<const float4*>(b + k), b1 = *reinterpret_cast<const float4*>(b + k + 4);
+    const float4 g0 = gv[c][0], g1 = gv[c][1], b0 = bv[c][0], b1 = bv[c][1];
     const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
     const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
     float y[8];
@@ -214,8 +223,10 @@ FE_DEV void ln_row_wide(const void* X, int x_f32, long long x_rs, int r, const f
   }
 }
 
-// One wave per row: Y = LN(X), padding rows (per nvalid) written as zeros.
-template <typename T>
+// One wave per row: Y = LN(X), padding rows (per nvalid) written as zeros.  NC > 0: d = 512 NC
+// (ln_row_wide); NC = 0: any d <= 1024.  Separate instances, so that the general form's registers
+// do not lower the occupancy of the wide one.
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void k_layernorm(const void* X, int x_f32, long long x_rs, int R, int d,
                                                    const float* g, const float* b, void* Y, int y_f32,
                                                    long long y_rs, const int32_t* nvalid, int rpb) {
@@ -223,34 +234,46 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* X, int x_f32, lon
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= R) return;
   const bool valid = !nvalid || (r % rpb) < nvalid[r / rpb];
-  if (d == 512) {
-    ln_row_wide<T, 1>(X, x_f32, x_rs, r, g, b, Y, y_f32, y_rs, valid, lane);
+  if constexpr (NC > 0) {
+    ln_row_wide<T, NC>(X, x_f32, x_rs, r, g, b, Y, y_f32, y_rs, valid, lane);
     return;
   }
-  if (d == 1024) {
-    ln_row_wide<T, 2>(X, x_f32, x_rs, r, g, b, Y, y_f32, y_rs, valid, lane);
-    return;
-  }
+  // up to four 4-column groups per lane (d <= 1024), all loads -- the row, the gains and the
+  // offsets -- requested before the first use; compile-time indices keep everything in registers
   float vals[16];
-  int nv = 0;
+  float4 gv[4], bv[4];
   float sum = 0.f;
   x_f32 = x_f32 || sizeof(T) == 4;
   const size_t xs = x_f32 ? 4 : sizeof(T);
   const char* xr = static_cast<const char*>(X) + (size_t)r * x_rs * xs;
-  for (int k = lane * 4; k < d; k += 256) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int k = lane * 4 + c * 256;
+    if (k >= d) continue;
     float v4[4];
     load4(xr + (size_t)k * xs, x_f32, v4);
-    for (int j = 0; j < 4; ++j) { vals[nv * 4 + j] = v4[j]; sum += v4[j]; }
-    ++nv;
+    gv[c] = *reinterpret_cast<const float4*>(g + k);
+    bv[c] = *reinterpret_cast<const float4*>(b + k);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { vals[c * 4 + j] = v4[j]; sum += v4[j]; }
   }
   const float mean = wave_sum(sum) / (float)d;
   float sq = 0.f;
-  for (int t = 0; t < nv * 4; ++t) { const float dl = vals[t] - mean; sq += dl * dl; }
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    if (lane * 4 + c * 256 >= d) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { const float dl = vals[c * 4 + j] - mean; sq += dl * dl; }
+  }
   const float rstd = rsqrtf(wave_sum(sq) / (float)d + 1e-5f);
-  nv = 0;
-  for (int k = lane * 4; k < d; k += 256, ++nv) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int k = lane * 4 + c * 256;
+    if (k >= d) continue;
+    const float gg[4] = {gv[c].x, gv[c].y, gv[c].z, gv[c].w}, bb[4] = {bv[c].x, bv[c].y, bv[c].z, bv[c].w};
     float y[4];
-    for (int j = 0; j < 4; ++j) y[j] = valid ? (vals[nv * 4 + j] - mean) * rstd * g[k + j] + b[k + j] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = valid ? (vals[c * 4 + j] - mean) * rstd * gg[j] + bb[j] : 0.f;
     if (y_f32) {
       *reinterpret_cast<float4*>(static_cast<float*>(Y) + (size_t)r * y_rs + k) = make_float4(y[0], y[1], y[2], y[3]);
     } else {
@@ -276,11 +299,18 @@ hipError_t launch_layernorm_masked(const void* X, int x_f32, long long x_rs, int
                                    const float* b, void* Y, int y_f32, long long y_rs, const int32_t* nvalid,
                                    int rpb, bool bf16_model, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  dim3 grid((R + 3) / 4);
-  if (bf16_model)
-    hipLaunchKernelGGL(k_layernorm<bf16>, grid, dim3(256), 0, s, X, x_f32, x_rs, R, d, g, b, Y, y_f32, y_rs, nvalid, rpb);
-  else
-    hipLaunchKernelGGL(k_layernorm<float>, grid, dim3(256), 0, s, X, x_f32, x_rs, R, d, g, b, Y, y_f32, y_rs, nvalid, rpb);
+  if (d > 1024 || d % 4) return hipErrorInvalidValue;
+  const dim3 grid((R + 3) / 4);
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, X, x_f32, x_rs, R, d, g, b, Y, y_f32, y_rs, nvalid, rpb); };
+  if (bf16_model) {
+    if (d == 512) go(k_layernorm<bf16, 1>);
+    else if (d == 1024) go(k_layernorm<bf16, 2>);
+    else go(k_layernorm<bf16, 0>);
+  } else {
+    if (d == 512) go(k_layernorm<float, 1>);
+    else if (d == 1024) go(k_layernorm<float, 2>);
+    else go(k_layernorm<float, 0>);
+  }
   return hipGetLastError();
 }
 
