@@ -173,6 +173,19 @@ def test_wide_heads_two_query_tiles_per_wave():
     check_whole_batch(c, out, requests=[0, c.B - 1])
 
 
+@pytest.mark.parametrize("cid,B", [(1, 2), (1, 24), (3, 6)])
+def test_tails_split_by_hidden_width(cid, B):
+    """Tails of launches with few 64-row tiles run as several workgroups per tile, each over a
+    slice of the FFN's hidden chunks, with the fp32 partial sums added in a fixed order by a second
+    kernel: d = 128 at two requests (context and item tails in four parts), at 24 requests (two
+    parts), and d = 256 at six requests (item tails in four parts, cross-sequence tails in eight).
+    First and last request against the oracle, stage by stage."""
+    c = gen.config(cid, B=B)
+    W, I = gen.make_weights(c), gen.make_inputs(c)
+    out = run_pass(c, W, I)
+    check_whole_batch(c, out, requests=[0, c.B - 1])
+
+
 # ------------------------------------------------------------------------- stage-isolated parity
 
 @pytest.mark.parametrize("cid,ffn", [(1, 256), (1, 768), (3, 512)])
