@@ -171,8 +171,16 @@ __global__ __launch_bounds__(256) void k_lin_merge(const float* __restrict__ par
   for (long long i = blockIdx.x * 256ll + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
     const long long bh = i / per_bh, x = i - bh * per_bh;
     const float* p = part + bh * nsplit * per_bh + x;
-    float s = p[0];
-    for (int sp = 1; sp < nsplit; ++sp) s += p[sp * per_bh];
+    // eight loads in flight at a time; the sum still runs in split order
+    float s = 0.f;
+    for (int sp0 = 0; sp0 < nsplit; sp0 += 8) {
+      float t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = sp0 + u < nsplit ? p[(long long)(sp0 + u) * per_bh] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (sp0 + u < nsplit) s = sp0 + u == 0 ? t[u] : s + t[u];
+    }
     St[i] = s;
   }
 }
@@ -191,20 +199,25 @@ __global__ __launch_bounds__(256) void k_lin_apply(const T* __restrict__ Q, int 
   __shared__ __attribute__((aligned(16))) float s_st[(DH + 1) * DH];
   const int id = xcd_tile(blockIdx.x, gridDim.x);
   const int tile = id % tiles, bh = id / tiles, h = bh % H, b = bh / H;
+  // the query row (any row below rpb: its address needs no valid count), the valid count and the
+  // state are all requested before the first of them is used
+  const int r = tile * RPB + threadIdx.x / TPR, c = (threadIdx.x % TPR) * 8;
+  const T* qrow = Q + ((long long)b * rpb + (r < rpb ? r : 0)) * q_rs + h * DH;
+  constexpr int QV = DH * (int)sizeof(T) / 16;               // 16-byte vectors of the row
+  uint4 qv[QV];
+#pragma unroll
+  for (int i = 0; i < QV; ++i) qv[i] = reinterpret_cast<const uint4*>(qrow)[i];
+  const int n = nvalid ? min(rpb, nvalid[b]) : rpb;
   const float* src = St + (long long)bh * (DH + 1) * DH;
   for (int x = threadIdx.x; x < (DH + 1) * DH / 4; x += 256)
     reinterpret_cast<float4*>(s_st)[x] = reinterpret_cast<const float4*>(src)[x];
-  const int n = nvalid ? min(rpb, nvalid[b]) : rpb;
-  const int r = tile * RPB + threadIdx.x / TPR, c = (threadIdx.x % TPR) * 8;
   const bool live = r < n;
   float fq[DH];
-  const T* qrow = Q + ((long long)b * rpb + (live ? r : 0)) * q_rs + h * DH;
 #pragma unroll
-  for (int i = 0; i < DH; i += 16 / (int)sizeof(T)) {
-    const uint4 t = *reinterpret_cast<const uint4*>(qrow + i);
-    const T* e = reinterpret_cast<const T*>(&t);
+  for (int i = 0; i < QV; ++i) {
+    const T* e = reinterpret_cast<const T*>(&qv[i]);
 #pragma unroll
-    for (int k = 0; k < 16 / (int)sizeof(T); ++k) fq[i + k] = phi(to_f32(e[k]));
+    for (int k = 0; k < 16 / (int)sizeof(T); ++k) fq[i * (16 / (int)sizeof(T)) + k] = phi(to_f32(e[k]));
   }
   __syncthreads();
   if (!live) return;
